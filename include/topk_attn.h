@@ -1,0 +1,172 @@
+/*
+ * topk_attn.h -- C ABI of the MI355X (gfx950) top-k attention library.
+ *
+ * The library computes the forward pass of top-k attention (arXiv 2106.06899,
+ * Section 2.2, Eq. 4):
+ *
+ *     out = activation( top-k( Q K^T ) ) V
+ *
+ * row by row: each query keeps the k keys with the largest raw scores q.k_j,
+ * an activation runs over those k survivors only, and the k matching value rows
+ * are summed with the resulting weights. Queries are processed in chunks of
+ * `chunk` rows (Section 2.2, "Query chunking"); the chunk size bounds the
+ * working memory and never changes the result.
+ *
+ * Conventions shared by every call:
+ *  - Every tensor pointer is a caller-owned DEVICE pointer to contiguous row-major
+ *    data, 16-byte aligned. The library never frees caller memory.
+ *  - dtype is TOPK_F32 or TOPK_BF16 for all of a call's tensors; scores are
+ *    accumulated in fp32; outputs are stored in the input dtype (bf16 is rounded
+ *    to nearest-even).
+ *  - Calls validate their arguments synchronously; on any error they return a
+ *    negative status, launch nothing and leave `out` untouched. On success all
+ *    work is enqueued on `hip_stream` (a hipStream_t; NULL = the null stream) and
+ *    the call returns without waiting.
+ *  - Selection order: (score desc, key index asc); among equal scores the lower
+ *    key index is kept. Inputs are assumed finite.
+ *  - Working memory: either the buffer registered with topk_set_workspace() on
+ *    the calling thread, or (when none is registered) stream-ordered memory the
+ *    library allocates and frees on `hip_stream`.
+ *  - Calls on different streams are safe if they use different workspaces.
+ */
+#ifndef TOPK_ATTN_H
+#define TOPK_ATTN_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+/* element types */
+#define TOPK_F32 0
+#define TOPK_BF16 1
+
+/* status codes */
+#define TOPK_OK 0
+#define TOPK_E_INVAL -1       /* a size, k, chunk, scale, flag or dtype is out of range */
+#define TOPK_E_NULL -2        /* a required pointer is NULL */
+#define TOPK_E_ALIGN -3       /* a tensor pointer is not 16-byte aligned */
+#define TOPK_E_UNSUPPORTED -4 /* valid arguments outside what this build implements */
+#define TOPK_E_NOMEM -5       /* the registered workspace is too small / allocation failed */
+#define TOPK_E_HIP -6         /* a HIP runtime call or kernel launch failed */
+
+/*
+ * topk_attn -- top-k attention (Eq. 4 with softmax; temperature of Eq. 1; causal
+ * mask of Eq. 2), for B*H independent heads (Section 2.1, multi-head attention).
+ *
+ *   Q   [B, H, Lq, d]   queries
+ *   K   [B, H, Lk, d]   keys
+ *   V   [B, H, Lk, d]   values
+ *   out [B, H, Lq, d]   written: out[i] = sum_{j in S_i} w_ij V[j], with S_i the
+ *                       k_eff = min(k, #valid keys) keys of largest q_i.k_j and
+ *                       w_ij = exp(scale*(s_ij - max_S s)) / sum_S exp(...)
+ *   k       1 <= k <= Lk
+ *   chunk   query chunk size C >= 1 (0 = library default); result-neutral
+ *   causal  0 or 1; with 1, key j is valid for query i iff j <= i (0-based)
+ *   scale   1/lambda of Eq. 1, finite and > 0; used only inside the softmax
+ *           (selection uses the raw score, which is invariant to scale > 0)
+ *   dtype   TOPK_F32 or TOPK_BF16; d must be a multiple of 8 and <= 1024
+ */
+int topk_attn(const void* Q, const void* K, const void* V, void* out,
+              int64_t B, int64_t H, int64_t Lq, int64_t Lk, int64_t d,
+              int64_t k, int64_t chunk, int causal, float scale,
+              int dtype, void* hip_stream);
+
+/*
+ * topk_ffn -- the feed-forward layer recast as attention (Eq. 3) with the top-k
+ * of Eq. 4 and a ReLU activation: out[i] = sum_{j in S_i} max(x_i.W1[j], 0) W2[j],
+ * where S_i holds the k largest scores x_i.W1[j]. No bias, no temperature; ReLU
+ * applies after selection, so negative survivors are selected with weight 0.
+ *
+ *   X   [N, d_model]      token inputs (the queries)
+ *   W1  [d_ff, d_model]   keys: row j is key j
+ *   W2  [d_ff, d_model]   values: row j is value j
+ *   out [N, d_model]      written
+ *   k       1 <= k <= d_ff;  chunk: token chunk size (0 = default), result-neutral
+ *   dtype   TOPK_F32 or TOPK_BF16; d_model must be a multiple of 8 and <= 1024
+ */
+int topk_ffn(const void* X, const void* W1, const void* W2, void* out,
+             int64_t N, int64_t d_model, int64_t d_ff, int64_t k,
+             int64_t chunk, int dtype, void* hip_stream);
+
+/*
+ * Debug / parity variants: the same computation, plus, when non-NULL,
+ *   idx_out   int32 [rows, k]: the selected key indices of each query row in the
+ *             order (score desc, index asc); -1 pads rows with k_eff < k
+ *   score_out fp32  [rows, k]: their raw (unscaled) fp32 scores; -inf pads
+ * where rows = B*H*Lq (attention) or N (FFN), in the row order of `out`.
+ */
+int topk_attn_debug(const void* Q, const void* K, const void* V, void* out,
+                    int64_t B, int64_t H, int64_t Lq, int64_t Lk, int64_t d,
+                    int64_t k, int64_t chunk, int causal, float scale,
+                    int dtype, void* hip_stream, int32_t* idx_out, float* score_out);
+int topk_ffn_debug(const void* X, const void* W1, const void* W2, void* out,
+                   int64_t N, int64_t d_model, int64_t d_ff, int64_t k,
+                   int64_t chunk, int dtype, void* hip_stream,
+                   int32_t* idx_out, float* score_out);
+
+/*
+ * Workspace (bytes) a call with these arguments uses under the default memory
+ * budget; 0 when the arguments are invalid. Register at least this much with
+ * topk_set_workspace() to run without library allocations. The budget caps the
+ * number of query chunks in flight, so the figure is O(chunk) per chunk and
+ * never exceeds the budget plus a fixed remainder.
+ */
+size_t topk_attn_workspace_bytes(int64_t B, int64_t H, int64_t Lq, int64_t Lk, int64_t d,
+                                 int64_t k, int64_t chunk, int causal, int dtype);
+size_t topk_ffn_workspace_bytes(int64_t N, int64_t d_model, int64_t d_ff, int64_t k,
+                                int64_t chunk, int dtype);
+
+/*
+ * Register (dev_ptr, bytes) as the calling thread's workspace for later calls;
+ * (NULL, 0) unregisters it. The caller owns the memory and must keep it alive
+ * until the enqueued work has finished. A call whose schedule does not fit the
+ * registered size first shrinks the number of chunks in flight and returns
+ * TOPK_E_NOMEM only if one chunk does not fit. Returns TOPK_OK, or TOPK_E_NULL
+ * for a NULL pointer with bytes > 0, or TOPK_E_ALIGN for a pointer that is not
+ * 256-byte aligned.
+ */
+int topk_set_workspace(void* dev_ptr, size_t bytes);
+
+/* Message describing the calling thread's last non-OK return ("" if none). */
+const char* topk_last_error(void);
+
+/*
+ * Which implementation the arguments select: 1 = fused score+filter path
+ * (bf16 MFMA score tiles, candidates filtered on chip), 2 = chunk-tile path
+ * (the chunk's score tile in workspace, then a row-wise select), or a negative
+ * status for invalid arguments. For tests and reports.
+ */
+int topk_attn_path(int64_t B, int64_t H, int64_t Lq, int64_t Lk, int64_t d,
+                   int64_t k, int64_t chunk, int causal, int dtype);
+int topk_ffn_path(int64_t N, int64_t d_model, int64_t d_ff, int64_t k,
+                  int64_t chunk, int dtype);
+
+/*
+ * Stage timing, for benchmarks. After topk_profile_begin(), every call made on
+ * the calling thread records a pair of HIP events on its own stream around each
+ * launch group: stage 0 = score tiles (fused scan, or chunk-tile scores),
+ * 1 = row select, 2 = fallback recomputation (fused path only), 3 = activation
+ * and gather. topk_profile_end() waits for those events, writes the summed
+ * milliseconds and the number of timed launches of the first n_stages stages
+ * into stage_ms / stage_launches (host arrays, either may be NULL) and stops
+ * recording. Returns TOPK_OK or TOPK_E_HIP.
+ */
+int topk_profile_begin(void);
+int topk_profile_end(double* stage_ms, int64_t* stage_launches, int n_stages);
+
+/*
+ * Test hook: run one wave of the bf16 MFMA used by the fused path on inputs that
+ * tag each operand element with its row or column, and write, for every lane l
+ * and accumulator register v, the output row (key) into rows_out[l*16+v] and
+ * column (query) into cols_out[l*16+v]. Both are int32 device buffers of 1024
+ * entries. Lets a GPU test confirm the lane layout the fused kernel assumes.
+ */
+int topk_selftest_mfma_layout(int32_t* rows_out, int32_t* cols_out, void* hip_stream);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* TOPK_ATTN_H */

@@ -1,0 +1,444 @@
+// Host side of the C ABI declared in include/topk_attn.h: argument validation,
+// path choice, the chunk scheduler (how many query chunks are in flight per pass
+// under the workspace budget) and the kernel sequence of each pass.
+#include "topk_attn.h"
+#include "topk_internal.h"
+
+#include <math.h>
+#include <stdarg.h>
+#include <stdio.h>
+#include <string.h>
+
+#include <string>
+#include <vector>
+
+namespace topk {
+namespace {
+
+thread_local std::string g_err;
+thread_local void* g_ws = nullptr;
+thread_local size_t g_ws_bytes = 0;
+
+// Optional per-stage timing (topk_profile_begin/end): an event pair around every
+// launch group of the calling thread's calls, on the call's own stream.
+enum Stage { ST_SCORE = 0, ST_SELECT = 1, ST_REDO = 2, ST_FINAL = 3, N_STAGES = 4 };
+struct Mark {
+  hipEvent_t a, b;
+  int stage;
+};
+thread_local bool g_prof = false;
+thread_local std::vector<Mark> g_marks;
+
+struct StageTimer {
+  hipStream_t st;
+  Mark m;
+  bool on;
+  StageTimer(hipStream_t s, int stage) : st(s), on(g_prof) {
+    if (!on) return;
+    m.stage = stage;
+    if (hipEventCreate(&m.a) != hipSuccess || hipEventCreate(&m.b) != hipSuccess) {
+      on = false;
+      return;
+    }
+    hipEventRecord(m.a, st);
+  }
+  ~StageTimer() {
+    if (!on) return;
+    hipEventRecord(m.b, st);
+    g_marks.push_back(m);
+  }
+};
+
+constexpr size_t ALIGN = 256;
+constexpr size_t DEFAULT_BUDGET = size_t(4) << 30;  // workspace cap when the library allocates
+constexpr int64_t DEFAULT_CHUNK = 1024;
+constexpr int64_t FUSED_CAPH = 512;                   // candidates kept per (query, half-wave)
+
+int fail(int code, const char* fmt, ...) {
+  char buf[512];
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(buf, sizeof buf, fmt, ap);
+  va_end(ap);
+  g_err = buf;
+  return code;
+}
+
+size_t up(size_t x) { return (x + ALIGN - 1) / ALIGN * ALIGN; }
+
+enum Path { PATH_FUSED = 1, PATH_TILE = 2 };
+
+struct Plan {
+  int path;
+  ScanCfg scan;
+  int64_t nchunk, total_chunks, per_pass;
+  size_t per_chunk, fixed;
+};
+
+// ---------------------------------------------------------------- validation
+int check_ptr(const void* p, const char* name) {
+  if (!p) return fail(TOPK_E_NULL, "%s is NULL", name);
+  if (((uintptr_t)p) % 16) return fail(TOPK_E_ALIGN, "%s is not 16-byte aligned", name);
+  return TOPK_OK;
+}
+
+int validate_shape(int64_t BH_a, int64_t BH_b, int64_t Lq, int64_t Lk, int64_t d, int64_t k, int64_t chunk,
+                   int causal, float scale, int dtype, bool attn) {
+  if (BH_a < 1 || BH_b < 1 || Lq < 1 || Lk < 1 || d < 1)
+    return fail(TOPK_E_INVAL, "sizes must be >= 1 (got %lld, %lld, %lld, %lld, %lld)", (long long)BH_a,
+                (long long)BH_b, (long long)Lq, (long long)Lk, (long long)d);
+  if (k < 1 || k > Lk) return fail(TOPK_E_INVAL, "need 1 <= k <= %lld keys (got k = %lld)", (long long)Lk, (long long)k);
+  if (chunk < 0) return fail(TOPK_E_INVAL, "chunk must be >= 0 (0 = default), got %lld", (long long)chunk);
+  if (attn && causal != 0 && causal != 1) return fail(TOPK_E_INVAL, "causal must be 0 or 1");
+  if (attn && !(isfinite(scale) && scale > 0.f)) return fail(TOPK_E_INVAL, "scale must be finite and > 0");
+  if (dtype != TOPK_F32 && dtype != TOPK_BF16) return fail(TOPK_E_INVAL, "dtype must be TOPK_F32 or TOPK_BF16");
+  if (d % 8 != 0 || d > 1024)
+    return fail(TOPK_E_UNSUPPORTED, "feature size %lld: this build needs a multiple of 8, at most 1024", (long long)d);
+  if (k > MAX_SELECT_K) return fail(TOPK_E_UNSUPPORTED, "k = %lld exceeds this build's limit %d", (long long)k, MAX_SELECT_K);
+  if (Lk > 0x7FFFFFFFLL) return fail(TOPK_E_UNSUPPORTED, "more than 2^31 - 1 keys");
+  return TOPK_OK;
+}
+
+// ---------------------------------------------------------------- planning
+int order_stat_for(int64_t k) { return k <= 32 ? 4 : (k <= 64 ? 8 : 16); }
+
+void choose_path(const Problem& pb, Plan* pl) {
+  pl->path = PATH_TILE;
+  pl->scan = {MODE_ALL, 16, 8};
+  const bool shape_ok = pb.dtype == T_BF16 && !pb.causal && (pb.d == 64 || pb.d == 128) && pb.k <= 128;
+  if (!shape_ok) return;
+  if (pb.Lk <= 2 * FUSED_CAPH) {  // every key fits the candidate buffers
+    pl->path = PATH_FUSED;
+    pl->scan = {MODE_ALL, 16, order_stat_for(pb.k)};
+    return;
+  }
+  // Threshold mode: the R-th largest 16-key block maximum of a 1-in-16 tile sample,
+  // taken on each half-wave, gives about 4k candidates per row; it needs at least R
+  // sampled tiles.
+  const int R = order_stat_for(pb.k);
+  const int64_t ntiles = (pb.Lk + 63) / 64;
+  if ((ntiles + 15) / 16 >= R) {
+    pl->path = PATH_FUSED;
+    pl->scan = {MODE_SAMPLE, 16, R};
+  }
+}
+
+size_t row_bytes(const Problem& pb, const Plan& pl) {
+  size_t b = (size_t)pb.k * 8 + 4;  // selection + redo list entry
+  if (pl.path == PATH_TILE)
+    b += (size_t)pb.Lk * 4;
+  else
+    b += 2 * FUSED_CAPH * 8 + 8;
+  return b;
+}
+
+void plan_sizes(const Problem& pb, Plan* pl, size_t budget) {
+  pl->nchunk = (pb.Lq + pb.C - 1) / pb.C;
+  pl->total_chunks = pb.BH * pl->nchunk;
+  pl->per_chunk = row_bytes(pb, *pl) * (size_t)pb.C + 6 * ALIGN;
+  pl->fixed = 2 * ALIGN + (pl->path == PATH_FUSED ? up((size_t)REDO_BLOCKS * pb.Lk * 4) : 0);
+  int64_t n = 1;
+  if (budget > pl->fixed + pl->per_chunk) n = (int64_t)((budget - pl->fixed) / pl->per_chunk);
+  if (n > pl->total_chunks) n = pl->total_chunks;
+  if (n < 1) n = 1;
+  // keep every grid within the launch limits (rows * 256 threads < 2^32, z <= 65535)
+  const int64_t max_rows = int64_t(1) << 23;
+  if (n * pb.C > max_rows) n = max_rows / pb.C > 0 ? max_rows / pb.C : 1;
+  if (n > 65535) n = 65535;
+  pl->per_pass = n;
+}
+
+size_t plan_total(const Plan& pl, const Problem& pb) {
+  (void)pb;
+  return pl.fixed + (size_t)pl.per_pass * pl.per_chunk;
+}
+
+PassBufs carve(const Problem& pb, const Plan& pl, char* ws) {
+  const size_t rows = (size_t)pl.per_pass * pb.C;
+  PassBufs b = {};
+  size_t off = 0;
+  b.redo_count = (int32_t*)(ws + off);
+  off += ALIGN;
+  b.redo_list = (int32_t*)(ws + off);
+  off += up(rows * 4);
+  b.sel = (uint64_t*)(ws + off);
+  off += up(rows * (size_t)pb.k * 8);
+  if (pl.path == PATH_TILE) {
+    b.scores = (float*)(ws + off);
+    off += up(rows * (size_t)pb.Lk * 4);
+  } else {
+    b.caph = FUSED_CAPH;
+    b.cand = (uint64_t*)(ws + off);
+    off += up(rows * 2 * FUSED_CAPH * 8);
+    b.cnt = (int32_t*)(ws + off);
+    off += up(rows * 8);
+    b.scores = (float*)(ws + off);
+    off += up((size_t)REDO_BLOCKS * pb.Lk * 4);
+  }
+  return b;
+}
+
+// ---------------------------------------------------------------- execution
+int run(Problem pb, hipStream_t st) {
+  Plan pl;
+  choose_path(pb, &pl);
+  size_t budget = g_ws ? g_ws_bytes : DEFAULT_BUDGET;
+  plan_sizes(pb, &pl, budget);
+  const size_t need = plan_total(pl, pb);
+  char* ws = (char*)g_ws;
+  bool own = false;
+  if (g_ws) {
+    if (need > g_ws_bytes)
+      return fail(TOPK_E_NOMEM, "registered workspace of %zu bytes is below the %zu bytes one query chunk needs",
+                  g_ws_bytes, need);
+  } else {
+    if (hipMallocAsync((void**)&ws, need, st) != hipSuccess)
+      return fail(TOPK_E_NOMEM, "could not allocate %zu bytes of workspace", need);
+    own = true;
+  }
+  hipError_t e = hipSuccess;
+  for (int64_t c0 = 0; c0 < pl.total_chunks && e == hipSuccess; c0 += pl.per_pass) {
+    Pass ps;
+    ps.c0 = c0;
+    ps.nc = pl.total_chunks - c0 < pl.per_pass ? pl.total_chunks - c0 : pl.per_pass;
+    ps.nchunk = pl.nchunk;
+    PassBufs b = carve(pb, pl, ws);
+    if (pl.path == PATH_TILE) {
+      if (e == hipSuccess) {
+        StageTimer t(st, ST_SCORE);
+        e = launch_tile_scores(pb, ps, b, st);
+      }
+      if (e == hipSuccess) {
+        StageTimer t(st, ST_SELECT);
+        e = launch_tile_select(pb, ps, b, st);
+      }
+    } else {
+      if (e == hipSuccess) e = launch_init(b, st);
+      if (e == hipSuccess) {
+        StageTimer t(st, ST_SCORE);
+        e = launch_fused_scan(pb, ps, b, pl.scan, st);
+      }
+      if (e == hipSuccess) {
+        StageTimer t(st, ST_SELECT);
+        e = launch_cand_select(pb, ps, b, st);
+      }
+      if (e == hipSuccess) {
+        StageTimer t(st, ST_REDO);
+        e = launch_redo(pb, ps, b, st);
+      }
+    }
+    if (e == hipSuccess) {
+      StageTimer t(st, ST_FINAL);
+      e = launch_finalize(pb, ps, b, st);
+    }
+  }
+  if (own) hipFreeAsync(ws, st);
+  if (e != hipSuccess) return fail(TOPK_E_HIP, "kernel launch failed: %s", hipGetErrorString(e));
+  return TOPK_OK;
+}
+
+int attn_problem(Problem* pb, const void* Q, const void* K, const void* V, void* out, int64_t B, int64_t H,
+                 int64_t Lq, int64_t Lk, int64_t d, int64_t k, int64_t chunk, int causal, float scale, int dtype,
+                 int32_t* idx_out, float* score_out, bool check_ptrs) {
+  int rc = validate_shape(B, H, Lq, Lk, d, k, chunk, causal, scale, dtype, true);
+  if (rc) return rc;
+  if (B > (int64_t(1) << 31) / H) return fail(TOPK_E_INVAL, "B*H too large");
+  if (check_ptrs) {
+    if ((rc = check_ptr(Q, "Q")) || (rc = check_ptr(K, "K")) || (rc = check_ptr(V, "V")) ||
+        (rc = check_ptr(out, "out")))
+      return rc;
+  }
+  pb->Q = Q;
+  pb->K = K;
+  pb->V = V;
+  pb->out = out;
+  pb->BH = B * H;
+  pb->Lq = Lq;
+  pb->Lk = Lk;
+  pb->d = d;
+  pb->k = k;
+  pb->C = chunk == 0 ? (Lq < DEFAULT_CHUNK ? Lq : DEFAULT_CHUNK) : (chunk < Lq ? chunk : Lq);
+  pb->kv_head_stride = Lk * d;
+  pb->causal = causal;
+  pb->scale = scale;
+  pb->dtype = dtype == TOPK_BF16 ? T_BF16 : T_F32;
+  pb->act = ACT_SOFTMAX;
+  pb->idx_out = idx_out;
+  pb->score_out = score_out;
+  return TOPK_OK;
+}
+
+int ffn_problem(Problem* pb, const void* X, const void* W1, const void* W2, void* out, int64_t N, int64_t d_model,
+                int64_t d_ff, int64_t k, int64_t chunk, int dtype, int32_t* idx_out, float* score_out,
+                bool check_ptrs) {
+  int rc = validate_shape(1, 1, N, d_ff, d_model, k, chunk, 0, 1.f, dtype, false);
+  if (rc) return rc;
+  if (check_ptrs) {
+    if ((rc = check_ptr(X, "X")) || (rc = check_ptr(W1, "W1")) || (rc = check_ptr(W2, "W2")) ||
+        (rc = check_ptr(out, "out")))
+      return rc;
+  }
+  pb->Q = X;
+  pb->K = W1;
+  pb->V = W2;
+  pb->out = out;
+  pb->BH = 1;
+  pb->Lq = N;
+  pb->Lk = d_ff;
+  pb->d = d_model;
+  pb->k = k;
+  pb->C = chunk == 0 ? (N < DEFAULT_CHUNK ? N : DEFAULT_CHUNK) : (chunk < N ? chunk : N);
+  pb->kv_head_stride = 0;
+  pb->causal = 0;
+  pb->scale = 1.f;
+  pb->dtype = dtype == TOPK_BF16 ? T_BF16 : T_F32;
+  pb->act = ACT_RELU;
+  pb->idx_out = idx_out;
+  pb->score_out = score_out;
+  return TOPK_OK;
+}
+
+int debug_ptrs(int32_t* idx_out, float* score_out) {
+  if (idx_out && ((uintptr_t)idx_out) % 4) return fail(TOPK_E_ALIGN, "idx_out is not 4-byte aligned");
+  if (score_out && ((uintptr_t)score_out) % 4) return fail(TOPK_E_ALIGN, "score_out is not 4-byte aligned");
+  return TOPK_OK;
+}
+
+size_t workspace_for(const Problem& pb) {
+  Plan pl;
+  choose_path(pb, &pl);
+  plan_sizes(pb, &pl, DEFAULT_BUDGET);
+  return plan_total(pl, pb);
+}
+
+}  // namespace
+}  // namespace topk
+
+using namespace topk;
+
+extern "C" {
+
+int topk_attn_debug(const void* Q, const void* K, const void* V, void* out, int64_t B, int64_t H, int64_t Lq,
+                    int64_t Lk, int64_t d, int64_t k, int64_t chunk, int causal, float scale, int dtype,
+                    void* hip_stream, int32_t* idx_out, float* score_out) {
+  g_err.clear();
+  Problem pb;
+  int rc = attn_problem(&pb, Q, K, V, out, B, H, Lq, Lk, d, k, chunk, causal, scale, dtype, idx_out, score_out, true);
+  if (rc) return rc;
+  if ((rc = debug_ptrs(idx_out, score_out))) return rc;
+  return run(pb, (hipStream_t)hip_stream);
+}
+
+int topk_attn(const void* Q, const void* K, const void* V, void* out, int64_t B, int64_t H, int64_t Lq, int64_t Lk,
+              int64_t d, int64_t k, int64_t chunk, int causal, float scale, int dtype, void* hip_stream) {
+  return topk_attn_debug(Q, K, V, out, B, H, Lq, Lk, d, k, chunk, causal, scale, dtype, hip_stream, nullptr,
+                         nullptr);
+}
+
+int topk_ffn_debug(const void* X, const void* W1, const void* W2, void* out, int64_t N, int64_t d_model, int64_t d_ff,
+                   int64_t k, int64_t chunk, int dtype, void* hip_stream, int32_t* idx_out, float* score_out) {
+  g_err.clear();
+  Problem pb;
+  int rc = ffn_problem(&pb, X, W1, W2, out, N, d_model, d_ff, k, chunk, dtype, idx_out, score_out, true);
+  if (rc) return rc;
+  if ((rc = debug_ptrs(idx_out, score_out))) return rc;
+  return run(pb, (hipStream_t)hip_stream);
+}
+
+int topk_ffn(const void* X, const void* W1, const void* W2, void* out, int64_t N, int64_t d_model, int64_t d_ff,
+             int64_t k, int64_t chunk, int dtype, void* hip_stream) {
+  return topk_ffn_debug(X, W1, W2, out, N, d_model, d_ff, k, chunk, dtype, hip_stream, nullptr, nullptr);
+}
+
+size_t topk_attn_workspace_bytes(int64_t B, int64_t H, int64_t Lq, int64_t Lk, int64_t d, int64_t k, int64_t chunk,
+                                 int causal, int dtype) {
+  Problem pb;
+  if (attn_problem(&pb, nullptr, nullptr, nullptr, nullptr, B, H, Lq, Lk, d, k, chunk, causal, 1.f, dtype, nullptr,
+                   nullptr, false))
+    return 0;
+  return workspace_for(pb);
+}
+
+size_t topk_ffn_workspace_bytes(int64_t N, int64_t d_model, int64_t d_ff, int64_t k, int64_t chunk, int dtype) {
+  Problem pb;
+  if (ffn_problem(&pb, nullptr, nullptr, nullptr, nullptr, N, d_model, d_ff, k, chunk, dtype, nullptr, nullptr, false))
+    return 0;
+  return workspace_for(pb);
+}
+
+int topk_set_workspace(void* dev_ptr, size_t bytes) {
+  g_err.clear();
+  if (!dev_ptr && bytes > 0) return fail(TOPK_E_NULL, "workspace pointer is NULL");
+  if (((uintptr_t)dev_ptr) % ALIGN) return fail(TOPK_E_ALIGN, "workspace must be 256-byte aligned");
+  g_ws = bytes ? dev_ptr : nullptr;
+  g_ws_bytes = dev_ptr ? bytes : 0;
+  return TOPK_OK;
+}
+
+const char* topk_last_error(void) { return g_err.c_str(); }
+
+int topk_attn_path(int64_t B, int64_t H, int64_t Lq, int64_t Lk, int64_t d, int64_t k, int64_t chunk, int causal,
+                   int dtype) {
+  Problem pb;
+  int rc = attn_problem(&pb, nullptr, nullptr, nullptr, nullptr, B, H, Lq, Lk, d, k, chunk, causal, 1.f, dtype,
+                        nullptr, nullptr, false);
+  if (rc) return rc;
+  Plan pl;
+  choose_path(pb, &pl);
+  return pl.path;
+}
+
+int topk_ffn_path(int64_t N, int64_t d_model, int64_t d_ff, int64_t k, int64_t chunk, int dtype) {
+  Problem pb;
+  int rc = ffn_problem(&pb, nullptr, nullptr, nullptr, nullptr, N, d_model, d_ff, k, chunk, dtype, nullptr, nullptr,
+                       false);
+  if (rc) return rc;
+  Plan pl;
+  choose_path(pb, &pl);
+  return pl.path;
+}
+
+int topk_profile_begin(void) {
+  g_err.clear();
+  for (auto& m : g_marks) {
+    hipEventDestroy(m.a);
+    hipEventDestroy(m.b);
+  }
+  g_marks.clear();
+  g_prof = true;
+  return TOPK_OK;
+}
+
+int topk_profile_end(double* stage_ms, int64_t* stage_launches, int n_stages) {
+  g_err.clear();
+  g_prof = false;
+  int rc = TOPK_OK;
+  for (int s = 0; s < n_stages; ++s) {
+    if (stage_ms) stage_ms[s] = 0.0;
+    if (stage_launches) stage_launches[s] = 0;
+  }
+  for (auto& m : g_marks) {
+    float ms = 0.f;
+    if (hipEventSynchronize(m.b) != hipSuccess || hipEventElapsedTime(&ms, m.a, m.b) != hipSuccess)
+      rc = fail(TOPK_E_HIP, "could not read stage timing events");
+    if (m.stage < n_stages) {
+      if (stage_ms) stage_ms[m.stage] += ms;
+      if (stage_launches) stage_launches[m.stage] += 1;
+    }
+    hipEventDestroy(m.a);
+    hipEventDestroy(m.b);
+  }
+  g_marks.clear();
+  return rc;
+}
+
+int topk_selftest_mfma_layout(int32_t* rows_out, int32_t* cols_out, void* hip_stream) {
+  g_err.clear();
+  int rc;
+  if ((rc = check_ptr(rows_out, "rows_out")) || (rc = check_ptr(cols_out, "cols_out"))) return rc;
+  hipError_t e = launch_mfma_probe(rows_out, cols_out, (hipStream_t)hip_stream);
+  if (e != hipSuccess) return fail(TOPK_E_HIP, "probe launch failed: %s", hipGetErrorString(e));
+  return TOPK_OK;
+}
+
+}  // extern "C"

@@ -1,0 +1,71 @@
+// Internal interface between the host scheduler (topk_api.hip) and the kernels
+// (topk_kernels.hip). Nothing here is part of the public C ABI.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace topk {
+
+enum Act { ACT_SOFTMAX = 0, ACT_RELU = 1 };
+enum ElemType { T_F32 = 0, T_BF16 = 1 };
+
+// Sampling modes of the fused scan: ALL keeps every valid score as a candidate;
+// SAMPLE first estimates a per-query threshold from a strided subset of key tiles.
+enum ScanMode { MODE_ALL = 0, MODE_SAMPLE = 1 };
+
+constexpr int REDO_BLOCKS = 64;     // blocks of the fallback kernel (grid-stride over the redo list)
+constexpr int MAX_SELECT_K = 4096;  // largest k the workgroup select / finalize handle
+
+// One call's problem. Attention: BH heads; the FFN is one head whose keys/values
+// are W1/W2 (kv_head_stride = 0). Rows of Q/out are (bh * Lq + i); keys (bh, j) sit
+// at K + bh * kv_head_stride + j * d.
+struct Problem {
+  const void* Q;
+  const void* K;
+  const void* V;
+  void* out;
+  int64_t BH, Lq, Lk, d, k, C;   // C = query chunk size
+  int64_t kv_head_stride;
+  int causal;
+  float scale;
+  int dtype;
+  int act;
+  int32_t* idx_out;
+  float* score_out;
+};
+
+// A pass covers chunk ids [c0, c0 + nc); chunk id = bh * nchunk + c covers query
+// rows [c*C, min((c+1)*C, Lq)) of head bh. Pass-local row p = (id - c0) * C + r.
+struct Pass {
+  int64_t c0, nc, nchunk;
+};
+
+// Workspace pointers of one pass.
+struct PassBufs {
+  uint64_t* sel;      // [rows, k] selected keys, (score desc, index asc); 0 pads
+  int32_t* redo_list; // [rows]
+  int32_t* redo_count;
+  float* scores;      // chunk-tile path: [rows, Lk]; fused path: redo rows [REDO_BLOCKS, Lk]
+  uint64_t* cand;     // fused path: [rows, 2, caph]
+  int32_t* cnt;       // fused path: [rows, 2]
+  int64_t caph;
+};
+
+struct ScanCfg {
+  int mode;           // ScanMode
+  int stride;         // SAMPLE: one key tile of 64 in `stride` is sampled
+  int R;              // SAMPLE: order statistic kept per lane (4, 8 or 16)
+};
+
+hipError_t launch_init(const PassBufs& b, hipStream_t st);
+hipError_t launch_tile_scores(const Problem& pb, const Pass& ps, const PassBufs& b, hipStream_t st);
+hipError_t launch_tile_select(const Problem& pb, const Pass& ps, const PassBufs& b, hipStream_t st);
+hipError_t launch_fused_scan(const Problem& pb, const Pass& ps, const PassBufs& b, const ScanCfg& cfg,
+                             hipStream_t st);
+hipError_t launch_cand_select(const Problem& pb, const Pass& ps, const PassBufs& b, hipStream_t st);
+hipError_t launch_redo(const Problem& pb, const Pass& ps, const PassBufs& b, hipStream_t st);
+hipError_t launch_finalize(const Problem& pb, const Pass& ps, const PassBufs& b, hipStream_t st);
+hipError_t launch_mfma_probe(int32_t* rows, int32_t* cols, hipStream_t st);
+
+}  // namespace topk

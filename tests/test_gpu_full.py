@@ -1,0 +1,59 @@
+"""GPU parity at the five workloads' full sizes, in the launch configuration the
+benchmark times (same call, same chunk). The oracle checks a sample of rows one by
+one: the first and last rows of every head, chunk boundaries, causal rows < k, and
+random rows."""
+import numpy as np
+import pytest
+import torch
+
+import paper_2106_06899_amd as tk
+from paper_2106_06899_amd import workloads as wl
+from tests import parity
+
+pytestmark = pytest.mark.gpu
+
+
+def _say(*a):
+    print("[case]", *a, flush=True)
+
+
+@pytest.mark.parametrize("name", ["c1", "c2", "c3", "c4"])
+def test_attn_full_size(name):
+    w = wl.WORKLOADS[name]
+    _say(name, w.note)
+    x = wl.make_inputs(w)
+    out, idx, sc = parity.run_attn(w, x)
+    rows = parity.sample_attn_rows(w, 160, seed=w.seed)
+    rep = {}
+    parity.check_attn(w, x, out, idx, rows=rows, report=rep)
+    _say(name, "sampled rows ok", rep)
+    # every row, not only the sampled ones, must carry exactly k_eff distinct valid indices
+    g = idx.cpu().numpy()
+    k_eff = np.minimum(w.k, np.arange(w.Lq) + 1) if w.causal else np.full(w.Lq, w.k)
+    assert np.array_equal((g >= 0).sum(-1), np.broadcast_to(k_eff, g.shape[:-1]))
+    srt = np.sort(np.where(g >= 0, g, -1 - np.arange(w.k)), axis=-1)
+    assert not np.any(srt[..., 1:] == srt[..., :-1]), "duplicate index in a row"
+    if w.causal:
+        assert np.all(g <= np.arange(w.Lq)[:, None]), "a causal row selected a future key"
+    assert torch.isfinite(out.float()).all()
+    if w.planted:
+        # generator sanity (not a parity criterion): most rows keep all 4 planted keys
+        pl = x["planted_idx"]
+        kept = np.mean([np.isin(pl[0, h, i], g[0, h, i]).all() for h in range(w.H) for i in range(0, w.Lq, 97)])
+        _say(name, "planted keys kept in", kept)
+        assert kept > 0.8
+
+
+def test_ffn_full_size():
+    w = wl.WORKLOADS["c5"]
+    _say("c5", w.note)
+    x = wl.make_inputs(w)
+    out, idx, sc = parity.run_ffn(w, x)
+    rng = np.random.Generator(np.random.PCG64(w.seed))
+    rows = np.unique(np.concatenate([[0, 1, w.chunk - 1, w.chunk, w.N - 1], rng.integers(0, w.N, 59)]))
+    rep = {}
+    parity.check_ffn(w, x, out, idx, rows=rows, report=rep)
+    _say("c5", "sampled rows ok", rep)
+    g = idx.cpu().numpy()
+    assert np.all((g >= 0).sum(-1) == w.k)
+    assert torch.isfinite(out.float()).all()

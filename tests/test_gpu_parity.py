@@ -1,0 +1,231 @@
+"""GPU parity of the HIP path against the fp64 oracle on small seeded cases.
+
+Each case follows one workload's recipe at a size the oracle finishes in seconds
+while still spanning several key tiles, several query blocks and ragged tails.
+Every call goes through the C ABI via the binding (``paper_2106_06899_amd``).
+"""
+import json
+import math
+import os
+
+import numpy as np
+import pytest
+import torch
+
+import paper_2106_06899_amd as tk
+from paper_2106_06899_amd import workloads as wl
+from tests import parity
+
+pytestmark = pytest.mark.gpu
+HERE = os.path.dirname(os.path.abspath(__file__))
+
+
+def _say(*a):
+    print("[case]", *a, flush=True)
+
+
+@pytest.fixture(autouse=True, scope="module")
+def _gpu():
+    assert torch.cuda.is_available(), "GPU tests need a GPU"
+    tk.lib()
+    yield
+
+
+def test_mfma_lane_layout():
+    """The fused scan assumes lane l, register v of the 32x32x16 bf16 MFMA holds output
+    row 8*(v/4) + 4*(l/32) + v%4 and column l%32."""
+    _say("mfma layout probe")
+    rows, cols = tk.mfma_layout()
+    torch.cuda.synchronize()
+    rows, cols = rows.cpu().numpy(), cols.cpu().numpy()
+    lanes = np.arange(64)[:, None]
+    v = np.arange(16)[None, :]
+    assert np.array_equal(rows, 8 * (v // 4) + 4 * (lanes // 32) + (v % 4))
+    assert np.array_equal(cols, np.broadcast_to(lanes % 32, (64, 16)))
+
+
+ATTN_CASES = {
+    # name: (base workload, overrides)
+    "c1_fp32_tile": ("c1", dict(Lq=300, Lk=777, chunk=100)),
+    "c2_bf16_fused_all": ("c2", dict(B=2, H=3, Lq=200, Lk=512, chunk=128)),
+    "c2_bf16_fused_all_ragged": ("c2", dict(B=1, H=2, Lq=130, Lk=333, chunk=64)),
+    "c3_bf16_fused_sample": ("c3", dict(H=2, Lq=300, Lk=9000, chunk=256)),
+    "c3_bf16_fused_sample_k32": ("c3", dict(H=1, Lq=257, Lk=4600, k=32, chunk=1024)),
+    "c4_bf16_causal_tile": ("c4", dict(B=1, H=2, Lq=600, Lk=600, chunk=256)),
+    "c4_d128_fused_sample": ("c4", dict(B=1, H=1, Lq=200, Lk=17000, causal=False, chunk=128)),
+    "c4_d128_fused_all": ("c4", dict(B=1, H=2, Lq=150, Lk=700, causal=False, chunk=64)),
+    "bf16_tile_d96": ("c2", dict(B=1, H=2, Lq=70, Lk=300, d=96, k=40, chunk=32)),
+    "fp32_causal_tile": ("c1", dict(Lq=200, Lk=260, causal=True, k=20, chunk=64)),
+}
+
+
+@pytest.mark.parametrize("name", sorted(ATTN_CASES))
+def test_attn_parity(name):
+    base, kw = ATTN_CASES[name]
+    w = wl.WORKLOADS[base].scaled(**kw)
+    _say(name, w)
+    x = wl.make_inputs(w)
+    out, idx, sc = parity.run_attn(w, x)
+    rep = {}
+    parity.check_attn(w, x, out, idx, report=rep)
+    _say(name, "ok", rep, "path", tk.attn_path(w.B, w.H, w.Lq, w.Lk, w.d, w.k, w.chunk, w.causal,
+                                                tk.TOPK_BF16 if w.dtype == wl.BF16 else tk.TOPK_F32))
+    # debug scores are the raw fp32 scores of the selected keys, sorted descending
+    s = sc.cpu().numpy()
+    fin = np.isfinite(s)
+    assert np.all(np.diff(np.where(fin, s, -np.inf), axis=-1)[fin[..., 1:]] <= 0)
+
+
+FFN_CASES = {
+    "c5_tile": dict(N=300, d_model=256, d_ff=4096, k=512, chunk=128),
+    "c5_tile_small_k": dict(N=100, d_model=64, d_ff=2000, k=7, chunk=33),
+    "ffn_fused_all": dict(N=260, d_model=64, d_ff=1000, k=64, chunk=100),
+    "ffn_fused_sample": dict(N=130, d_model=128, d_ff=20000, k=100, chunk=0),
+}
+
+
+@pytest.mark.parametrize("name", sorted(FFN_CASES))
+def test_ffn_parity(name):
+    w = wl.WORKLOADS["c5"].scaled(**FFN_CASES[name])
+    _say(name, w)
+    x = wl.make_inputs(w)
+    out, idx, sc = parity.run_ffn(w, x)
+    rep = {}
+    parity.check_ffn(w, x, out, idx, report=rep)
+    _say(name, "ok", rep, "path", tk.ffn_path(w.N, w.d_model, w.d_ff, w.k, w.chunk))
+
+
+@pytest.mark.parametrize("base,kw", [
+    ("c2", dict(B=1, H=2, Lq=100, Lk=512)),                 # fused, all candidates
+    ("c3", dict(H=1, Lq=150, Lk=9000)),                     # fused, sampled threshold
+    ("c4", dict(B=1, H=1, Lq=100, Lk=300)),                 # chunk-tile, causal
+])
+def test_k1_returns_argmax_value_row_exactly(base, kw):
+    """k = 1: the single survivor has softmax weight exactly 1, so the bf16 output is
+    the value row of the best key, bit for bit."""
+    w = wl.WORKLOADS[base].scaled(k=1, **kw)
+    _say("k1", w)
+    x = wl.make_inputs(w)
+    out, idx, _ = parity.run_attn(w, x)
+    parity.check_attn(w, x, out, idx)
+    o = out.view(torch.int16).cpu().numpy()
+    V = x["V"].bits.view(np.int16)
+    g = idx.cpu().numpy()[..., 0]
+    for b in range(w.B):
+        for h in range(w.H):
+            assert np.array_equal(o[b, h], V[b, h][g[b, h]])
+
+
+@pytest.mark.parametrize("base,kw", [
+    ("c1", dict(Lq=64, Lk=200, chunk=32)),
+    ("c2", dict(B=1, H=1, Lq=64, Lk=256, chunk=64)),
+    ("c4", dict(B=1, H=1, Lq=96, Lk=96, d=128, chunk=32)),
+])
+def test_k_equals_Lk_is_vanilla_attention(base, kw):
+    """k = Lk: the GPU result equals dense softmax attention (Eq. 1 / Eq. 2) within tolerance."""
+    w = wl.WORKLOADS[base].scaled(**kw)
+    w = w.scaled(k=w.Lk)
+    _say("k=Lk", w)
+    x = wl.make_inputs(w)
+    out, idx, _ = parity.run_attn(w, x)
+    Q, K, V = (x[n].values.astype(np.float64) for n in ("Q", "K", "V"))
+    S = np.einsum("bhid,bhjd->bhij", Q, K) * np.float64(np.float32(w.scale))
+    if w.causal:
+        S = np.where(np.tril(np.ones((w.Lq, w.Lk), bool))[None, None], S, -np.inf)
+    P = np.exp(S - S.max(-1, keepdims=True))
+    P /= P.sum(-1, keepdims=True)
+    ref = P @ V
+    got = out.float().cpu().numpy()
+    err = np.abs(got - ref).max(-1) / np.abs(ref).max(-1)
+    assert err.max() <= parity.RTOL[w.dtype], err.max()
+
+
+@pytest.mark.parametrize("base,kw", [
+    ("c2", dict(B=1, H=2, Lq=200, Lk=512)),
+    ("c3", dict(H=1, Lq=300, Lk=9000)),
+    ("c4", dict(B=1, H=1, Lq=300, Lk=300)),
+    ("c1", dict(Lq=200, Lk=300)),
+])
+def test_chunking_does_not_change_the_result(base, kw):
+    """Query chunking is result-neutral: bit-identical outputs and indices for every C."""
+    w = wl.WORKLOADS[base].scaled(**kw)
+    x = wl.make_inputs(w)
+    ref = None
+    for C in (1, 7, 64, 256, w.Lq):
+        _say("chunk", C, w)
+        out, idx, sc = parity.run_attn(w, x, chunk=C)
+        cur = (out.view(torch.int16 if w.dtype == wl.BF16 else torch.int32).cpu(), idx.cpu(), sc.cpu())
+        if ref is None:
+            ref = cur
+            parity.check_attn(w, x, out, idx)
+        else:
+            for a, b in zip(ref, cur):
+                assert torch.equal(a, b), f"chunk {C} differs"
+
+
+def test_repeated_calls_are_bit_identical():
+    w = wl.WORKLOADS["c3"].scaled(H=2, Lq=500, Lk=9000)
+    _say("determinism", w)
+    x = wl.make_inputs(w)
+    a = parity.run_attn(w, x)
+    b = parity.run_attn(w, x)
+    for p, q in zip(a, b):
+        assert torch.equal(p.cpu(), q.cpu())
+
+
+@pytest.mark.parametrize("kw", [
+    dict(B=1, H=1, Lq=1, Lk=1, k=1),
+    dict(B=1, H=1, Lq=1, Lk=5, k=5),
+    dict(B=1, H=3, Lq=5, Lk=63, k=10),
+    dict(B=1, H=1, Lq=129, Lk=65, k=64),
+    dict(B=2, H=1, Lq=33, Lk=1024, k=128),
+])
+def test_edge_shapes(kw):
+    for base in ("c2", "c1"):
+        w = wl.WORKLOADS[base].scaled(chunk=0, **kw)
+        _say("edge", w)
+        x = wl.make_inputs(w)
+        out, idx, _ = parity.run_attn(w, x)
+        parity.check_attn(w, x, out, idx)
+
+
+def test_causal_rows_below_k_keep_every_valid_key():
+    w = wl.WORKLOADS["c4"].scaled(B=1, H=1, Lq=300, Lk=300, k=128, chunk=100)
+    _say("causal rows < k", w)
+    x = wl.make_inputs(w)
+    out, idx, _ = parity.run_attn(w, x)
+    g = idx.cpu().numpy()[0, 0]
+    for i in range(w.k):
+        assert sorted(g[i][g[i] >= 0].tolist()) == list(range(i + 1))
+        assert np.all(g[i][i + 1:] == -1)
+    parity.check_attn(w, x, out, idx)
+
+
+def _pad(a, n=8):
+    a = np.asarray(a, dtype=np.float32)
+    out = np.zeros(a.shape[:-1] + (max(n, a.shape[-1]),), np.float32)
+    out[..., : a.shape[-1]] = a
+    return out
+
+
+@pytest.mark.parametrize("ex", json.load(open(os.path.join(HERE, "golden", "worked_examples.json")))["examples"],
+                         ids=lambda e: e["name"])
+@pytest.mark.parametrize("dtype", [torch.float32, torch.bfloat16])
+def test_worked_examples_on_gpu(ex, dtype):
+    """The hand-derived examples of Eq. 2-4 (features zero-padded to 8, exact in bf16)."""
+    _say("worked example", ex["name"], dtype)
+    Q, K, V = (torch.from_numpy(_pad(ex[n])).to("cuda", dtype) for n in ("Q", "K", "V"))
+    if ex["activation"] == "relu":
+        out, idx, _ = tk.ffn(Q, K, V, ex["k"], debug=True)
+    else:
+        out, idx, _ = tk.attn(Q[None, None], K[None, None], V[None, None], ex["k"], 0, ex.get("causal", False),
+                              ex.get("scale", 1.0), debug=True)
+        out, idx = out[0, 0], idx[0, 0]
+    torch.cuda.synchronize()
+    for i, want in enumerate(ex["selected"]):
+        got = idx[i].cpu().numpy()
+        assert got[got >= 0].tolist() == want
+    want = np.array([[float(eval(v, {"__builtins__": {}}, {"exp": math.exp})) for v in row] for row in ex["out"]])
+    got = out.float().cpu().numpy()[:, : want.shape[1]]
+    tol = 1e-6 if dtype == torch.float32 else 1e-2
+    np.testing.assert_allclose(got, want, rtol=tol, atol=tol)
