@@ -50,7 +50,7 @@ struct StageTimer {
 };
 
 constexpr size_t ALIGN = 256;
-constexpr size_t DEFAULT_BUDGET = size_t(4) << 30;  // workspace cap when the library allocates
+constexpr size_t DEFAULT_BUDGET = size_t(8) << 30;  // workspace cap when the library allocates
 constexpr int64_t DEFAULT_CHUNK = 1024;
 constexpr int64_t FUSED_CAPH = 512;                   // candidates kept per (query, half-wave)
 
@@ -100,12 +100,13 @@ int validate_shape(int64_t BH_a, int64_t BH_b, int64_t Lq, int64_t Lk, int64_t d
 }
 
 // ---------------------------------------------------------------- planning
-int order_stat_for(int64_t k) { return k <= 32 ? 4 : (k <= 64 ? 8 : 16); }
+int order_stat_for(int64_t k) { return k <= 32 ? 3 : (k <= 64 ? 6 : 12); }
 
 void choose_path(const Problem& pb, Plan* pl) {
   pl->path = PATH_TILE;
   pl->scan = {MODE_ALL, 16, 8};
-  const bool shape_ok = pb.dtype == T_BF16 && !pb.causal && (pb.d == 64 || pb.d == 128) && pb.k <= 128;
+  const bool shape_ok = pb.dtype == T_BF16 && !pb.causal && (pb.d == 64 || pb.d == 128) && pb.k <= 128 &&
+                        pb.Lk < (int64_t(1) << 25);
   if (!shape_ok) return;
   if (pb.Lk <= 2 * FUSED_CAPH) {  // every key fits the candidate buffers
     pl->path = PATH_FUSED;
@@ -113,11 +114,12 @@ void choose_path(const Problem& pb, Plan* pl) {
     return;
   }
   // Threshold mode: the R-th largest 16-key block maximum of a 1-in-16 tile sample,
-  // taken on each half-wave, gives about 4k candidates per row; it needs at least R
-  // sampled tiles.
+  // taken on each half-wave, gives about 4k candidates per row; each lane needs at
+  // least 2R sampled blocks of 16 keys.
   const int R = order_stat_for(pb.k);
-  const int64_t ntiles = (pb.Lk + 63) / 64;
-  if ((ntiles + 15) / 16 >= R) {
+  const int64_t kt = 64;  // key tile of the scan kernel
+  const int64_t sampled_tiles = ((pb.Lk + kt - 1) / kt + 15) / 16;
+  if (sampled_tiles * (kt / 32) >= 2 * R) {
     pl->path = PATH_FUSED;
     pl->scan = {MODE_SAMPLE, 16, R};
   }
@@ -136,7 +138,7 @@ void plan_sizes(const Problem& pb, Plan* pl, size_t budget) {
   pl->nchunk = (pb.Lq + pb.C - 1) / pb.C;
   pl->total_chunks = pb.BH * pl->nchunk;
   pl->per_chunk = row_bytes(pb, *pl) * (size_t)pb.C + 6 * ALIGN;
-  pl->fixed = 2 * ALIGN + (pl->path == PATH_FUSED ? up((size_t)REDO_BLOCKS * pb.Lk * 4) : 0);
+  pl->fixed = 2 * ALIGN + (pl->path == PATH_FUSED ? up((size_t)(REDO_CAP + REDO_BLOCKS) * pb.Lk * 4) : 0);
   int64_t n = 1;
   if (budget > pl->fixed + pl->per_chunk) n = (int64_t)((budget - pl->fixed) / pl->per_chunk);
   if (n > pl->total_chunks) n = pl->total_chunks;
@@ -145,7 +147,9 @@ void plan_sizes(const Problem& pb, Plan* pl, size_t budget) {
   const int64_t max_rows = int64_t(1) << 23;
   if (n * pb.C > max_rows) n = max_rows / pb.C > 0 ? max_rows / pb.C : 1;
   if (n > 65535) n = 65535;
-  pl->per_pass = n;
+  // equal passes: the last pass must not run a handful of chunks on an idle GPU
+  const int64_t passes = (pl->total_chunks + n - 1) / n;
+  pl->per_pass = (pl->total_chunks + passes - 1) / passes;
 }
 
 size_t plan_total(const Plan& pl, const Problem& pb) {
@@ -173,7 +177,7 @@ PassBufs carve(const Problem& pb, const Plan& pl, char* ws) {
     b.cnt = (int32_t*)(ws + off);
     off += up(rows * 8);
     b.scores = (float*)(ws + off);
-    off += up((size_t)REDO_BLOCKS * pb.Lk * 4);
+    off += up((size_t)(REDO_CAP + REDO_BLOCKS) * pb.Lk * 4);
   }
   return b;
 }

@@ -14,7 +14,10 @@ enum ElemType { T_F32 = 0, T_BF16 = 1 };
 // SAMPLE first estimates a per-query threshold from a strided subset of key tiles.
 enum ScanMode { MODE_ALL = 0, MODE_SAMPLE = 1 };
 
-constexpr int REDO_BLOCKS = 64;     // blocks of the fallback kernel (grid-stride over the redo list)
+constexpr int REDO_CAP = 1024;          // redo rows recomputed by the wide fallback kernels
+constexpr int REDO_SPLIT = 2048;        // keys per work item of the wide fallback
+constexpr int REDO_SCORE_BLOCKS = 512;  // workgroups of the wide fallback's score kernel
+constexpr int REDO_BLOCKS = 64;         // workgroups of the fallback for rows beyond REDO_CAP
 constexpr int MAX_SELECT_K = 4096;  // largest k the workgroup select / finalize handle
 
 // One call's problem. Attention: BH heads; the FFN is one head whose keys/values
@@ -46,7 +49,7 @@ struct PassBufs {
   uint64_t* sel;      // [rows, k] selected keys, (score desc, index asc); 0 pads
   int32_t* redo_list; // [rows]
   int32_t* redo_count;
-  float* scores;      // chunk-tile path: [rows, Lk]; fused path: redo rows [REDO_BLOCKS, Lk]
+  float* scores;      // chunk-tile path: [rows, Lk]; fused path: redo rows [REDO_CAP + REDO_BLOCKS, Lk]
   uint64_t* cand;     // fused path: [rows, 2, caph]
   int32_t* cnt;       // fused path: [rows, 2]
   int64_t caph;
@@ -54,8 +57,8 @@ struct PassBufs {
 
 struct ScanCfg {
   int mode;           // ScanMode
-  int stride;         // SAMPLE: one key tile of 64 in `stride` is sampled
-  int R;              // SAMPLE: order statistic kept per lane (4, 8 or 16)
+  int stride;         // SAMPLE: one key tile in `stride` is sampled
+  int R;              // SAMPLE: order statistic kept per lane (3, 6 or 12)
 };
 
 hipError_t launch_init(const PassBufs& b, hipStream_t st);

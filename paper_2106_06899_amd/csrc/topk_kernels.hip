@@ -270,13 +270,23 @@ __global__ __launch_bounds__(256) void k_tile_select(Problem pb, Pass ps, const 
 }
 
 // ------------------------------------------------------------------ fused path: scan
-// One workgroup = 4 waves x 32 queries of one head. The B operand (32 queries x d)
-// stays in registers; key tiles of 64 rows are staged in LDS; each wave computes
-// S^T = K Q^T with v_mfma_f32_32x32x16_bf16, so lane l holds 16 keys' scores of
-// query l % 32 (keys 8*(v/4) + 4*(l/32) + v%4 of the 32-key block, v = 0..15).
-// The feature dimension is split between the half-waves: lane half h holds
-// features [h*D/2, h*D/2 + D/2) of its row in both operands (the contraction is
-// order-free), so every lane loads 2*(D/2) contiguous bytes.
+// One workgroup = 4 waves x 64 queries of one head. Each wave keeps the B operand
+// of two 32-query column groups (its 64 queries x d) in registers; key tiles are
+// staged in LDS (two buffers, the next tile prefetched into registers while the
+// current one is consumed). Each wave computes S^T = K Q^T with
+// v_mfma_f32_32x32x16_bf16, so lane l holds 16 keys' scores of query l % 32 of a
+// group (keys 8*(v/4) + 4*(l/32) + v%4 of the 32-key block, v = 0..15); one LDS
+// read of the K operand feeds both groups. The feature dimension is split between
+// the half-waves: half h holds features [h*D/2, h*D/2 + D/2) of its row in both
+// operands (the contraction is order-free), so every lane loads D contiguous bytes.
+//
+// Filtering is two-level. Per 16-score lane block, a max tree decides whether any
+// score beats the query's threshold; only such "dirty" blocks are copied into a
+// per-wave LDS staging ring. When the ring fills, the whole wave drains it: each
+// lane takes one staged block, finds its passing scores and appends them as
+// 64-bit words  (raw fp32 score bits << 32) | (~key)  to the query's candidate
+// buffer in global memory (one buffer per query and half-wave, positions from LDS
+// atomic counters). The select converts the words to order-preserving keys.
 struct ScanArgs {
   const uint16_t* Q;
   const uint16_t* K;
@@ -288,110 +298,243 @@ struct ScanArgs {
   int mode, stride;
 };
 
+constexpr int STAGE_CAP = 112;  // staged 16-score blocks per wave
+
 template <int D, int R>
-__global__ __launch_bounds__(256) void k_fused_scan(ScanArgs a) {
-  constexpr int KT = 64;             // keys per LDS tile (two 32-key MFMA blocks)
-  constexpr int ROWB = 2 * D + 16;   // padded LDS row (bytes): conflict-free 16-byte reads
-  constexpr int NS = D / 16;         // MFMA steps over the features
-  constexpr int CH = 2 * D / 16;     // 16-byte pieces per key row
-  __shared__ __attribute__((aligned(16))) unsigned char ks[KT * ROWB];
+__global__ __launch_bounds__(256, D == 64 ? 3 : 2) void k_fused_scan(ScanArgs a) {
+  constexpr int KT = 64;                  // keys per LDS tile
+  constexpr int NRB = KT / 32;            // 32-key MFMA blocks per tile
+  constexpr int ROWB = 2 * D + 16;        // padded LDS row (bytes): conflict-free 16-byte reads
+  constexpr int NS = D / 16;              // MFMA steps over the features
+  constexpr int CH = 2 * D / 16;          // 16-byte pieces per key row
+  constexpr int PT = KT * CH / 256;       // pieces per thread per tile
+  constexpr int QB = 256;                 // queries per workgroup
+  __shared__ __attribute__((aligned(16))) unsigned char ks[2][KT * ROWB];
+  // staging slot = 16 scores (64 bytes) stored as four 16-byte chunks; chunk c of
+  // slot s sits at chunk position c ^ ((s >> 2) & 3), so the 8 lanes one LDS cycle
+  // serves (consecutive slots) hit 8 different bank groups
+  __shared__ __attribute__((aligned(16))) float stage[4][STAGE_CAP][16];
+  __shared__ uint32_t stage_meta[4][STAGE_CAP];
+  __shared__ float tau_lds[4][64];
+  __shared__ uint32_t cnt_lds[4][128];
 
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63, half = lane >> 5, n = lane & 31;
-  const int64_t wg = blockIdx.x, cl = wg / a.wgs_per_chunk, blk = wg - cl * a.wgs_per_chunk;
+  // XCD-aware order: the hardware deals workgroups round-robin over the 8 XCDs;
+  // renumber so each XCD runs consecutive logical workgroups (same head) and K
+  // stays in that XCD's L2.
+  const int64_t G = gridDim.x, bid = blockIdx.x;
+  const int64_t wg = (G % 8 == 0) ? (bid % 8) * (G / 8) + bid / 8 : bid;
+  const int64_t cl = wg / a.wgs_per_chunk, blk = wg - cl * a.wgs_per_chunk;
   const int64_t id = a.c0 + cl, bh = id / a.nchunk, c = id - bh * a.nchunk;
-  const int64_t local = blk * 128 + wave * 32 + n, i = c * a.C + local;
-  const bool row_ok = local < a.C && i < a.Lq;
-  const int64_t p = cl * a.C + local;
   const uint16_t* Kh = a.K + bh * a.kv_head_stride;
   const int64_t ntiles = (a.Lk + KT - 1) / KT;
+  const bool tail = ntiles * KT != a.Lk;
+  const int64_t wave_row0 = cl * a.C + blk * QB + wave * 64;  // pass-local row of the wave's query 0
 
-  bf16x8 b[NS];
+  bool ok[2];
+  bf16x8 b[2][NS];
   {
     const bf16x8 zero8 = {};
-    const uint16_t* q = a.Q + (bh * a.Lq + (row_ok ? i : 0)) * D + (D / 2) * half;
 #pragma unroll
-    for (int s = 0; s < NS; ++s) {
-      b[s] = *(const bf16x8*)(q + 8 * s);
-      if (!row_ok) b[s] = zero8;
+    for (int g = 0; g < 2; ++g) {
+      const int64_t local = blk * QB + wave * 64 + g * 32 + n, i = c * a.C + local;
+      ok[g] = local < a.C && i < a.Lq;
+      const uint16_t* q = a.Q + (bh * a.Lq + (ok[g] ? i : 0)) * D + (D / 2) * half;
+#pragma unroll
+      for (int s = 0; s < NS; ++s) b[g][s] = ok[g] ? *(const bf16x8*)(q + 8 * s) : zero8;
     }
   }
+  cnt_lds[wave][lane] = 0;
+  cnt_lds[wave][64 + lane] = 0;
 
-  auto load_tile = [&](int64_t t) {
+  uint4 pre[PT];
+  auto issue = [&](int64_t t) {
     const int64_t key0 = t * KT;
 #pragma unroll
-    for (int cidx = tid; cidx < KT * CH; cidx += 256) {
-      const int kr = cidx / CH, part = cidx - kr * CH;
-      uint4 v = make_uint4(0u, 0u, 0u, 0u);
-      if (key0 + kr < a.Lk) v = *(const uint4*)(Kh + (key0 + kr) * D + part * 8);
-      *(uint4*)(ks + kr * ROWB + part * 16) = v;
+    for (int e = 0; e < PT; ++e) {
+      const int cidx = tid + 256 * e, kr = cidx / CH, part = cidx - kr * CH;
+      pre[e] = key0 + kr < a.Lk ? *(const uint4*)(Kh + (key0 + kr) * D + part * 8) : make_uint4(0u, 0u, 0u, 0u);
     }
   };
-  auto block_scores = [&](int rb) {
-    f32x16 acc = {};
-    const unsigned char* base = ks + (rb * 32 + n) * ROWB + half * D;
+  auto stash = [&](int buf) {
+#pragma unroll
+    for (int e = 0; e < PT; ++e) {
+      const int cidx = tid + 256 * e, kr = cidx / CH, part = cidx - kr * CH;
+      *(uint4*)(&ks[buf][kr * ROWB + part * 16]) = pre[e];
+    }
+  };
+  // Runs body(tile, lds) over tiles 0, step, 2*step, ... (count of them),
+  // double-buffered: tile t+1's global loads are in flight while t is consumed.
+  auto pipeline = [&](int64_t count, int64_t step, auto&& body) {
+    if (count <= 0) return;
+    issue(0);
+    for (int64_t t = 0; t < count; ++t) {
+      const int buf = (int)(t & 1);
+      stash(buf);
+      __syncthreads();
+      if (t + 1 < count) issue((t + 1) * step);
+      body(t * step, &ks[buf][0]);
+    }
+    __syncthreads();
+  };
+  // scores of 32 keys (block rb of the tile) for both query groups
+  auto block_scores = [&](const unsigned char* kb, int rb, f32x16& acc0, f32x16& acc1) {
+    const unsigned char* base = kb + (rb * 32 + n) * ROWB + half * D;
+    bf16x8 av[NS];
+#pragma unroll
+    for (int s = 0; s < NS; ++s) av[s] = *(const bf16x8*)(base + 16 * s);
+    acc0 = (f32x16){};
+    acc1 = (f32x16){};
 #pragma unroll
     for (int s = 0; s < NS; ++s) {
-      const bf16x8 av = *(const bf16x8*)(base + 16 * s);
-      acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(av, b[s], acc, 0, 0, 0);
+      acc0 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(av[s], b[0][s], acc0, 0, 0, 0);
+      acc1 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(av[s], b[1][s], acc1, 0, 0, 0);
     }
-    return acc;
   };
-  auto mask_tail = [&](f32x16& acc, int64_t jb) {  // keys >= Lk of the last tile -> -inf
+  auto mask_keys = [&](f32x16& acc, int64_t jb) {  // keys >= Lk of the last tile -> -inf
 #pragma unroll
     for (int v = 0; v < 16; ++v)
       if (jb + 8 * (v >> 2) + (v & 3) >= a.Lk) acc[v] = -INFINITY;
   };
+  auto block_max = [&](const f32x16& acc) {
+    float m = acc[0];
+#pragma unroll
+    for (int v = 1; v < 16; ++v) m = fmaxf(m, acc[v]);
+    return m;
+  };
 
-  float tau = -INFINITY;
+  float tau[2] = {-INFINITY, -INFINITY};
   if (a.mode == MODE_SAMPLE) {
-    float top[R];
+    float top[2][R];
 #pragma unroll
-    for (int r = 0; r < R; ++r) top[r] = -INFINITY;
-    for (int64_t t = 0; t < ntiles; t += a.stride) {
-      __syncthreads();
-      load_tile(t);
-      __syncthreads();
+    for (int g = 0; g < 2; ++g)
 #pragma unroll
-      for (int rb = 0; rb < 2; ++rb) {
-        f32x16 acc = block_scores(rb);
-        if ((t + 1) * KT > a.Lk) mask_tail(acc, t * KT + rb * 32 + 4 * half);
-        float m = acc[0];
+      for (int r = 0; r < R; ++r) top[g][r] = -INFINITY;
+    auto insert = [&](float (&tp)[R], float m) {
 #pragma unroll
-        for (int v = 1; v < 16; ++v) m = fmaxf(m, acc[v]);
-#pragma unroll
-        for (int r = 0; r < R; ++r) {  // sorted insert, descending
-          const float hi = fmaxf(top[r], m);
-          m = fminf(top[r], m);
-          top[r] = hi;
-        }
+      for (int r = 0; r < R; ++r) {  // sorted insert, descending
+        const float hi = fmaxf(tp[r], m);
+        m = fminf(tp[r], m);
+        tp[r] = hi;
       }
+    };
+    const int64_t ns = (ntiles + a.stride - 1) / a.stride;
+    pipeline(ns, a.stride, [&](int64_t t, const unsigned char* kb) {
+#pragma unroll 1
+      for (int rb = 0; rb < NRB; ++rb) {
+        f32x16 acc0, acc1;
+        block_scores(kb, rb, acc0, acc1);
+        if (tail && t == ntiles - 1) {
+          const int64_t jb = t * KT + rb * 32 + 4 * half;
+          mask_keys(acc0, jb);
+          mask_keys(acc1, jb);
+        }
+        insert(top[0], block_max(acc0));
+        insert(top[1], block_max(acc1));
+      }
+    });
+#pragma unroll
+    for (int g = 0; g < 2; ++g) {
+      const float mine = top[g][R - 1];
+      tau[g] = fminf(mine, __shfl_xor(mine, 32, 64));
     }
-    const float mine = top[R - 1];
-    tau = fminf(mine, __shfl_xor(mine, 32, 64));
   }
-  if (!row_ok) tau = INFINITY;
+#pragma unroll
+  for (int g = 0; g < 2; ++g) {
+    if (!ok[g]) tau[g] = INFINITY;
+    if (half == 0) tau_lds[wave][g * 32 + n] = tau[g];
+  }
 
-  uint64_t* mybuf = a.cand + (p * 2 + half) * a.caph;
-  int cnt = 0;
-  for (int64_t t = 0; t < ntiles; ++t) {
-    __syncthreads();
-    load_tile(t);
-    __syncthreads();
+  // ---- staging ring and its drain (all per wave; LDS ops of one wave execute in order)
+  int scount = 0;  // wave-uniform
+  auto drain = [&]() {
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+    for (int base = 0; base < scount; base += 64) {
+      const int slot = base + lane;
+      uint32_t mask = 0, meta = 0;
+      if (slot < scount) {
+        meta = stage_meta[wave][slot];
+        const float t = tau_lds[wave][(meta >> 6 & 1) * 32 + (meta & 31)];
+        const float4* sp = (const float4*)&stage[wave][slot][0];
+        const int sw = (slot >> 2) & 3;
 #pragma unroll
-    for (int rb = 0; rb < 2; ++rb) {
-      f32x16 acc = block_scores(rb);
-      const int64_t jb = t * KT + rb * 32 + 4 * half;
-      if ((t + 1) * KT > a.Lk) mask_tail(acc, jb);
+        for (int q4 = 0; q4 < 4; ++q4) {
+          const float4 x = sp[q4 ^ sw];
+          mask |= (x.x > t ? 1u : 0u) << (4 * q4) | (x.y > t ? 2u : 0u) << (4 * q4) |
+                  (x.z > t ? 4u : 0u) << (4 * q4) | (x.w > t ? 8u : 0u) << (4 * q4);
+        }
+      }
+      const uint32_t ql = meta & 63, g = meta >> 6 & 1, h = ql >> 5;
+      const uint32_t nj = 0xFFFFFFFFu - ((meta >> 7) * 32u + 4u * h);
+      uint64_t* dst = a.cand + ((wave_row0 + g * 32 + (ql & 31)) * 2 + h) * a.caph;
+      while (mask) {
+        const uint32_t v = __builtin_ctz(mask);
+        mask &= mask - 1;
+        const float sc = stage[wave][slot][(((v >> 2) ^ (uint32_t)((slot >> 2) & 3)) << 2) | (v & 3u)];
+        const uint32_t pos = atomicAdd(&cnt_lds[wave][g * 64 + ql], 1u);
+        if (pos < (uint32_t)a.caph)
+          dst[pos] = ((uint64_t)__float_as_uint(sc) << 32) | (uint64_t)(nj - (8u * (v >> 2) + (v & 3u)));
+      }
+    }
+    scount = 0;
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+  };
+  auto filter = [&](int g, const f32x16& acc, int64_t t, int rb) {
+    const bool dirty = block_max(acc) > tau[g];
+    const uint64_t bal = __ballot(dirty);
+    if (bal == 0) return;
+    if (dirty) {
+      const int rank = __builtin_amdgcn_mbcnt_hi((uint32_t)(bal >> 32), __builtin_amdgcn_mbcnt_lo((uint32_t)bal, 0u));
+      const int slot = scount + rank;
+      float4* sp = (float4*)&stage[wave][slot][0];
+      const int sw = (slot >> 2) & 3;
+      sp[0 ^ sw] = make_float4(acc[0], acc[1], acc[2], acc[3]);
+      sp[1 ^ sw] = make_float4(acc[4], acc[5], acc[6], acc[7]);
+      sp[2 ^ sw] = make_float4(acc[8], acc[9], acc[10], acc[11]);
+      sp[3 ^ sw] = make_float4(acc[12], acc[13], acc[14], acc[15]);
+      stage_meta[wave][slot] = (uint32_t)((t * KT + rb * 32) / 32) << 7 | (uint32_t)(g << 6) | (uint32_t)lane;
+    }
+    scount += __popcll(bal);
+    if (scount > STAGE_CAP - 64) drain();
+  };
+  pipeline(ntiles, 1, [&](int64_t t, const unsigned char* kb) {
+    if (tail && t == ntiles - 1) {
+#pragma unroll 1
+      for (int rb = 0; rb < NRB; ++rb) {
+        f32x16 acc0, acc1;
+        block_scores(kb, rb, acc0, acc1);
+        const int64_t jb = t * KT + rb * 32 + 4 * half;
+        mask_keys(acc0, jb);
+        mask_keys(acc1, jb);
+        filter(0, acc0, t, rb);
+        filter(1, acc1, t, rb);
+      }
+    } else {
+      // the next block's MFMAs are issued before this block is filtered, so the
+      // matrix core works while the filter runs
+      f32x16 c0, c1;
+      block_scores(kb, 0, c0, c1);
 #pragma unroll
-      for (int v = 0; v < 16; ++v) {
-        if (acc[v] > tau) {
-          if (cnt < a.caph) mybuf[cnt] = make_key(acc[v], (uint32_t)(jb + 8 * (v >> 2) + (v & 3)));
-          ++cnt;
+      for (int rb = 0; rb < NRB; ++rb) {
+        f32x16 n0, n1;
+        if (rb + 1 < NRB) block_scores(kb, rb + 1, n0, n1);
+        filter(0, c0, t, rb);
+        filter(1, c1, t, rb);
+        if (rb + 1 < NRB) {
+          c0 = n0;
+          c1 = n1;
         }
       }
     }
-  }
-  if (row_ok) a.cnt[p * 2 + half] = cnt;
+  });
+  drain();
+#pragma unroll
+  for (int g = 0; g < 2; ++g)
+    if (ok[g]) a.cnt[(wave_row0 + g * 32 + n) * 2 + half] = (int32_t)cnt_lds[wave][g * 64 + lane];
 }
 
 // ------------------------------------------------------------------ fused path: select
@@ -414,34 +557,115 @@ __global__ __launch_bounds__(64) void k_cand_select(Problem pb, Pass ps, PassBuf
   }
   const uint64_t* b0 = bufs.cand + (2 * p) * bufs.caph;
   const uint64_t* b1 = b0 + bufs.caph;
-  auto getkey = [&](int64_t e) { return e < c0 ? b0[e] : b1[e - c0]; };
+  auto getkey = [&](int64_t e) {  // raw (score bits, ~key) -> (ord(score), ~key)
+    const uint64_t wd = e < c0 ? b0[e] : b1[e - c0];
+    return ((uint64_t)ord_u32(__uint_as_float((uint32_t)(wd >> 32))) << 32) | (wd & 0xFFFFFFFFull);
+  };
   team_topk<64>(getkey, c0 + c1, k_eff, (uint32_t)pb.k, sbuf, pow2_at_least(k_eff), hist, misc,
                 bufs.sel + p * pb.k);
 }
 
 // ------------------------------------------------------------------ fused path: fallback
-// Exact recomputation of the rows on the redo list: fp32 dot products of the row
-// against every valid key into a per-block row buffer, then the same radix select.
+// Exact recomputation of the rows on the redo list (candidate buffer overflow, or
+// a threshold that turned out above the row's k-th score). The first REDO_CAP rows
+// are spread over many workgroups: fp32 dot products of each row against every
+// valid key (key splits of REDO_SPLIT keys per work item) into a row buffer, then
+// one workgroup per row runs the radix select. Rows beyond REDO_CAP (only when the
+// threshold fails wholesale, e.g. adversarially ordered scores) take the slower
+// one-workgroup-per-row kernel.
 template <typename T>
-__global__ __launch_bounds__(256) void k_redo(Problem pb, Pass ps, PassBufs bufs) {
+__device__ __forceinline__ void load8(const T* p, float (&x)[8]);
+template <>
+__device__ __forceinline__ void load8<uint16_t>(const uint16_t* p, float (&x)[8]) {
+  const uint4 v = *(const uint4*)p;
+  const uint32_t w[4] = {v.x, v.y, v.z, v.w};
+#pragma unroll
+  for (int e = 0; e < 4; ++e) {
+    x[2 * e] = __uint_as_float(w[e] << 16);
+    x[2 * e + 1] = __uint_as_float(w[e] & 0xFFFF0000u);
+  }
+}
+template <>
+__device__ __forceinline__ void load8<float>(const float* p, float (&x)[8]) {
+  const float4 u = *(const float4*)p, v = *(const float4*)(p + 4);
+  x[0] = u.x; x[1] = u.y; x[2] = u.z; x[3] = u.w;
+  x[4] = v.x; x[5] = v.y; x[6] = v.z; x[7] = v.w;
+}
+
+template <typename T>
+__global__ __launch_bounds__(256) void k_redo_scores(Problem pb, Pass ps, PassBufs bufs) {
+  __shared__ float qrow[1024];
+  const int32_t total = *bufs.redo_count;
+  const int64_t rows = total < REDO_CAP ? total : REDO_CAP;
+  const int64_t splits = (pb.Lk + REDO_SPLIT - 1) / REDO_SPLIT;
+  for (int64_t item = blockIdx.x; item < rows * splits; item += gridDim.x) {
+    const int64_t r = item / splits, sp = item - r * splits;
+    const int64_t p = bufs.redo_list[r];
+    const RowRef rr = row_of(pb, ps, p);
+    const int64_t nv = valid_keys(pb, rr.i);
+    const T* q = (const T*)pb.Q + (rr.bh * pb.Lq + rr.i) * pb.d;
+    for (int f = threadIdx.x; f < pb.d; f += 256) qrow[f] = load_elem<T>(q, f);
+    __syncthreads();
+    const T* Kh = (const T*)pb.K + rr.bh * pb.kv_head_stride;
+    float* row = bufs.scores + r * pb.Lk;
+    const int64_t j1 = (sp + 1) * REDO_SPLIT < nv ? (sp + 1) * REDO_SPLIT : nv;
+    for (int64_t j = sp * REDO_SPLIT + threadIdx.x; j < j1; j += 256) {
+      const T* kr = Kh + j * pb.d;
+      float acc = 0.f;
+      for (int64_t f = 0; f < pb.d; f += 8) {
+        float x[8];
+        load8<T>(kr + f, x);
+#pragma unroll
+        for (int e = 0; e < 8; ++e) acc = fmaf(qrow[f + e], x[e], acc);
+      }
+      row[j] = acc;
+    }
+    __syncthreads();
+  }
+}
+
+__global__ __launch_bounds__(256) void k_redo_select(Problem pb, Pass ps, PassBufs bufs) {
+  extern __shared__ uint64_t sbuf[];
+  __shared__ uint32_t hist[256];
+  __shared__ uint32_t misc[8];
+  const int64_t r = blockIdx.x;
+  if (r >= *bufs.redo_count) return;
+  const int64_t p = bufs.redo_list[r];
+  const RowRef rr = row_of(pb, ps, p);
+  const int64_t nv = valid_keys(pb, rr.i);
+  const uint32_t k_eff = (uint32_t)(pb.k < nv ? pb.k : nv);
+  const float* row = bufs.scores + r * pb.Lk;
+  auto getkey = [&](int64_t e) { return make_key(row[e], (uint32_t)e); };
+  team_topk<256>(getkey, nv, k_eff, (uint32_t)pb.k, sbuf, pow2_at_least(k_eff), hist, misc, bufs.sel + p * pb.k);
+}
+
+template <typename T>
+__global__ __launch_bounds__(256) void k_redo_rest(Problem pb, Pass ps, PassBufs bufs) {
   extern __shared__ uint64_t sbuf[];
   __shared__ uint32_t hist[256];
   __shared__ uint32_t misc[8];
   __shared__ float qrow[1024];
-  float* row = bufs.scores + (int64_t)blockIdx.x * pb.Lk;
+  float* row = bufs.scores + ((int64_t)REDO_CAP + blockIdx.x) * pb.Lk;
   const int32_t total = *bufs.redo_count;
-  for (int32_t t = blockIdx.x; t < total; t += gridDim.x) {
+  for (int32_t t = REDO_CAP + blockIdx.x; t < total; t += gridDim.x) {
     const int64_t p = bufs.redo_list[t];
     const RowRef rr = row_of(pb, ps, p);
     const int64_t nv = valid_keys(pb, rr.i);
     const uint32_t k_eff = (uint32_t)(pb.k < nv ? pb.k : nv);
-    for (int f = threadIdx.x; f < pb.d; f += 256) qrow[f] = load_elem<T>(pb.Q, (rr.bh * pb.Lq + rr.i) * pb.d + f);
+    const T* q = (const T*)pb.Q + (rr.bh * pb.Lq + rr.i) * pb.d;
+    for (int f = threadIdx.x; f < pb.d; f += 256) qrow[f] = load_elem<T>(q, f);
     __syncthreads();
-    const char* Kh = (const char*)pb.K + rr.bh * pb.kv_head_stride * (int64_t)sizeof(T);
+    const T* Kh = (const T*)pb.K + rr.bh * pb.kv_head_stride;
     for (int64_t j = threadIdx.x; j < nv; j += 256) {
-      float s = 0.f;
-      for (int64_t f = 0; f < pb.d; ++f) s = fmaf(qrow[f], load_elem<T>(Kh, j * pb.d + f), s);
-      row[j] = s;
+      const T* kr = Kh + j * pb.d;
+      float acc = 0.f;
+      for (int64_t f = 0; f < pb.d; f += 8) {
+        float x[8];
+        load8<T>(kr + f, x);
+#pragma unroll
+        for (int e = 0; e < 8; ++e) acc = fmaf(qrow[f + e], x[e], acc);
+      }
+      row[j] = acc;
     }
     __syncthreads();
     auto getkey = [&](int64_t e) { return make_key(row[e], (uint32_t)e); };
@@ -566,7 +790,7 @@ hipError_t launch_fused_scan(const Problem& pb, const Pass& ps, const PassBufs& 
   a.kv_head_stride = pb.kv_head_stride;
   a.c0 = ps.c0;
   a.nchunk = ps.nchunk;
-  a.wgs_per_chunk = (pb.C + 127) / 128;
+  a.wgs_per_chunk = (pb.C + 255) / 256;
   a.cand = b.cand;
   a.cnt = b.cnt;
   a.caph = b.caph;
@@ -575,13 +799,13 @@ hipError_t launch_fused_scan(const Problem& pb, const Pass& ps, const PassBufs& 
   const unsigned grid = (unsigned)(ps.nc * a.wgs_per_chunk);
 #define TOPK_SCAN(D_, R_) k_fused_scan<D_, R_><<<grid, 256, 0, st>>>(a)
   if (pb.d == 64) {
-    if (cfg.R == 4) TOPK_SCAN(64, 4);
-    else if (cfg.R == 8) TOPK_SCAN(64, 8);
-    else TOPK_SCAN(64, 16);
+    if (cfg.R == 3) TOPK_SCAN(64, 3);
+    else if (cfg.R == 6) TOPK_SCAN(64, 6);
+    else TOPK_SCAN(64, 12);
   } else {
-    if (cfg.R == 4) TOPK_SCAN(128, 4);
-    else if (cfg.R == 8) TOPK_SCAN(128, 8);
-    else TOPK_SCAN(128, 16);
+    if (cfg.R == 3) TOPK_SCAN(128, 3);
+    else if (cfg.R == 6) TOPK_SCAN(128, 6);
+    else TOPK_SCAN(128, 12);
   }
 #undef TOPK_SCAN
   return hipGetLastError();
@@ -593,11 +817,16 @@ hipError_t launch_cand_select(const Problem& pb, const Pass& ps, const PassBufs&
 }
 
 hipError_t launch_redo(const Problem& pb, const Pass& ps, const PassBufs& b, hipStream_t st) {
-  const int P = pow2_at_least(pb.k);
-  if (pb.dtype == T_BF16)
-    k_redo<uint16_t><<<REDO_BLOCKS, 256, (size_t)P * 8, st>>>(pb, ps, b);
-  else
-    k_redo<float><<<REDO_BLOCKS, 256, (size_t)P * 8, st>>>(pb, ps, b);
+  const size_t P8 = (size_t)pow2_at_least(pb.k) * 8;
+  if (pb.dtype == T_BF16) {
+    k_redo_scores<uint16_t><<<REDO_SCORE_BLOCKS, 256, 0, st>>>(pb, ps, b);
+    k_redo_select<<<REDO_CAP, 256, P8, st>>>(pb, ps, b);
+    k_redo_rest<uint16_t><<<REDO_BLOCKS, 256, P8, st>>>(pb, ps, b);
+  } else {
+    k_redo_scores<float><<<REDO_SCORE_BLOCKS, 256, 0, st>>>(pb, ps, b);
+    k_redo_select<<<REDO_CAP, 256, P8, st>>>(pb, ps, b);
+    k_redo_rest<float><<<REDO_BLOCKS, 256, P8, st>>>(pb, ps, b);
+  }
   return hipGetLastError();
 }
 
