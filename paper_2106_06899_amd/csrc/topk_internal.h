@@ -18,7 +18,7 @@ constexpr int REDO_CAP = 1024;          // redo rows recomputed by the wide fall
 constexpr int REDO_SPLIT = 2048;        // keys per work item of the wide fallback
 constexpr int REDO_SCORE_BLOCKS = 512;  // workgroups of the wide fallback's score kernel
 constexpr int REDO_BLOCKS = 64;         // workgroups of the fallback for rows beyond REDO_CAP
-constexpr int MAX_SELECT_K = 4096;  // largest k the workgroup select / finalize handle
+constexpr int MAX_SELECT_K = 2048;  // largest k the workgroup select / finalize handle
 
 // One call's problem. Attention: BH heads; the FFN is one head whose keys/values
 // are W1/W2 (kv_head_stride = 0). Rows of Q/out are (bh * Lq + i); keys (bh, j) sit

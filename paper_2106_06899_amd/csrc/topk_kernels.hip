@@ -540,29 +540,170 @@ __global__ __launch_bounds__(256, D == 64 ? 3 : 2) void k_fused_scan(ScanArgs a)
 // ------------------------------------------------------------------ fused path: select
 // One wave per row. A row whose candidates overflowed, or (threshold mode) hold
 // fewer than k_eff keys, goes to the redo list; otherwise the candidate set is
-// proven to contain the row's top-k and an exact select runs over it.
-__global__ __launch_bounds__(64) void k_cand_select(Problem pb, Pass ps, PassBufs bufs) {
-  __shared__ uint64_t sbuf[256];
-  __shared__ uint32_t hist[256];
-  __shared__ uint32_t misc[8];
-  const int64_t p = blockIdx.x;
+// proven to contain the row's top-k and an exact select runs over it:
+//  * the candidates (at most 2 * caph <= CAND_REGS * 64) are read once into
+//    registers as order-preserving keys;
+//  * the key bytes shared by every candidate are skipped (min/max reduction), and
+//    radix passes of 8 bits find the k_eff-th largest key; the pass's digit is
+//    broadcast with ballot/shuffle, only the histogram lives in LDS;
+//  * the selected keys are compacted with mbcnt and sorted (descending) by a
+//    bitonic network on registers, E = P/64 keys per lane.
+constexpr int CAND_REGS = 16;
+
+__device__ __forceinline__ uint64_t shfl_xor_u64(uint64_t x, int m) {
+  const uint32_t lo = __shfl_xor((uint32_t)x, m, 64), hi = __shfl_xor((uint32_t)(x >> 32), m, 64);
+  return ((uint64_t)hi << 32) | lo;
+}
+
+// Bitonic sort, descending, of 64*E keys held as r[e] = element (e*64 + lane).
+template <int E>
+__device__ __forceinline__ void wave_sort_desc(uint64_t (&r)[E]) {
+  const int lane = threadIdx.x & 63;
+  constexpr int P = 64 * E;
+  for (int size = 2; size <= P; size <<= 1) {
+    for (int stride = size >> 1; stride > 0; stride >>= 1) {
+      if (stride >= 64) {  // partners in the same lane, other register
+        const int rs = stride / 64;
+#pragma unroll
+        for (int e = 0; e < E; ++e) {
+          if ((e & rs) == 0) {
+            const int i = e * 64 + lane;
+            const bool desc = (i & size) == 0;
+            const uint64_t x = r[e], y = r[e + rs];
+            if ((x < y) == desc) {
+              r[e] = y;
+              r[e + rs] = x;
+            }
+          }
+        }
+      } else {  // partners in another lane, same register
+#pragma unroll
+        for (int e = 0; e < E; ++e) {
+          const int i = e * 64 + lane;
+          const uint64_t y = shfl_xor_u64(r[e], stride);
+          const bool desc = (i & size) == 0;
+          const bool lower = (lane & stride) == 0;
+          // the lower element of a pair keeps the larger key when descending
+          const bool keep_max = lower == desc;
+          r[e] = keep_max ? (r[e] > y ? r[e] : y) : (r[e] < y ? r[e] : y);
+        }
+      }
+    }
+  }
+}
+
+template <int E>
+__device__ __forceinline__ void wave_sort_store(const uint64_t* sbuf, uint32_t k_eff, int64_t k, uint64_t* out) {
+  const int lane = threadIdx.x & 63;
+  uint64_t r[E];
+#pragma unroll
+  for (int e = 0; e < E; ++e) r[e] = (uint32_t)(e * 64 + lane) < k_eff ? sbuf[e * 64 + lane] : 0ull;
+  wave_sort_desc<E>(r);
+#pragma unroll
+  for (int e = 0; e < E; ++e)
+    if (e * 64 + lane < k) out[e * 64 + lane] = r[e];
+}
+
+__device__ __forceinline__ void cand_select_row(const Problem& pb, const Pass& ps, const PassBufs& bufs, int64_t p,
+                                                uint64_t* sbuf, uint32_t* hist) {
   const RowRef rr = row_of(pb, ps, p);
   if (!rr.ok) return;
   const int64_t nv = valid_keys(pb, rr.i);
   const uint32_t k_eff = (uint32_t)(pb.k < nv ? pb.k : nv);
   const int64_t c0 = bufs.cnt[2 * p], c1 = bufs.cnt[2 * p + 1];
-  if (c0 > bufs.caph || c1 > bufs.caph || c0 + c1 < (int64_t)k_eff || k_eff > 256) {
-    if (threadIdx.x == 0) bufs.redo_list[atomicAdd(bufs.redo_count, 1)] = (int32_t)p;
+  if (c0 > bufs.caph || c1 > bufs.caph || c0 + c1 < (int64_t)k_eff || k_eff > 256 ||
+      c0 + c1 > 64 * CAND_REGS) {
+    if ((threadIdx.x & 63) == 0) bufs.redo_list[atomicAdd(bufs.redo_count, 1)] = (int32_t)p;
     return;
   }
+  const int lane = threadIdx.x & 63;
+  const int n = (int)(c0 + c1);
   const uint64_t* b0 = bufs.cand + (2 * p) * bufs.caph;
   const uint64_t* b1 = b0 + bufs.caph;
-  auto getkey = [&](int64_t e) {  // raw (score bits, ~key) -> (ord(score), ~key)
-    const uint64_t wd = e < c0 ? b0[e] : b1[e - c0];
-    return ((uint64_t)ord_u32(__uint_as_float((uint32_t)(wd >> 32))) << 32) | (wd & 0xFFFFFFFFull);
-  };
-  team_topk<64>(getkey, c0 + c1, k_eff, (uint32_t)pb.k, sbuf, pow2_at_least(k_eff), hist, misc,
-                bufs.sel + p * pb.k);
+  uint64_t key[CAND_REGS];
+  uint64_t kmin = ~0ull, kmax = 0ull;
+#pragma unroll
+  for (int e = 0; e < CAND_REGS; ++e) {
+    const int i = lane + 64 * e;
+    uint64_t wd = 0;
+    if (i < n) wd = i < c0 ? b0[i] : b1[i - c0];
+    key[e] = ((uint64_t)ord_u32(__uint_as_float((uint32_t)(wd >> 32))) << 32) | (wd & 0xFFFFFFFFull);
+    if (i < n) {
+      kmin = key[e] < kmin ? key[e] : kmin;
+      kmax = key[e] > kmax ? key[e] : kmax;
+    }
+  }
+#pragma unroll
+  for (int off = 32; off > 0; off >>= 1) {
+    const uint64_t a0 = shfl_xor_u64(kmin, off), a1 = shfl_xor_u64(kmax, off);
+    kmin = a0 < kmin ? a0 : kmin;
+    kmax = a1 > kmax ? a1 : kmax;
+  }
+  // bytes above the highest differing bit are common to every candidate
+  const uint64_t diff = kmin ^ kmax;
+  int shift = diff == 0 ? 8 : ((63 - __builtin_clzll(diff)) / 8 + 1) * 8;
+  uint64_t prefix = (shift >= 64) ? 0 : (kmax >> shift) << shift;
+  uint32_t kr = k_eff;
+  while (shift > 0 && kr < (uint32_t)n) {
+    shift -= 8;
+    reinterpret_cast<uint4*>(hist)[lane] = make_uint4(0u, 0u, 0u, 0u);
+    __syncthreads();
+    const uint64_t pre_hi = shift + 8 >= 64 ? 0 : prefix >> (shift + 8);
+#pragma unroll
+    for (int e = 0; e < CAND_REGS; ++e) {
+      const bool match = lane + 64 * e < n && (shift + 8 >= 64 || (key[e] >> (shift + 8)) == pre_hi);
+      if (match) atomicAdd(&hist[(uint32_t)(key[e] >> shift) & 255u], 1u);
+    }
+    __syncthreads();
+    const uint4 h4 = reinterpret_cast<const uint4*>(hist)[63 - lane];  // bins 255-4l .. 252-4l
+    const uint32_t c4[4] = {h4.w, h4.z, h4.y, h4.x};                   // descending digit order
+    const uint32_t local = c4[0] + c4[1] + c4[2] + c4[3];
+    uint32_t run = team_excl_scan<64>(local, nullptr);
+    uint32_t digit = 0, above = 0, cnt = 0;
+    bool here = false;
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      if (!here && run < kr && kr <= run + c4[e]) {
+        here = true;
+        digit = 255u - (uint32_t)(lane * 4 + e);
+        above = run;
+        cnt = c4[e];
+      }
+      run += c4[e];
+    }
+    const uint64_t who = __ballot(here);
+    const int src = __builtin_ctzll(who);
+    digit = __shfl(digit, src, 64);
+    above = __shfl(above, src, 64);
+    cnt = __shfl(cnt, src, 64);
+    __syncthreads();  // hist is cleared again by the next pass
+    prefix |= (uint64_t)digit << shift;
+    kr -= above;
+    if (cnt == kr) break;  // every key of this bucket is selected
+  }
+  // selected: (key >> shift) >= (prefix >> shift); compact them into sbuf
+  const uint64_t lim = prefix >> shift;
+  int base = 0;
+#pragma unroll
+  for (int e = 0; e < CAND_REGS; ++e) {
+    const bool take = lane + 64 * e < n && (key[e] >> shift) >= lim;
+    const uint64_t m = __ballot(take);
+    const int pos = base + (int)__builtin_amdgcn_mbcnt_hi((uint32_t)(m >> 32), __builtin_amdgcn_mbcnt_lo((uint32_t)m, 0u));
+    if (take && pos < 256) sbuf[pos] = key[e];
+    base += __popcll(m);
+  }
+  __syncthreads();
+  uint64_t* out = bufs.sel + p * pb.k;
+  if (k_eff <= 64) wave_sort_store<1>(sbuf, k_eff, pb.k, out);
+  else if (k_eff <= 128) wave_sort_store<2>(sbuf, k_eff, pb.k, out);
+  else wave_sort_store<4>(sbuf, k_eff, pb.k, out);
+  for (int64_t t = lane + 64 * (k_eff <= 64 ? 1 : k_eff <= 128 ? 2 : 4); t < pb.k; t += 64) out[t] = 0ull;
+}
+
+__global__ __launch_bounds__(64) void k_cand_select(Problem pb, Pass ps, PassBufs bufs) {
+  __shared__ uint64_t sbuf[256];
+  __shared__ uint32_t hist[256];
+  cand_select_row(pb, ps, bufs, blockIdx.x, sbuf, hist);
 }
 
 // ------------------------------------------------------------------ fused path: fallback
@@ -676,20 +817,53 @@ __global__ __launch_bounds__(256) void k_redo_rest(Problem pb, Pass ps, PassBufs
 
 // ------------------------------------------------------------------ finalize
 // One wave per row: activation over the k_eff survivors (softmax with the Eq. 1
-// temperature, or ReLU), then the weighted sum of the selected value rows.
+// temperature, or ReLU), then the weighted sum of the selected value rows. Value
+// rows are read as 16-byte vectors: with NV vectors per row, 64/NV rows are
+// gathered per wave instruction (d = 64 bf16: 8 rows), each lane accumulating its
+// vector's columns in fp32; the row slots are then reduced across lanes.
+template <typename T> struct Vec16;
+template <> struct Vec16<uint16_t> {
+  static constexpr int E = 8;
+  static __device__ __forceinline__ void load(const uint16_t* p, float (&x)[8]) {
+    const uint4 v = *(const uint4*)p;
+    const uint32_t w[4] = {v.x, v.y, v.z, v.w};
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      x[2 * e] = __uint_as_float(w[e] << 16);
+      x[2 * e + 1] = __uint_as_float(w[e] & 0xFFFF0000u);
+    }
+  }
+  static __device__ __forceinline__ void store(uint16_t* p, const float (&x)[8]) {
+    uint32_t w[4];
+#pragma unroll
+    for (int e = 0; e < 4; ++e) w[e] = (uint32_t)f32_to_bf16(x[2 * e]) | ((uint32_t)f32_to_bf16(x[2 * e + 1]) << 16);
+    *(uint4*)p = make_uint4(w[0], w[1], w[2], w[3]);
+  }
+};
+template <> struct Vec16<float> {
+  static constexpr int E = 4;
+  static __device__ __forceinline__ void load(const float* p, float (&x)[4]) {
+    const float4 v = *(const float4*)p;
+    x[0] = v.x; x[1] = v.y; x[2] = v.z; x[3] = v.w;
+  }
+  static __device__ __forceinline__ void store(float* p, const float (&x)[4]) {
+    *(float4*)p = make_float4(x[0], x[1], x[2], x[3]);
+  }
+};
+
 template <typename T>
-__global__ __launch_bounds__(64) void k_finalize(Problem pb, Pass ps, const uint64_t* sel) {
-  extern __shared__ float fsh[];
-  float* w = fsh;
-  uint32_t* jj = (uint32_t*)(fsh + pb.k);
-  const int64_t p = blockIdx.x;
+__device__ __forceinline__ void finalize_row(const Problem& pb, const Pass& ps, const uint64_t* sel, int64_t p,
+                                             float* w, uint32_t* jj) {
+  constexpr int E = Vec16<T>::E;
   const RowRef rr = row_of(pb, ps, p);
   if (!rr.ok) return;
+  const int lane = threadIdx.x & 63;
   const int64_t nv = valid_keys(pb, rr.i);
   const int64_t k_eff = pb.k < nv ? pb.k : nv;
   const int64_t grow = rr.bh * pb.Lq + rr.i;
   const uint64_t* srow = sel + p * pb.k;
-  for (int64_t t = threadIdx.x; t < pb.k; t += 64) {
+  const uint32_t jmax = (uint32_t)(pb.Lk - 1);
+  for (int64_t t = lane; t < pb.k; t += 64) {
     float s = -INFINITY;
     int32_t j = -1;
     if (t < k_eff) {
@@ -697,7 +871,7 @@ __global__ __launch_bounds__(64) void k_finalize(Problem pb, Pass ps, const uint
       s = key_score(key);
       j = (int32_t)key_index(key);
       w[t] = s;
-      jj[t] = (uint32_t)j;
+      jj[t] = (uint32_t)j < jmax ? (uint32_t)j : jmax;  // keeps a bad selection from reading out of bounds
     }
     if (pb.idx_out) pb.idx_out[grow * pb.k + t] = j;
     if (pb.score_out) pb.score_out[grow * pb.k + t] = s;
@@ -708,7 +882,7 @@ __global__ __launch_bounds__(64) void k_finalize(Problem pb, Pass ps, const uint
     const float m = w[0];
     const float c = pb.scale * 1.4426950408889634f;  // exp(x) = exp2(x * log2 e)
     float sum = 0.f;
-    for (int64_t t = threadIdx.x; t < k_eff; t += 64) {
+    for (int64_t t = lane; t < k_eff; t += 64) {
       const float e = exp2f((w[t] - m) * c);
       w[t] = e;
       sum += e;
@@ -717,19 +891,61 @@ __global__ __launch_bounds__(64) void k_finalize(Problem pb, Pass ps, const uint
     for (int off = 32; off > 0; off >>= 1) sum += __shfl_xor(sum, off, 64);
     inv = 1.f / sum;
   } else {
-    for (int64_t t = threadIdx.x; t < k_eff; t += 64) w[t] = fmaxf(w[t], 0.f);
+    for (int64_t t = lane; t < k_eff; t += 64) w[t] = fmaxf(w[t], 0.f);
   }
   __syncthreads();
-  const char* Vh = (const char*)pb.V + rr.bh * pb.kv_head_stride * (int64_t)sizeof(T);
-  const uint32_t jmax = (uint32_t)(pb.Lk - 1);
-  for (int64_t col = threadIdx.x; col < pb.d; col += 64) {
-    float acc = 0.f;
-    for (int64_t t = 0; t < k_eff; ++t) {
-      const uint32_t j = jj[t] < jmax ? jj[t] : jmax;  // keeps a bad selection from reading out of bounds
-      acc = fmaf(w[t], load_elem<T>(Vh, (int64_t)j * pb.d + col), acc);
+  const T* Vh = (const T*)pb.V + rr.bh * pb.kv_head_stride;
+  T* orow = (T*)pb.out + grow * pb.d;
+  const int nvec = (int)(pb.d / E);                 // 16-byte vectors per value row
+  int np2 = 1;                                      // lanes per row slot: a power of two >= nvec
+  while (np2 < nvec && np2 < 64) np2 <<= 1;
+  const int slots = 64 / np2;                       // rows gathered per instruction
+  const int vlane = lane % np2, slot = lane / np2;
+  for (int v0 = vlane; v0 < nvec; v0 += 64) {
+    float acc[E];
+#pragma unroll
+    for (int e = 0; e < E; ++e) acc[e] = 0.f;
+    {
+      int64_t t = slot;
+      for (; t + 3 * slots < k_eff; t += 4 * slots) {  // four independent gathers in flight
+        float x0[E], x1[E], x2[E], x3[E];
+        Vec16<T>::load(Vh + (int64_t)jj[t] * pb.d + v0 * E, x0);
+        Vec16<T>::load(Vh + (int64_t)jj[t + slots] * pb.d + v0 * E, x1);
+        Vec16<T>::load(Vh + (int64_t)jj[t + 2 * slots] * pb.d + v0 * E, x2);
+        Vec16<T>::load(Vh + (int64_t)jj[t + 3 * slots] * pb.d + v0 * E, x3);
+        const float w0 = w[t], w1 = w[t + slots], w2 = w[t + 2 * slots], w3 = w[t + 3 * slots];
+#pragma unroll
+        for (int e = 0; e < E; ++e) acc[e] = fmaf(w3, x3[e], fmaf(w2, x2[e], fmaf(w1, x1[e], fmaf(w0, x0[e], acc[e]))));
+      }
+      for (; t < k_eff; t += slots) {
+        float x[E];
+        Vec16<T>::load(Vh + (int64_t)jj[t] * pb.d + v0 * E, x);
+        const float wt = w[t];
+#pragma unroll
+        for (int e = 0; e < E; ++e) acc[e] = fmaf(wt, x[e], acc[e]);
+      }
     }
-    store_elem<T>(pb.out, grow * pb.d + col, acc * inv);
+    // reduce the row slots: lanes with the same vector index differ by multiples of np2
+    for (int off = np2; off < 64; off <<= 1) {
+#pragma unroll
+      for (int e = 0; e < E; ++e) acc[e] += __shfl_xor(acc[e], off, 64);
+    }
+    if (slot == 0) {
+#pragma unroll
+      for (int e = 0; e < E; ++e) acc[e] *= inv;
+      Vec16<T>::store(orow + v0 * E, acc);
+    }
   }
+}
+
+template <typename T>
+__global__ __launch_bounds__(64) void k_finalize(Problem pb, Pass ps, const uint64_t* sel) {
+  extern __shared__ float fsh[];
+  // same XCD-aware renumbering as the scan: neighbouring rows (same head, same
+  // value rows) run on one XCD
+  const int64_t G = gridDim.x, bid = blockIdx.x;
+  const int64_t p = (G % 8 == 0) ? (bid % 8) * (G / 8) + bid / 8 : bid;
+  finalize_row<T>(pb, ps, sel, p, fsh, (uint32_t*)(fsh + pb.k));
 }
 
 // ------------------------------------------------------------------ MFMA layout probe

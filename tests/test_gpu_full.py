@@ -37,10 +37,11 @@ def test_attn_full_size(name):
         assert np.all(g <= np.arange(w.Lq)[:, None]), "a causal row selected a future key"
     assert torch.isfinite(out.float()).all()
     if w.planted:
-        # generator sanity (not a parity criterion): most rows keep all 4 planted keys
+        # generator sanity (not a parity criterion): a planted key scores about
+        # |k|^2 = d above the noise, so most planted keys make the top-k
         pl = x["planted_idx"]
-        kept = np.mean([np.isin(pl[0, h, i], g[0, h, i]).all() for h in range(w.H) for i in range(0, w.Lq, 97)])
-        _say(name, "planted keys kept in", kept)
+        kept = np.mean([np.isin(pl[0, h, i], g[0, h, i]).mean() for h in range(w.H) for i in range(0, w.Lq, 97)])
+        _say(name, "fraction of planted keys kept", kept)
         assert kept > 0.8
 
 
