@@ -177,7 +177,7 @@ def main():
         "score_frac_of_bf16_peak_whole_call": score_tflops_call / PEAK_BF16_TFLOPS,
         "stage_ms_per_step": {s: stages[s][0] / args.steps for s in stages},
         "roofline": {
-            "kernel": "k_fused_scan<64,8>" if path == 1 else "k_tile_scores",
+            "kernel": f"k_fused_scan (d={w.d})" if path == 1 else "k_tile_scores",
             "bound": "mfma",
             "achieved": achieved,
             "peak": PEAK_BF16_TFLOPS,

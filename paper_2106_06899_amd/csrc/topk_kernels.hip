@@ -254,6 +254,96 @@ __global__ __launch_bounds__(256) void k_tile_scores(Problem pb, Pass ps, float*
   }
 }
 
+// ------------------------------------------------------------------ chunk-tile path: MFMA scores
+// bf16 inputs with d % 32 == 0: a 128-query x 128-key tile per workgroup, the
+// feature dimension consumed 32 at a time from LDS (double-buffered, next slice
+// prefetched into registers). Each wave owns 64 queries x 64 keys = 2 x 2 blocks of
+// v_mfma_f32_32x32x16_bf16 with A = Q (rows = queries) and B = K^T (columns =
+// keys), so lane l holds key l % 32 of a block for 16 queries and a store
+// instruction writes two 128-byte runs of a score row. Tiles entirely above the
+// causal diagonal are skipped (never read by the select).
+template <int DUMMY>
+__global__ __launch_bounds__(256, 2) void k_tile_scores_mfma(Problem pb, Pass ps, float* S) {
+  constexpr int TQ = 128, TK = 128, KS = 32;     // tile rows, tile keys, features per slice
+  constexpr int ROWB = KS * 2 + 16;               // padded LDS row: 80 bytes
+  __shared__ __attribute__((aligned(16))) unsigned char qs[2][TQ * ROWB];
+  __shared__ __attribute__((aligned(16))) unsigned char ksm[2][TK * ROWB];
+  const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63, half = lane >> 5, n = lane & 31;
+  const int64_t key0 = (int64_t)blockIdx.x * TK, r0 = (int64_t)blockIdx.y * TQ, cl = blockIdx.z;
+  const int64_t id = ps.c0 + cl, bh = id / ps.nchunk, c = id - bh * ps.nchunk, i0 = c * pb.C;
+  if (r0 >= pb.C || i0 + r0 >= pb.Lq) return;
+  if (pb.causal) {
+    const int64_t last = r0 + TQ - 1 < pb.C ? r0 + TQ - 1 : pb.C - 1;
+    if (key0 > i0 + last) return;
+  }
+  const int64_t d = pb.d;
+  const uint16_t* Qb = (const uint16_t*)pb.Q;
+  const uint16_t* Kh = (const uint16_t*)pb.K + bh * pb.kv_head_stride;
+  // global -> register -> LDS: each thread moves 2 x 16 bytes of Q and of K per slice
+  uint4 pq[2], pk[2];
+  auto issue = [&](int64_t f0) {
+#pragma unroll
+    for (int e = 0; e < 2; ++e) {
+      const int cidx = tid + 256 * e, row = cidx >> 2, part = cidx & 3;  // 4 pieces of 16 B per row
+      const int64_t lr = r0 + row, i = i0 + lr, key = key0 + row;
+      pq[e] = (lr < pb.C && i < pb.Lq) ? *(const uint4*)(Qb + (bh * pb.Lq + i) * d + f0 + part * 8)
+                                       : make_uint4(0u, 0u, 0u, 0u);
+      pk[e] = key < pb.Lk ? *(const uint4*)(Kh + key * d + f0 + part * 8) : make_uint4(0u, 0u, 0u, 0u);
+    }
+  };
+  auto stash = [&](int buf) {
+#pragma unroll
+    for (int e = 0; e < 2; ++e) {
+      const int cidx = tid + 256 * e, row = cidx >> 2, part = cidx & 3;
+      *(uint4*)(&qs[buf][row * ROWB + part * 16]) = pq[e];
+      *(uint4*)(&ksm[buf][row * ROWB + part * 16]) = pk[e];
+    }
+  };
+  const int wq = (wave >> 1) * 64, wk = (wave & 1) * 64;  // this wave's 64 x 64 sub-tile
+  f32x16 acc[2][2];
+#pragma unroll
+  for (int a = 0; a < 2; ++a)
+#pragma unroll
+    for (int b = 0; b < 2; ++b) acc[a][b] = (f32x16){};
+  const int64_t nsl = d / KS;
+  issue(0);
+  for (int64_t sl = 0; sl < nsl; ++sl) {
+    const int buf = (int)(sl & 1);
+    stash(buf);
+    __syncthreads();
+    if (sl + 1 < nsl) issue((sl + 1) * KS);
+#pragma unroll
+    for (int st = 0; st < KS / 16; ++st) {
+      bf16x8 av[2], bv[2];
+#pragma unroll
+      for (int a = 0; a < 2; ++a)
+        av[a] = *(const bf16x8*)(&qs[buf][(wq + a * 32 + n) * ROWB + st * 32 + half * 16]);
+#pragma unroll
+      for (int b = 0; b < 2; ++b)
+        bv[b] = *(const bf16x8*)(&ksm[buf][(wk + b * 32 + n) * ROWB + st * 32 + half * 16]);
+#pragma unroll
+      for (int a = 0; a < 2; ++a)
+#pragma unroll
+        for (int b = 0; b < 2; ++b) acc[a][b] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(av[a], bv[b], acc[a][b], 0, 0, 0);
+    }
+  }
+  // D[m][n]: m = query row 8*(v/4) + 4*half + v%4 of the block, n = key lane%32
+#pragma unroll
+  for (int a = 0; a < 2; ++a) {
+#pragma unroll
+    for (int v = 0; v < 16; ++v) {
+      const int64_t lr = r0 + wq + a * 32 + 8 * (v >> 2) + 4 * half + (v & 3), i = i0 + lr;
+      if (lr >= pb.C || i >= pb.Lq) continue;
+      const int64_t nv = valid_keys(pb, i);
+#pragma unroll
+      for (int b = 0; b < 2; ++b) {
+        const int64_t key = key0 + wk + b * 32 + n;
+        if (key < nv) S[(cl * pb.C + lr) * pb.Lk + key] = acc[a][b][v];
+      }
+    }
+  }
+}
+
 // ------------------------------------------------------------------ chunk-tile path: select
 __global__ __launch_bounds__(256) void k_tile_select(Problem pb, Pass ps, const float* S, uint64_t* sel) {
   extern __shared__ uint64_t sbuf[];
@@ -981,6 +1071,11 @@ hipError_t launch_init(const PassBufs& b, hipStream_t st) {
 }
 
 hipError_t launch_tile_scores(const Problem& pb, const Pass& ps, const PassBufs& b, hipStream_t st) {
+  if (pb.dtype == T_BF16 && pb.d % 32 == 0) {
+    dim3 g((unsigned)((pb.Lk + 127) / 128), (unsigned)((pb.C + 127) / 128), (unsigned)ps.nc);
+    k_tile_scores_mfma<0><<<g, 256, 0, st>>>(pb, ps, b.scores);
+    return hipGetLastError();
+  }
   dim3 grid((unsigned)((pb.Lk + 63) / 64), (unsigned)((pb.C + 63) / 64), (unsigned)ps.nc);
   if (pb.dtype == T_BF16)
     k_tile_scores<uint16_t><<<grid, 256, 0, st>>>(pb, ps, b.scores);
