@@ -59,6 +59,7 @@ struct ScanCfg {
   int mode;           // ScanMode
   int stride;         // SAMPLE: one key tile in `stride` is sampled
   int R;              // SAMPLE: order statistic kept per lane (3, 6 or 12)
+  int groups;         // 32-query groups per wave (2, or 4 when d = 64)
 };
 
 hipError_t launch_init(const PassBufs& b, hipStream_t st);

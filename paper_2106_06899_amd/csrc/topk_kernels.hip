@@ -360,23 +360,26 @@ __global__ __launch_bounds__(256) void k_tile_select(Problem pb, Pass ps, const 
 }
 
 // ------------------------------------------------------------------ fused path: scan
-// One workgroup = 4 waves x 64 queries of one head. Each wave keeps the B operand
-// of two 32-query column groups (its 64 queries x d) in registers; key tiles are
-// staged in LDS (two buffers, the next tile prefetched into registers while the
-// current one is consumed). Each wave computes S^T = K Q^T with
-// v_mfma_f32_32x32x16_bf16, so lane l holds 16 keys' scores of query l % 32 of a
-// group (keys 8*(v/4) + 4*(l/32) + v%4 of the 32-key block, v = 0..15); one LDS
-// read of the K operand feeds both groups. The feature dimension is split between
+// One workgroup = 4 waves x 32*G queries of one head (G = 2). Each wave keeps the B operand
+// of G 32-query column groups in registers; key tiles of 64 keys stream through a
+// ring of SCAN_NB LDS buffers that are filled by direct global-to-LDS loads issued
+// SCAN_NB - 1 tiles ahead (no register staging). Each wave computes S^T = K Q^T
+// with v_mfma_f32_32x32x16_bf16, so lane l holds 16 keys' scores of query l % 32 of
+// a group (keys 8*(v/4) + 4*(l/32) + v%4 of the 32-key block, v = 0..15); one LDS
+// read of the K operand feeds all G groups. The feature dimension is split between
 // the half-waves: half h holds features [h*D/2, h*D/2 + D/2) of its row in both
-// operands (the contraction is order-free), so every lane loads D contiguous bytes.
+// operands (the contraction is order-free). In LDS, 16-byte part p of key row r
+// sits at position r*CH + (p ^ (r & 7)), so the 8 rows one LDS cycle serves hit 8
+// different bank groups.
 //
 // Filtering is two-level. Per 16-score lane block, a max tree decides whether any
 // score beats the query's threshold; only such "dirty" blocks are copied into a
 // per-wave LDS staging ring. When the ring fills, the whole wave drains it: each
 // lane takes one staged block, finds its passing scores and appends them as
 // 64-bit words  (raw fp32 score bits << 32) | (~key)  to the query's candidate
-// buffer in global memory (one buffer per query and half-wave, positions from LDS
-// atomic counters). The select converts the words to order-preserving keys.
+// buffer in global memory (one buffer per query and half-wave; one LDS counter
+// update per block reserves the positions). The select converts the words to
+// order-preserving keys.
 struct ScanArgs {
   const uint16_t* Q;
   const uint16_t* K;
@@ -388,98 +391,122 @@ struct ScanArgs {
   int mode, stride;
 };
 
-constexpr int STAGE_CAP = 112;  // staged 16-score blocks per wave
+constexpr int SCAN_KT = 64;  // keys per K tile
 
-template <int D, int R>
-__global__ __launch_bounds__(256, D == 64 ? 3 : 2) void k_fused_scan(ScanArgs a) {
-  constexpr int KT = 64;                  // keys per LDS tile
+// Launch shape of the scan: G = 32-query groups per wave, NB = K tiles resident
+// in the LDS ring, CAP = staged 16-score blocks per wave (a wave drains its ring
+// when the next block's dirty lanes would not fit, so a drain is one 64-lane
+// round), OCC = waves per SIMD the register and LDS sizes allow (36 KB of LDS per
+// workgroup: four workgroups per CU).
+template <int G>
+struct ScanShape;
+template <>
+struct ScanShape<2> {  // 256 queries per workgroup
+  static constexpr int NB = 2, CAP = 64, OCC = 4;
+};
+
+template <int G>
+constexpr int scan_queries_per_wg() { return 4 * 32 * G; }
+
+// s_waitcnt immediate that waits until at most n vector-memory operations are
+// outstanding and does not wait on the other counters
+#define TOPK_WAIT_VM(n) (((n) & 15) | (7 << 4) | (15 << 8) | (((n) >> 4) << 14))
+
+template <int D, int R, int G>
+__global__ __launch_bounds__(256, ScanShape<G>::OCC) void k_fused_scan(ScanArgs a) {
+  static_assert(ScanShape<G>::CAP >= 64, "a ring holds at least one block's 64 lanes");
+  constexpr int SCAN_NB = ScanShape<G>::NB;
+  constexpr int STAGE_CAP = ScanShape<G>::CAP;
+  constexpr int KT = SCAN_KT;
   constexpr int NRB = KT / 32;            // 32-key MFMA blocks per tile
-  constexpr int ROWB = 2 * D + 16;        // padded LDS row (bytes): conflict-free 16-byte reads
   constexpr int NS = D / 16;              // MFMA steps over the features
-  constexpr int CH = 2 * D / 16;          // 16-byte pieces per key row
-  constexpr int PT = KT * CH / 256;       // pieces per thread per tile
-  constexpr int QB = 256;                 // queries per workgroup
-  __shared__ __attribute__((aligned(16))) unsigned char ks[2][KT * ROWB];
-  // staging slot = 16 scores (64 bytes) stored as four 16-byte chunks; chunk c of
-  // slot s sits at chunk position c ^ ((s >> 2) & 3), so the 8 lanes one LDS cycle
-  // serves (consecutive slots) hit 8 different bank groups
+  constexpr int CH = 2 * D / 16;          // 16-byte parts per key row
+  constexpr int TILEB = KT * 2 * D;       // bytes per K tile
+  constexpr int LPW = TILEB / 1024 / 4;   // 1 KB direct loads per wave per tile
+  constexpr int QB = scan_queries_per_wg<G>();
+  static_assert(LPW >= 1 && TILEB % 4096 == 0, "tile must split evenly over the 4 waves");
+  __shared__ __attribute__((aligned(16))) unsigned char ks[SCAN_NB][TILEB];
+  // staging slot = the 16 scores (64 bytes) of one dirty lane block
   __shared__ __attribute__((aligned(16))) float stage[4][STAGE_CAP][16];
   __shared__ uint32_t stage_meta[4][STAGE_CAP];
-  __shared__ float tau_lds[4][64];
-  __shared__ uint32_t cnt_lds[4][128];
+  __shared__ float tau_lds[4][32 * G];
+  __shared__ uint32_t cnt_lds[4][64 * G];
 
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63, half = lane >> 5, n = lane & 31;
   // XCD-aware order: the hardware deals workgroups round-robin over the 8 XCDs;
   // renumber so each XCD runs consecutive logical workgroups (same head) and K
   // stays in that XCD's L2.
-  const int64_t G = gridDim.x, bid = blockIdx.x;
-  const int64_t wg = (G % 8 == 0) ? (bid % 8) * (G / 8) + bid / 8 : bid;
+  const int64_t NG = gridDim.x, bid = blockIdx.x;
+  const int64_t wg = (NG % 8 == 0) ? (bid % 8) * (NG / 8) + bid / 8 : bid;
   const int64_t cl = wg / a.wgs_per_chunk, blk = wg - cl * a.wgs_per_chunk;
   const int64_t id = a.c0 + cl, bh = id / a.nchunk, c = id - bh * a.nchunk;
   const uint16_t* Kh = a.K + bh * a.kv_head_stride;
   const int64_t ntiles = (a.Lk + KT - 1) / KT;
   const bool tail = ntiles * KT != a.Lk;
-  const int64_t wave_row0 = cl * a.C + blk * QB + wave * 64;  // pass-local row of the wave's query 0
+  const int64_t wave_row0 = cl * a.C + blk * QB + wave * 32 * G;  // pass-local row of the wave's query 0
 
-  bool ok[2];
-  bf16x8 b[2][NS];
+  bool ok[G];
+  bf16x8 b[G][NS];
   {
     const bf16x8 zero8 = {};
 #pragma unroll
-    for (int g = 0; g < 2; ++g) {
-      const int64_t local = blk * QB + wave * 64 + g * 32 + n, i = c * a.C + local;
+    for (int g = 0; g < G; ++g) {
+      const int64_t local = blk * QB + wave * 32 * G + g * 32 + n, i = c * a.C + local;
       ok[g] = local < a.C && i < a.Lq;
       const uint16_t* q = a.Q + (bh * a.Lq + (ok[g] ? i : 0)) * D + (D / 2) * half;
 #pragma unroll
       for (int s = 0; s < NS; ++s) b[g][s] = ok[g] ? *(const bf16x8*)(q + 8 * s) : zero8;
     }
   }
-  cnt_lds[wave][lane] = 0;
-  cnt_lds[wave][64 + lane] = 0;
+#pragma unroll
+  for (int g = 0; g < G; ++g) cnt_lds[wave][g * 64 + lane] = 0;
 
-  uint4 pre[PT];
-  auto issue = [&](int64_t t) {
-    const int64_t key0 = t * KT;
+  // direct loads of tile t into ring buffer buf: lane `lane` of this wave's j-th
+  // load fills LDS position cidx = (wave*LPW + j)*64 + lane with part
+  // (cidx % CH) ^ (row & 7) of key row cidx / CH (rows past Lk load the last key;
+  // their scores are masked)
+  auto issue = [&](int64_t t, int buf) {
 #pragma unroll
-    for (int e = 0; e < PT; ++e) {
-      const int cidx = tid + 256 * e, kr = cidx / CH, part = cidx - kr * CH;
-      pre[e] = key0 + kr < a.Lk ? *(const uint4*)(Kh + (key0 + kr) * D + part * 8) : make_uint4(0u, 0u, 0u, 0u);
+    for (int j = 0; j < LPW; ++j) {
+      const int cidx = (wave * LPW + j) * 64 + lane, r = cidx / CH, p = (cidx % CH) ^ (r & 7);
+      int64_t key = t * KT + r;
+      key = key < a.Lk ? key : a.Lk - 1;
+      __builtin_amdgcn_global_load_lds((const void*)(Kh + key * D + p * 8),
+                                       (__attribute__((address_space(3))) void*)&ks[buf][(wave * LPW + j) * 1024], 16,
+                                       0, 0);
     }
   };
-  auto stash = [&](int buf) {
-#pragma unroll
-    for (int e = 0; e < PT; ++e) {
-      const int cidx = tid + 256 * e, kr = cidx / CH, part = cidx - kr * CH;
-      *(uint4*)(&ks[buf][kr * ROWB + part * 16]) = pre[e];
-    }
-  };
-  // Runs body(tile, lds) over tiles 0, step, 2*step, ... (count of them),
-  // double-buffered: tile t+1's global loads are in flight while t is consumed.
+  // Runs body(tile, lds) over tiles 0, step, 2*step, ... (count of them) with
+  // SCAN_NB - 1 tiles in flight. Before tile t is read, this wave's loads of t are
+  // complete (with a ring of three only the loads of t + 1 may still be
+  // outstanding; loads complete in order) and the barrier publishes every wave's
+  // part; the barrier also proves that no wave still reads the buffer the next
+  // load overwrites.
   auto pipeline = [&](int64_t count, int64_t step, auto&& body) {
     if (count <= 0) return;
-    issue(0);
+    static_assert(SCAN_NB == 2 || SCAN_NB == 3, "ring of two or three tiles");
+    for (int i = 0; i < SCAN_NB - 1 && i < count; ++i) issue(i * step, i);
     for (int64_t t = 0; t < count; ++t) {
-      const int buf = (int)(t & 1);
-      stash(buf);
+      if (SCAN_NB == 3 && t + 1 < count) __builtin_amdgcn_s_waitcnt(TOPK_WAIT_VM(LPW));
+      else __builtin_amdgcn_s_waitcnt(TOPK_WAIT_VM(0));
       __syncthreads();
-      if (t + 1 < count) issue((t + 1) * step);
-      body(t * step, &ks[buf][0]);
+      if (t + SCAN_NB - 1 < count) issue((t + SCAN_NB - 1) * step, (int)((t + SCAN_NB - 1) % SCAN_NB));
+      body(t * step, &ks[t % SCAN_NB][0]);
     }
     __syncthreads();
   };
-  // scores of 32 keys (block rb of the tile) for both query groups
-  auto block_scores = [&](const unsigned char* kb, int rb, f32x16& acc0, f32x16& acc1) {
-    const unsigned char* base = kb + (rb * 32 + n) * ROWB + half * D;
+  // scores of 32 keys (block rb of the tile) for all G query groups
+  auto block_scores = [&](const unsigned char* kb, int rb, f32x16 (&acc)[G]) {
+    const int r = rb * 32 + n;
     bf16x8 av[NS];
 #pragma unroll
-    for (int s = 0; s < NS; ++s) av[s] = *(const bf16x8*)(base + 16 * s);
-    acc0 = (f32x16){};
-    acc1 = (f32x16){};
+    for (int s = 0; s < NS; ++s) av[s] = *(const bf16x8*)(kb + (r * CH + ((half * NS + s) ^ (r & 7))) * 16);
 #pragma unroll
-    for (int s = 0; s < NS; ++s) {
-      acc0 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(av[s], b[0][s], acc0, 0, 0, 0);
-      acc1 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(av[s], b[1][s], acc1, 0, 0, 0);
-    }
+    for (int g = 0; g < G; ++g) acc[g] = (f32x16){};
+#pragma unroll
+    for (int s = 0; s < NS; ++s)
+#pragma unroll
+      for (int g = 0; g < G; ++g) acc[g] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(av[s], b[g][s], acc[g], 0, 0, 0);
   };
   auto mask_keys = [&](f32x16& acc, int64_t jb) {  // keys >= Lk of the last tile -> -inf
 #pragma unroll
@@ -493,11 +520,13 @@ __global__ __launch_bounds__(256, D == 64 ? 3 : 2) void k_fused_scan(ScanArgs a)
     return m;
   };
 
-  float tau[2] = {-INFINITY, -INFINITY};
-  if (a.mode == MODE_SAMPLE) {
-    float top[2][R];
+  float tau[G];
 #pragma unroll
-    for (int g = 0; g < 2; ++g)
+  for (int g = 0; g < G; ++g) tau[g] = -INFINITY;
+  if (a.mode == MODE_SAMPLE) {
+    float top[G][R];
+#pragma unroll
+    for (int g = 0; g < G; ++g)
 #pragma unroll
       for (int r = 0; r < R; ++r) top[g][r] = -INFINITY;
     auto insert = [&](float (&tp)[R], float m) {
@@ -512,30 +541,31 @@ __global__ __launch_bounds__(256, D == 64 ? 3 : 2) void k_fused_scan(ScanArgs a)
     pipeline(ns, a.stride, [&](int64_t t, const unsigned char* kb) {
 #pragma unroll 1
       for (int rb = 0; rb < NRB; ++rb) {
-        f32x16 acc0, acc1;
-        block_scores(kb, rb, acc0, acc1);
+        f32x16 acc[G];
+        block_scores(kb, rb, acc);
         if (tail && t == ntiles - 1) {
           const int64_t jb = t * KT + rb * 32 + 4 * half;
-          mask_keys(acc0, jb);
-          mask_keys(acc1, jb);
+#pragma unroll
+          for (int g = 0; g < G; ++g) mask_keys(acc[g], jb);
         }
-        insert(top[0], block_max(acc0));
-        insert(top[1], block_max(acc1));
+#pragma unroll
+        for (int g = 0; g < G; ++g) insert(top[g], block_max(acc[g]));
       }
     });
 #pragma unroll
-    for (int g = 0; g < 2; ++g) {
+    for (int g = 0; g < G; ++g) {
       const float mine = top[g][R - 1];
       tau[g] = fminf(mine, __shfl_xor(mine, 32, 64));
     }
   }
 #pragma unroll
-  for (int g = 0; g < 2; ++g) {
+  for (int g = 0; g < G; ++g) {
     if (!ok[g]) tau[g] = INFINITY;
     if (half == 0) tau_lds[wave][g * 32 + n] = tau[g];
   }
 
   // ---- staging ring and its drain (all per wave; LDS ops of one wave execute in order)
+  // slot meta = (32-key block index << 8) | (group << 6) | lane
   int scount = 0;  // wave-uniform
   auto drain = [&]() {
     __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
@@ -544,28 +574,35 @@ __global__ __launch_bounds__(256, D == 64 ? 3 : 2) void k_fused_scan(ScanArgs a)
     for (int base = 0; base < scount; base += 64) {
       const int slot = base + lane;
       uint32_t mask = 0, meta = 0;
+      const float* sp = &stage[wave][slot < STAGE_CAP ? slot : 0][0];
       if (slot < scount) {
         meta = stage_meta[wave][slot];
-        const float t = tau_lds[wave][(meta >> 6 & 1) * 32 + (meta & 31)];
-        const float4* sp = (const float4*)&stage[wave][slot][0];
-        const int sw = (slot >> 2) & 3;
+        const float t = tau_lds[wave][(meta >> 6 & 3) * 32 + (meta & 31)];
+        // neighbouring slots start their four 16-byte reads at different chunks,
+        // so the 8 lanes one LDS cycle serves hit 8 different bank groups
+        const uint32_t r = (uint32_t)(slot >> 1) & 3u;
 #pragma unroll
-        for (int q4 = 0; q4 < 4; ++q4) {
-          const float4 x = sp[q4 ^ sw];
-          mask |= (x.x > t ? 1u : 0u) << (4 * q4) | (x.y > t ? 2u : 0u) << (4 * q4) |
-                  (x.z > t ? 4u : 0u) << (4 * q4) | (x.w > t ? 8u : 0u) << (4 * q4);
+        for (uint32_t q4 = 0; q4 < 4; ++q4) {
+          const uint32_t cc = (q4 + r) & 3u;
+          const float4 x = *(const float4*)(sp + 4 * cc);
+          const uint32_t m4 = (x.x > t ? 1u : 0u) | (x.y > t ? 2u : 0u) | (x.z > t ? 4u : 0u) | (x.w > t ? 8u : 0u);
+          mask |= m4 << (4 * cc);
         }
       }
-      const uint32_t ql = meta & 63, g = meta >> 6 & 1, h = ql >> 5;
-      const uint32_t nj = 0xFFFFFFFFu - ((meta >> 7) * 32u + 4u * h);
-      uint64_t* dst = a.cand + ((wave_row0 + g * 32 + (ql & 31)) * 2 + h) * a.caph;
-      while (mask) {
-        const uint32_t v = __builtin_ctz(mask);
-        mask &= mask - 1;
-        const float sc = stage[wave][slot][(((v >> 2) ^ (uint32_t)((slot >> 2) & 3)) << 2) | (v & 3u)];
-        const uint32_t pos = atomicAdd(&cnt_lds[wave][g * 64 + ql], 1u);
-        if (pos < (uint32_t)a.caph)
-          dst[pos] = ((uint64_t)__float_as_uint(sc) << 32) | (uint64_t)(nj - (8u * (v >> 2) + (v & 3u)));
+      if (mask) {
+        const uint32_t ql = meta & 63, g = meta >> 6 & 3, h = ql >> 5;
+        // one counter update per slot reserves room for all its passing scores
+        uint32_t pos = atomicAdd(&cnt_lds[wave][g * 64 + ql], (uint32_t)__builtin_popcount(mask));
+        const uint32_t nj = 0xFFFFFFFFu - ((meta >> 8) * 32u + 4u * h);
+        uint64_t* dst = a.cand + ((wave_row0 + g * 32 + (ql & 31)) * 2 + h) * a.caph;
+        do {
+          const uint32_t v = __builtin_ctz(mask);
+          mask &= mask - 1;
+          // score v of the block is key 8*(v/4) + v%4 = v + (v & ~3) past the block's first key
+          if (pos < (uint32_t)a.caph)
+            dst[pos] = ((uint64_t)__float_as_uint(sp[v]) << 32) | (uint64_t)(nj - (v + (v & 12u)));
+          ++pos;
+        } while (mask);
       }
     }
     scount = 0;
@@ -577,53 +614,58 @@ __global__ __launch_bounds__(256, D == 64 ? 3 : 2) void k_fused_scan(ScanArgs a)
     const bool dirty = block_max(acc) > tau[g];
     const uint64_t bal = __ballot(dirty);
     if (bal == 0) return;
+    const int nd = __popcll(bal);
+    if (scount + nd > STAGE_CAP) drain();
     if (dirty) {
       const int rank = __builtin_amdgcn_mbcnt_hi((uint32_t)(bal >> 32), __builtin_amdgcn_mbcnt_lo((uint32_t)bal, 0u));
       const int slot = scount + rank;
       float4* sp = (float4*)&stage[wave][slot][0];
-      const int sw = (slot >> 2) & 3;
-      sp[0 ^ sw] = make_float4(acc[0], acc[1], acc[2], acc[3]);
-      sp[1 ^ sw] = make_float4(acc[4], acc[5], acc[6], acc[7]);
-      sp[2 ^ sw] = make_float4(acc[8], acc[9], acc[10], acc[11]);
-      sp[3 ^ sw] = make_float4(acc[12], acc[13], acc[14], acc[15]);
-      stage_meta[wave][slot] = (uint32_t)((t * KT + rb * 32) / 32) << 7 | (uint32_t)(g << 6) | (uint32_t)lane;
+      sp[0] = make_float4(acc[0], acc[1], acc[2], acc[3]);
+      sp[1] = make_float4(acc[4], acc[5], acc[6], acc[7]);
+      sp[2] = make_float4(acc[8], acc[9], acc[10], acc[11]);
+      sp[3] = make_float4(acc[12], acc[13], acc[14], acc[15]);
+      stage_meta[wave][slot] = (uint32_t)((t * KT + rb * 32) / 32) << 8 | (uint32_t)(g << 6) | (uint32_t)lane;
     }
-    scount += __popcll(bal);
-    if (scount > STAGE_CAP - 64) drain();
+    scount += nd;
   };
-  pipeline(ntiles, 1, [&](int64_t t, const unsigned char* kb) {
-    if (tail && t == ntiles - 1) {
-#pragma unroll 1
-      for (int rb = 0; rb < NRB; ++rb) {
-        f32x16 acc0, acc1;
-        block_scores(kb, rb, acc0, acc1);
+  // Main scan: a stream of 32-key blocks. When a block opens a new tile, that
+  // tile's wait and barrier (and the loads of the tile SCAN_NB - 1 further on,
+  // into the buffer of the tile just finished) come first.
+  {
+    const int64_t nblocks = ntiles * NRB;
+    auto open_tile = [&](int64_t t) {
+      if (SCAN_NB == 3 && t + 1 < ntiles) __builtin_amdgcn_s_waitcnt(TOPK_WAIT_VM(LPW));
+      else __builtin_amdgcn_s_waitcnt(TOPK_WAIT_VM(0));
+      __syncthreads();
+      if (t + SCAN_NB - 1 < ntiles) issue(t + SCAN_NB - 1, (int)((t + SCAN_NB - 1) % SCAN_NB));
+    };
+    auto compute = [&](int64_t blkno, f32x16 (&acc)[G]) {
+      const int64_t t = blkno / NRB;
+      const int rb = (int)(blkno - t * NRB);
+      block_scores(&ks[t % SCAN_NB][0], rb, acc);
+      if (tail && t == ntiles - 1) {
         const int64_t jb = t * KT + rb * 32 + 4 * half;
-        mask_keys(acc0, jb);
-        mask_keys(acc1, jb);
-        filter(0, acc0, t, rb);
-        filter(1, acc1, t, rb);
-      }
-    } else {
-      // the next block's MFMAs are issued before this block is filtered, so the
-      // matrix core works while the filter runs
-      f32x16 c0, c1;
-      block_scores(kb, 0, c0, c1);
 #pragma unroll
-      for (int rb = 0; rb < NRB; ++rb) {
-        f32x16 n0, n1;
-        if (rb + 1 < NRB) block_scores(kb, rb + 1, n0, n1);
-        filter(0, c0, t, rb);
-        filter(1, c1, t, rb);
-        if (rb + 1 < NRB) {
-          c0 = n0;
-          c1 = n1;
-        }
+        for (int g = 0; g < G; ++g) mask_keys(acc[g], jb);
       }
+    };
+    for (int i = 0; i < SCAN_NB - 1 && i < ntiles; ++i) issue(i, i);
+    open_tile(0);
+    auto filter_all = [&](const f32x16 (&acc)[G], int64_t blkno) {
+      const int64_t t = blkno / NRB;
+#pragma unroll
+      for (int g = 0; g < G; ++g) filter(g, acc[g], t, (int)(blkno - t * NRB));
+    };
+    for (int64_t blkno = 0; blkno < nblocks; ++blkno) {
+      if (blkno > 0 && blkno % NRB == 0) open_tile(blkno / NRB);
+      f32x16 x[G];
+      compute(blkno, x);
+      filter_all(x, blkno);
     }
-  });
+  }
   drain();
 #pragma unroll
-  for (int g = 0; g < 2; ++g)
+  for (int g = 0; g < G; ++g)
     if (ok[g]) a.cnt[(wave_row0 + g * 32 + n) * 2 + half] = (int32_t)cnt_lds[wave][g * 64 + lane];
 }
 
@@ -1101,23 +1143,23 @@ hipError_t launch_fused_scan(const Problem& pb, const Pass& ps, const PassBufs& 
   a.kv_head_stride = pb.kv_head_stride;
   a.c0 = ps.c0;
   a.nchunk = ps.nchunk;
-  a.wgs_per_chunk = (pb.C + 255) / 256;
   a.cand = b.cand;
   a.cnt = b.cnt;
   a.caph = b.caph;
   a.mode = cfg.mode;
   a.stride = cfg.stride;
+  const int G = cfg.groups;
+  a.wgs_per_chunk = (pb.C + 128 * G - 1) / (128 * G);
   const unsigned grid = (unsigned)(ps.nc * a.wgs_per_chunk);
-#define TOPK_SCAN(D_, R_) k_fused_scan<D_, R_><<<grid, 256, 0, st>>>(a)
-  if (pb.d == 64) {
-    if (cfg.R == 3) TOPK_SCAN(64, 3);
-    else if (cfg.R == 6) TOPK_SCAN(64, 6);
-    else TOPK_SCAN(64, 12);
-  } else {
-    if (cfg.R == 3) TOPK_SCAN(128, 3);
-    else if (cfg.R == 6) TOPK_SCAN(128, 6);
-    else TOPK_SCAN(128, 12);
-  }
+#define TOPK_SCAN(D_, G_)                                                 \
+  do {                                                                    \
+    if (cfg.R == 3) k_fused_scan<D_, 3, G_><<<grid, 256, 0, st>>>(a);     \
+    else if (cfg.R == 6) k_fused_scan<D_, 6, G_><<<grid, 256, 0, st>>>(a); \
+    else k_fused_scan<D_, 12, G_><<<grid, 256, 0, st>>>(a);               \
+  } while (0)
+  if (G != 2) return hipErrorInvalidValue;
+  if (pb.d == 64) TOPK_SCAN(64, 2);
+  else TOPK_SCAN(128, 2);
 #undef TOPK_SCAN
   return hipGetLastError();
 }
