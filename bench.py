@@ -26,15 +26,20 @@ METRIC = "top-k attn queries/s + score TFLOP/s (% bf16 MFMA peak) at L=32k,k=64"
 PEAK_BF16_TFLOPS = 2516.6          # MI355X dense bf16 MFMA, published
 PEAK_HBM_GBS = 8000.0
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "fused_scan_c3_traffic.json")
-SCAN_SOURCES = [os.path.join(ROOT, "paper_2106_06899_amd", "csrc", f) for f in
-                ("topk_kernels.hip", "topk_internal.h")]
+CSRC = os.path.join(ROOT, "paper_2106_06899_amd", "csrc")
+SCAN_BEGIN = "// ------------------------------------------------------------------ fused path: scan"
+SCAN_END = "// ------------------------------------------------------------------ fused path: select"
 
 
 def scan_source_digest() -> str:
-    h = hashlib.sha256()
-    for p in SCAN_SOURCES:
-        with open(p, "rb") as f:
-            h.update(f.read())
+    """Digest of the scan kernel's own source (its section of topk_kernels.hip plus
+    the shared internal header): counter readings stay valid while it is unchanged."""
+    with open(os.path.join(CSRC, "topk_kernels.hip")) as f:
+        text = f.read()
+    a, b = text.index(SCAN_BEGIN), text.index(SCAN_END)
+    h = hashlib.sha256(text[a:b].encode())
+    with open(os.path.join(CSRC, "topk_internal.h"), "rb") as f:
+        h.update(f.read())
     return h.hexdigest()[:16]
 
 
@@ -49,6 +54,35 @@ def traffic_for_current_kernel():
     if t.get("kernel_source_sha") != scan_source_digest():
         return None
     return t.get("bytes_per_launch")
+
+
+def _pmc_average(path: str, kernel_substr: str) -> float:
+    """Average counter value per dispatch (KiB) of the kernels whose name holds kernel_substr."""
+    import csv
+    vals = [float(r["Counter_Value"]) for r in csv.DictReader(open(path)) if kernel_substr in r["Kernel_Name"]]
+    if not vals:
+        raise SystemExit(f"no dispatch of {kernel_substr} in {path}")
+    return sum(vals) / len(vals)
+
+
+def write_traffic(scan_fetch: str, scan_write: str, copy_fetch: str, copy_write: str, copy_bytes: int,
+                  command: str) -> dict:
+    """HBM bytes per scan launch from rocprofv3 FETCH_SIZE / WRITE_SIZE runs, each
+    scaled by what the same counter reads for a plain device copy of copy_bytes."""
+    f_copy = _pmc_average(copy_fetch, "copyBuffer")
+    w_copy = _pmc_average(copy_write, "copyBuffer")
+    kib = copy_bytes / 1024.0
+    ff, fw = kib / f_copy, kib / w_copy
+    fetch = _pmc_average(scan_fetch, "k_fused_scan") * ff * 1024.0
+    write = _pmc_average(scan_write, "k_fused_scan") * fw * 1024.0
+    rec = {"kernel_source_sha": scan_source_digest(), "bytes_per_launch": fetch + write,
+           "fetch_bytes_per_launch": fetch, "write_bytes_per_launch": write,
+           "fetch_factor": ff, "write_factor": fw, "copy_bytes": copy_bytes, "command": command}
+    os.makedirs(os.path.dirname(TRAFFIC_FILE), exist_ok=True)
+    with open(TRAFFIC_FILE, "w") as f:
+        json.dump(rec, f, indent=1)
+        f.write("\n")
+    return rec
 
 
 def cpu_baseline(w, x, budget_s: float):
@@ -85,7 +119,14 @@ def main():
     ap.add_argument("--no-cpu", action="store_true")
     ap.add_argument("--copy-probe", type=int, default=0, metavar="BYTES",
                     help="only run a plain device-to-device copy of BYTES bytes 5 times (counter calibration)")
+    ap.add_argument("--write-traffic", nargs=4, metavar=("SCAN_FETCH", "SCAN_WRITE", "COPY_FETCH", "COPY_WRITE"),
+                    help="write the scan's HBM bytes per launch from four rocprofv3 counter_collection.csv files")
+    ap.add_argument("--copy-bytes", type=int, default=1 << 30)
+    ap.add_argument("--traffic-command", default="")
     args = ap.parse_args()
+    if args.write_traffic:
+        print(json.dumps(write_traffic(*args.write_traffic, args.copy_bytes, args.traffic_command)))
+        return
     if args.copy_probe:
         import torch
         src = torch.ones(args.copy_probe // 4, dtype=torch.float32, device="cuda:0")
