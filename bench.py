@@ -43,15 +43,18 @@ def scan_source_digest() -> str:
     return h.hexdigest()[:16]
 
 
-def traffic_for_current_kernel():
+def traffic_for_current_kernel(workload: str, path: int):
     """HBM bytes per scan launch from committed rocprofv3 counter runs, or None when
-    they are missing or were taken on a different kernel source."""
+    they are missing, were taken on another workload or a different kernel source,
+    or the call does not run the fused scan."""
+    if path != 1:
+        return None
     try:
         with open(TRAFFIC_FILE) as f:
             t = json.load(f)
     except (OSError, ValueError):
         return None
-    if t.get("kernel_source_sha") != scan_source_digest():
+    if t.get("kernel_source_sha") != scan_source_digest() or t.get("workload") != workload:
         return None
     return t.get("bytes_per_launch")
 
@@ -75,7 +78,7 @@ def write_traffic(scan_fetch: str, scan_write: str, copy_fetch: str, copy_write:
     ff, fw = kib / f_copy, kib / w_copy
     fetch = _pmc_average(scan_fetch, "k_fused_scan") * ff * 1024.0
     write = _pmc_average(scan_write, "k_fused_scan") * fw * 1024.0
-    rec = {"kernel_source_sha": scan_source_digest(), "bytes_per_launch": fetch + write,
+    rec = {"kernel_source_sha": scan_source_digest(), "workload": "c3", "bytes_per_launch": fetch + write,
            "fetch_bytes_per_launch": fetch, "write_bytes_per_launch": write,
            "fetch_factor": ff, "write_factor": fw, "copy_bytes": copy_bytes, "command": command}
     os.makedirs(os.path.dirname(TRAFFIC_FILE), exist_ok=True)
@@ -189,7 +192,7 @@ def main():
     flops_per_launch = flops / max(launches_per_step, 1)
     achieved = flops_per_launch / scan_avg_s / 1e12
     score_tflops_call = flops / (ms_step / 1e3) / 1e12
-    traffic = traffic_for_current_kernel()
+    traffic = traffic_for_current_kernel(w.name, path)
 
     cpu = None
     if not args.no_cpu:

@@ -211,6 +211,7 @@ int run(Problem pb, hipStream_t st) {
     ps.nchunk = pl.nchunk;
     PassBufs b = carve(pb, pl, ws);
     if (pl.path == PATH_TILE) {
+      if (e == hipSuccess) e = launch_init(b, st);
       if (e == hipSuccess) {
         StageTimer t(st, ST_SCORE);
         e = launch_tile_scores(pb, ps, b, st);

@@ -345,18 +345,79 @@ __global__ __launch_bounds__(256, 2) void k_tile_scores_mfma(Problem pb, Pass ps
 }
 
 // ------------------------------------------------------------------ chunk-tile path: select
+// One workgroup per query row of the score tile. Every key at or above a
+// threshold key is gathered into LDS in one streaming pass over the row, and the
+// exact select runs on that candidate set in LDS:
+//  * rows of at most TS_CAP valid keys take all of them;
+//  * longer rows take the R-th largest key of a sample of TS_SAMPLE keys (32
+//    blocks of 32 contiguous scores spread over the row), with R a few standard
+//    deviations above the sample's expected share of the top k;
+//  * the set is proven to hold the row's top k when it has at least k_eff keys
+//    and did not overflow; otherwise the row is selected from global memory by the
+//    multi-pass radix select (exact for any input).
+constexpr int TS_CAP = 4096;
+constexpr int TS_SAMPLE = 1024;
+
 __global__ __launch_bounds__(256) void k_tile_select(Problem pb, Pass ps, const float* S, uint64_t* sel) {
   extern __shared__ uint64_t sbuf[];
+  __shared__ uint64_t cand[TS_CAP];
   __shared__ uint32_t hist[256];
   __shared__ uint32_t misc[8];
+  __shared__ uint32_t ccount;
   const int64_t p = blockIdx.x;
   const RowRef rr = row_of(pb, ps, p);
   if (!rr.ok) return;
+  const int tid = threadIdx.x, lane = tid & 63;
   const int64_t nv = valid_keys(pb, rr.i);
   const uint32_t k_eff = (uint32_t)(pb.k < nv ? pb.k : nv);
+  const int P = pow2_at_least(k_eff);
   const float* row = S + p * pb.Lk;
-  auto getkey = [&](int64_t e) { return make_key(row[e], (uint32_t)e); };
-  team_topk<256>(getkey, nv, k_eff, (uint32_t)pb.k, sbuf, pow2_at_least(k_eff), hist, misc, sel + p * pb.k);
+  uint64_t* out = sel + p * pb.k;
+
+  uint64_t thr = 0;  // candidates: keys >= thr (every key is > 0)
+  if (nv > TS_CAP) {
+    // sample: block b covers [start_b, start_b + 32), start_b = 32 * floor(b * nv / (32 * 32))
+    for (int s = tid; s < TS_SAMPLE; s += 256) {
+      const int64_t b = s >> 5, start = ((b * nv) / (32 * 32)) * 32, e = start + (s & 31);
+      cand[s] = e < nv ? make_key(row[e], (uint32_t)e) : 0ull;
+    }
+    __syncthreads();
+    team_sort_desc<256>(cand, TS_SAMPLE);
+    // expected sampled keys among the row's top k_eff: mu = k_eff * TS_SAMPLE / nv;
+    // R = mu + 6 sqrt(mu) + 8 keeps P(sample rank R below the k-th key) negligible
+    const float mu = (float)k_eff * (float)TS_SAMPLE / (float)nv;
+    int R = (int)ceilf(mu + 6.0f * sqrtf(mu) + 8.0f);
+    R = R < TS_SAMPLE ? R : TS_SAMPLE;
+    thr = cand[R - 1];
+    __syncthreads();
+  }
+  if (tid == 0) ccount = 0;
+  __syncthreads();
+  // one pass: wave-level compaction, one counter update per wave and step
+  for (int64_t base = 0; base < nv; base += 256) {
+    const int64_t e = base + tid;
+    const uint64_t key = e < nv ? make_key(row[e], (uint32_t)e) : 0ull;
+    const bool take = e < nv && key >= thr;
+    const uint64_t bal = __ballot(take);
+    if (bal) {
+      uint32_t wbase = 0;
+      if (lane == 0) wbase = atomicAdd(&ccount, (uint32_t)__popcll(bal));
+      wbase = __shfl(wbase, 0, 64);
+      const uint32_t pos = wbase + __builtin_amdgcn_mbcnt_hi((uint32_t)(bal >> 32),
+                                                             __builtin_amdgcn_mbcnt_lo((uint32_t)bal, 0u));
+      if (take && pos < (uint32_t)TS_CAP) cand[pos] = key;
+    }
+  }
+  __syncthreads();
+  const uint32_t c = ccount;
+  __syncthreads();
+  if (c >= k_eff && c <= (uint32_t)TS_CAP) {
+    auto getkey = [&](int64_t e) { return cand[e]; };
+    team_topk<256>(getkey, c, k_eff, (uint32_t)pb.k, sbuf, P, hist, misc, out);
+  } else {
+    auto getkey = [&](int64_t e) { return make_key(row[e], (uint32_t)e); };
+    team_topk<256>(getkey, nv, k_eff, (uint32_t)pb.k, sbuf, P, hist, misc, out);
+  }
 }
 
 // ------------------------------------------------------------------ fused path: scan
@@ -736,31 +797,17 @@ __device__ __forceinline__ void wave_sort_store(const uint64_t* sbuf, uint32_t k
     if (e * 64 + lane < k) out[e * 64 + lane] = r[e];
 }
 
-__device__ __forceinline__ void cand_select_row(const Problem& pb, const Pass& ps, const PassBufs& bufs, int64_t p,
-                                                uint64_t* sbuf, uint32_t* hist) {
-  const RowRef rr = row_of(pb, ps, p);
-  if (!rr.ok) return;
-  const int64_t nv = valid_keys(pb, rr.i);
-  const uint32_t k_eff = (uint32_t)(pb.k < nv ? pb.k : nv);
-  const int64_t c0 = bufs.cnt[2 * p], c1 = bufs.cnt[2 * p + 1];
-  if (c0 > bufs.caph || c1 > bufs.caph || c0 + c1 < (int64_t)k_eff || k_eff > 256 ||
-      c0 + c1 > 64 * CAND_REGS) {
-    if ((threadIdx.x & 63) == 0) bufs.redo_list[atomicAdd(bufs.redo_count, 1)] = (int32_t)p;
-    return;
-  }
+// Radix select on n <= CAND_REGS * 64 distinct keys held in registers (key[e] is
+// element e*64 + lane; elements >= n are ignored). Returns (shift, prefix): the
+// k_eff largest keys are exactly those with (key >> shift) >= (prefix >> shift).
+// The block is one wave (hist: 256 words of LDS).
+__device__ __forceinline__ void wave_radix_select(const uint64_t (&key)[CAND_REGS], int n, uint32_t k_eff,
+                                                  uint32_t* hist, int* shift_out, uint64_t* prefix_out) {
   const int lane = threadIdx.x & 63;
-  const int n = (int)(c0 + c1);
-  const uint64_t* b0 = bufs.cand + (2 * p) * bufs.caph;
-  const uint64_t* b1 = b0 + bufs.caph;
-  uint64_t key[CAND_REGS];
   uint64_t kmin = ~0ull, kmax = 0ull;
 #pragma unroll
   for (int e = 0; e < CAND_REGS; ++e) {
-    const int i = lane + 64 * e;
-    uint64_t wd = 0;
-    if (i < n) wd = i < c0 ? b0[i] : b1[i - c0];
-    key[e] = ((uint64_t)ord_u32(__uint_as_float((uint32_t)(wd >> 32))) << 32) | (wd & 0xFFFFFFFFull);
-    if (i < n) {
+    if (lane + 64 * e < n) {
       kmin = key[e] < kmin ? key[e] : kmin;
       kmax = key[e] > kmax ? key[e] : kmax;
     }
@@ -813,6 +860,18 @@ __device__ __forceinline__ void cand_select_row(const Problem& pb, const Pass& p
     kr -= above;
     if (cnt == kr) break;  // every key of this bucket is selected
   }
+  *shift_out = shift;
+  *prefix_out = prefix;
+}
+
+// The k_eff (<= 256) largest of n register keys, sorted descending, written as k
+// words to out (0 pads). sbuf: 256 keys of LDS.
+__device__ __forceinline__ void wave_select_store(const uint64_t (&key)[CAND_REGS], int n, uint32_t k_eff, int64_t k,
+                                                  uint64_t* sbuf, uint32_t* hist, uint64_t* out) {
+  const int lane = threadIdx.x & 63;
+  int shift;
+  uint64_t prefix;
+  wave_radix_select(key, n, k_eff, hist, &shift, &prefix);
   // selected: (key >> shift) >= (prefix >> shift); compact them into sbuf
   const uint64_t lim = prefix >> shift;
   int base = 0;
@@ -825,17 +884,162 @@ __device__ __forceinline__ void cand_select_row(const Problem& pb, const Pass& p
     base += __popcll(m);
   }
   __syncthreads();
-  uint64_t* out = bufs.sel + p * pb.k;
-  if (k_eff <= 64) wave_sort_store<1>(sbuf, k_eff, pb.k, out);
-  else if (k_eff <= 128) wave_sort_store<2>(sbuf, k_eff, pb.k, out);
-  else wave_sort_store<4>(sbuf, k_eff, pb.k, out);
-  for (int64_t t = lane + 64 * (k_eff <= 64 ? 1 : k_eff <= 128 ? 2 : 4); t < pb.k; t += 64) out[t] = 0ull;
+  if (k_eff <= 64) wave_sort_store<1>(sbuf, k_eff, k, out);
+  else if (k_eff <= 128) wave_sort_store<2>(sbuf, k_eff, k, out);
+  else wave_sort_store<4>(sbuf, k_eff, k, out);
+  for (int64_t t = lane + 64 * (k_eff <= 64 ? 1 : k_eff <= 128 ? 2 : 4); t < k; t += 64) out[t] = 0ull;
+}
+
+__device__ __forceinline__ void cand_select_row(const Problem& pb, const Pass& ps, const PassBufs& bufs, int64_t p,
+                                                uint64_t* sbuf, uint32_t* hist) {
+  const RowRef rr = row_of(pb, ps, p);
+  if (!rr.ok) return;
+  const int64_t nv = valid_keys(pb, rr.i);
+  const uint32_t k_eff = (uint32_t)(pb.k < nv ? pb.k : nv);
+  const int64_t c0 = bufs.cnt[2 * p], c1 = bufs.cnt[2 * p + 1];
+  if (c0 > bufs.caph || c1 > bufs.caph || c0 + c1 < (int64_t)k_eff || k_eff > 256 ||
+      c0 + c1 > 64 * CAND_REGS) {
+    if ((threadIdx.x & 63) == 0) bufs.redo_list[atomicAdd(bufs.redo_count, 1)] = (int32_t)p;
+    return;
+  }
+  const int lane = threadIdx.x & 63;
+  const int n = (int)(c0 + c1);
+  const uint64_t* b0 = bufs.cand + (2 * p) * bufs.caph;
+  const uint64_t* b1 = b0 + bufs.caph;
+  uint64_t key[CAND_REGS];
+#pragma unroll
+  for (int e = 0; e < CAND_REGS; ++e) {
+    const int i = lane + 64 * e;
+    uint64_t wd = 0;
+    if (i < n) wd = i < c0 ? b0[i] : b1[i - c0];
+    key[e] = ((uint64_t)ord_u32(__uint_as_float((uint32_t)(wd >> 32))) << 32) | (wd & 0xFFFFFFFFull);
+  }
+  wave_select_store(key, n, k_eff, pb.k, sbuf, hist, bufs.sel + p * pb.k);
 }
 
 __global__ __launch_bounds__(64) void k_cand_select(Problem pb, Pass ps, PassBufs bufs) {
   __shared__ uint64_t sbuf[256];
   __shared__ uint32_t hist[256];
   cand_select_row(pb, ps, bufs, blockIdx.x, sbuf, hist);
+}
+
+// ------------------------------------------------------------------ chunk-tile path: short-row select
+// One wave per query row of the score tile, for rows of at most TSW_MAX_N valid
+// keys and k <= 256. Rows of at most 64 * CAND_REGS keys are selected in
+// registers directly. Longer rows take as threshold the R-th largest of
+// 64 * CAND_REGS evenly spaced sampled keys (R a few standard deviations above the
+// sample's expected share of the top k), gather every key at or above it into LDS
+// in one pass, and select in registers; a row whose gathered set is short of k_eff
+// keys or overflows goes to the redo list (exact fallback from the tile row).
+constexpr int TSW_MAX_N = 8192;
+
+__global__ __launch_bounds__(64) void k_tile_select_wave(Problem pb, Pass ps, const float* S, uint64_t* sel,
+                                                         int32_t* redo_list, int32_t* redo_count) {
+  constexpr int CAPW = 64 * CAND_REGS;
+  __shared__ uint64_t sbuf[256];
+  __shared__ uint64_t cbuf[CAPW];
+  __shared__ uint32_t hist[256];
+  const int64_t p = blockIdx.x;
+  const RowRef rr = row_of(pb, ps, p);
+  if (!rr.ok) return;
+  const int lane = threadIdx.x & 63;
+  const int64_t nv = valid_keys(pb, rr.i);
+  const uint32_t k_eff = (uint32_t)(pb.k < nv ? pb.k : nv);
+  const float* row = S + p * pb.Lk;
+  uint64_t* out = sel + p * pb.k;
+  uint64_t key[CAND_REGS];
+  if (nv <= CAPW) {
+#pragma unroll
+    for (int e = 0; e < CAND_REGS; ++e) {
+      const int64_t i = lane + 64 * e;
+      key[e] = i < nv ? make_key(row[i], (uint32_t)i) : 0ull;
+    }
+    wave_select_store(key, (int)nv, k_eff, pb.k, sbuf, hist, out);
+    return;
+  }
+  // sampled keys at positions floor(s * nv / CAPW), s = 0 .. CAPW - 1 (distinct: nv > CAPW)
+#pragma unroll
+  for (int e = 0; e < CAND_REGS; ++e) {
+    const int64_t i = ((int64_t)(lane + 64 * e) * nv) / CAPW;
+    key[e] = make_key(row[i], (uint32_t)i);
+  }
+  const float mu = (float)k_eff * (float)CAPW / (float)nv;
+  int R = (int)ceilf(mu + 6.0f * sqrtf(mu) + 8.0f);
+  R = R < CAPW ? R : CAPW;
+  int shift;
+  uint64_t prefix;
+  wave_radix_select(key, CAPW, (uint32_t)R, hist, &shift, &prefix);
+  uint64_t thr = ~0ull;  // the R-th largest sampled key = smallest selected one
+#pragma unroll
+  for (int e = 0; e < CAND_REGS; ++e)
+    if ((key[e] >> shift) >= (prefix >> shift)) thr = key[e] < thr ? key[e] : thr;
+#pragma unroll
+  for (int off = 32; off > 0; off >>= 1) {
+    const uint64_t o = shfl_xor_u64(thr, off);
+    thr = o < thr ? o : thr;
+  }
+  // gather every key >= thr (wave-level compaction; c is wave-uniform)
+  uint32_t c = 0;
+  auto offer = [&](int64_t i, float v) {
+    const uint64_t kk = make_key(v, (uint32_t)i);
+    const bool take = i < nv && kk >= thr;
+    const uint64_t bal = __ballot(take);
+    const uint32_t pos = c + __builtin_amdgcn_mbcnt_hi((uint32_t)(bal >> 32), __builtin_amdgcn_mbcnt_lo((uint32_t)bal, 0u));
+    if (take && pos < (uint32_t)CAPW) cbuf[pos] = kk;
+    c += (uint32_t)__popcll(bal);
+  };
+  if ((pb.Lk & 3) == 0) {  // 16-byte rows: four scores per lane and load
+    for (int64_t base = 0; base < nv; base += 256) {
+      const int64_t i = base + 4 * lane;
+      float4 v = make_float4(0.f, 0.f, 0.f, 0.f);
+      if (i + 3 < nv) v = *(const float4*)(row + i);
+      else {
+        if (i < nv) v.x = row[i];
+        if (i + 1 < nv) v.y = row[i + 1];
+        if (i + 2 < nv) v.z = row[i + 2];
+      }
+      offer(i, v.x);
+      offer(i + 1, v.y);
+      offer(i + 2, v.z);
+      offer(i + 3, v.w);
+    }
+  } else {
+    for (int64_t base = 0; base < nv; base += 64) {
+      const int64_t i = base + lane;
+      offer(i, i < nv ? row[i] : 0.f);
+    }
+  }
+  if (c < k_eff || c > (uint32_t)CAPW) {
+    if (lane == 0) redo_list[atomicAdd(redo_count, 1)] = (int32_t)p;
+    return;
+  }
+  __syncthreads();
+#pragma unroll
+  for (int e = 0; e < CAND_REGS; ++e) {
+    const uint32_t i = (uint32_t)(lane + 64 * e);
+    key[e] = i < c ? cbuf[i] : 0ull;
+  }
+  wave_select_store(key, (int)c, k_eff, pb.k, sbuf, hist, out);
+}
+
+// Rows the short-row select could not settle: multi-pass radix select straight
+// from the tile row, one workgroup per row, REDO_BLOCKS workgroups in turn.
+__global__ __launch_bounds__(256) void k_tile_select_redo(Problem pb, Pass ps, const float* S, uint64_t* sel,
+                                                          const int32_t* redo_list, const int32_t* redo_count) {
+  extern __shared__ uint64_t sbuf[];
+  __shared__ uint32_t hist[256];
+  __shared__ uint32_t misc[8];
+  const int32_t nredo = *redo_count;
+  for (int32_t r = blockIdx.x; r < nredo; r += gridDim.x) {
+    const int64_t p = redo_list[r];
+    const RowRef rr = row_of(pb, ps, p);
+    const int64_t nv = valid_keys(pb, rr.i);
+    const uint32_t k_eff = (uint32_t)(pb.k < nv ? pb.k : nv);
+    const float* row = S + p * pb.Lk;
+    auto getkey = [&](int64_t e) { return make_key(row[e], (uint32_t)e); };
+    team_topk<256>(getkey, nv, k_eff, (uint32_t)pb.k, sbuf, pow2_at_least(k_eff), hist, misc, sel + p * pb.k);
+    __syncthreads();
+  }
 }
 
 // ------------------------------------------------------------------ fused path: fallback
@@ -1128,7 +1332,13 @@ hipError_t launch_tile_scores(const Problem& pb, const Pass& ps, const PassBufs&
 
 hipError_t launch_tile_select(const Problem& pb, const Pass& ps, const PassBufs& b, hipStream_t st) {
   const int P = pow2_at_least(pb.k);
-  k_tile_select<<<(unsigned)pass_rows(pb, ps), 256, (size_t)P * 8, st>>>(pb, ps, b.scores, b.sel);
+  if (pb.k <= 256 && pb.Lk <= TSW_MAX_N) {
+    k_tile_select_wave<<<(unsigned)pass_rows(pb, ps), 64, 0, st>>>(pb, ps, b.scores, b.sel, b.redo_list,
+                                                                    b.redo_count);
+    k_tile_select_redo<<<REDO_BLOCKS, 256, (size_t)P * 8, st>>>(pb, ps, b.scores, b.sel, b.redo_list, b.redo_count);
+  } else {
+    k_tile_select<<<(unsigned)pass_rows(pb, ps), 256, (size_t)P * 8, st>>>(pb, ps, b.scores, b.sel);
+  }
   return hipGetLastError();
 }
 
