@@ -258,10 +258,10 @@ __global__ __launch_bounds__(256) void k_tile_scores(Problem pb, Pass ps, float*
 // bf16 inputs with d % 32 == 0: a 128-query x 128-key tile per workgroup, the
 // feature dimension consumed 32 at a time from LDS (double-buffered, next slice
 // prefetched into registers). Each wave owns 64 queries x 64 keys = 2 x 2 blocks of
-// v_mfma_f32_32x32x16_bf16 with A = Q (rows = queries) and B = K^T (columns =
-// keys), so lane l holds key l % 32 of a block for 16 queries and a store
-// instruction writes two 128-byte runs of a score row. Tiles entirely above the
-// causal diagonal are skipped (never read by the select).
+// v_mfma_f32_32x32x16_bf16 with A = K (rows = keys) and B = Q^T (columns =
+// queries), so lane l holds keys 8*(v/4) + 4*(l/32) + v%4 of a block for query
+// l % 32: four consecutive keys of one score row per 16-byte store. Tiles entirely
+// above the causal diagonal are skipped (never read by the select).
 template <int DUMMY>
 __global__ __launch_bounds__(256, 2) void k_tile_scores_mfma(Problem pb, Pass ps, float* S) {
   constexpr int TQ = 128, TK = 128, KS = 32;     // tile rows, tile keys, features per slice
@@ -324,22 +324,84 @@ __global__ __launch_bounds__(256, 2) void k_tile_scores_mfma(Problem pb, Pass ps
 #pragma unroll
       for (int a = 0; a < 2; ++a)
 #pragma unroll
-        for (int b = 0; b < 2; ++b) acc[a][b] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(av[a], bv[b], acc[a][b], 0, 0, 0);
+        for (int b = 0; b < 2; ++b) acc[a][b] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(bv[b], av[a], acc[a][b], 0, 0, 0);
     }
   }
-  // D[m][n]: m = query row 8*(v/4) + 4*half + v%4 of the block, n = key lane%32
+  // D[m][n]: m = key 8*(v/4) + 4*half + v%4 of block b, n = query lane%32 of block a
+  const bool vec = (pb.Lk & 3) == 0;  // rows start 16-byte aligned
 #pragma unroll
   for (int a = 0; a < 2; ++a) {
+    const int64_t lr = r0 + wq + a * 32 + n, i = i0 + lr;
+    if (lr >= pb.C || i >= pb.Lq) continue;
+    const int64_t nv = valid_keys(pb, i);
+    float* srow = S + (cl * pb.C + lr) * pb.Lk;
 #pragma unroll
-    for (int v = 0; v < 16; ++v) {
-      const int64_t lr = r0 + wq + a * 32 + 8 * (v >> 2) + 4 * half + (v & 3), i = i0 + lr;
-      if (lr >= pb.C || i >= pb.Lq) continue;
-      const int64_t nv = valid_keys(pb, i);
+    for (int b = 0; b < 2; ++b) {
 #pragma unroll
-      for (int b = 0; b < 2; ++b) {
-        const int64_t key = key0 + wk + b * 32 + n;
-        if (key < nv) S[(cl * pb.C + lr) * pb.Lk + key] = acc[a][b][v];
+      for (int j = 0; j < 4; ++j) {
+        const int64_t key = key0 + wk + b * 32 + 8 * j + 4 * half;
+        const f32x16& x = acc[a][b];
+        if (vec && key + 3 < nv) {
+          *(float4*)(srow + key) = make_float4(x[4 * j], x[4 * j + 1], x[4 * j + 2], x[4 * j + 3]);
+        } else {
+#pragma unroll
+          for (int u = 0; u < 4; ++u)
+            if (key + u < nv) srow[key + u] = x[4 * j + u];
+        }
       }
+    }
+  }
+}
+
+// ------------------------------------------------------------------ row gather helper
+// Appends the key (score, index) of every element of row[0, nv) whose score is
+// >= ts to cbuf (LDS, capacity cap; positions past cap are counted but not
+// written), wave-compacted: reserve(n) returns the base position of this wave's
+// next n keys (wave-uniform). ts = -inf takes every element. Each lane loads
+// 4 x 16 bytes before testing them; rows must start 16-byte aligned when vec.
+// (The gathered set {score >= ts} holds the row's top k whenever it holds k keys:
+// a key outside it is below every key inside.)
+template <class Reserve>
+__device__ __forceinline__ void gather_row(const float* row, int64_t nv, float ts, bool vec, int64_t lane0,
+                                           int64_t lanes, uint64_t* cbuf, uint32_t cap, const Reserve& reserve) {
+  auto offer = [&](int64_t i, float v) {
+    const bool take = i < nv && v >= ts;
+    const uint64_t bal = __ballot(take);
+    if (bal == 0) return;
+    const uint32_t base = reserve((uint32_t)__popcll(bal));
+    const uint32_t pos = base + __builtin_amdgcn_mbcnt_hi((uint32_t)(bal >> 32), __builtin_amdgcn_mbcnt_lo((uint32_t)bal, 0u));
+    if (take && pos < cap) cbuf[pos] = make_key(v, (uint32_t)i);
+  };
+  if (vec) {
+    constexpr int U = 4;  // float4 loads in flight per lane
+    const int64_t step = 4 * lanes * U;
+    for (int64_t base = 0; base < nv; base += step) {
+      float4 v[U];
+#pragma unroll
+      for (int u = 0; u < U; ++u) {
+        const int64_t i = base + 4 * (lane0 + lanes * u);
+        v[u] = make_float4(0.f, 0.f, 0.f, 0.f);
+        if (i + 3 < nv) {
+          v[u] = *(const float4*)(row + i);
+        } else if (i < nv) {
+          v[u].x = row[i];
+          if (i + 1 < nv) v[u].y = row[i + 1];
+          if (i + 2 < nv) v[u].z = row[i + 2];
+        }
+      }
+#pragma unroll
+      for (int u = 0; u < U; ++u) {
+        const int64_t i = base + 4 * (lane0 + lanes * u);
+        offer(i, v[u].x);
+        offer(i + 1, v[u].y);
+        offer(i + 2, v[u].z);
+        offer(i + 3, v[u].w);
+      }
+    }
+  } else {
+    for (int64_t base = 0; base < nv; base += lanes) {
+      const int64_t i = base + lane0;
+      offer(i, i < nv ? row[i] : 0.f);
     }
   }
 }
@@ -374,7 +436,7 @@ __global__ __launch_bounds__(256) void k_tile_select(Problem pb, Pass ps, const 
   const float* row = S + p * pb.Lk;
   uint64_t* out = sel + p * pb.k;
 
-  uint64_t thr = 0;  // candidates: keys >= thr (every key is > 0)
+  float ts = -INFINITY;  // candidates: scores >= ts
   if (nv > TS_CAP) {
     // sample: block b covers [start_b, start_b + 32), start_b = 32 * floor(b * nv / (32 * 32))
     for (int s = tid; s < TS_SAMPLE; s += 256) {
@@ -388,26 +450,18 @@ __global__ __launch_bounds__(256) void k_tile_select(Problem pb, Pass ps, const 
     const float mu = (float)k_eff * (float)TS_SAMPLE / (float)nv;
     int R = (int)ceilf(mu + 6.0f * sqrtf(mu) + 8.0f);
     R = R < TS_SAMPLE ? R : TS_SAMPLE;
-    thr = cand[R - 1];
+    ts = key_score(cand[R - 1]);
     __syncthreads();
   }
   if (tid == 0) ccount = 0;
   __syncthreads();
   // one pass: wave-level compaction, one counter update per wave and step
-  for (int64_t base = 0; base < nv; base += 256) {
-    const int64_t e = base + tid;
-    const uint64_t key = e < nv ? make_key(row[e], (uint32_t)e) : 0ull;
-    const bool take = e < nv && key >= thr;
-    const uint64_t bal = __ballot(take);
-    if (bal) {
-      uint32_t wbase = 0;
-      if (lane == 0) wbase = atomicAdd(&ccount, (uint32_t)__popcll(bal));
-      wbase = __shfl(wbase, 0, 64);
-      const uint32_t pos = wbase + __builtin_amdgcn_mbcnt_hi((uint32_t)(bal >> 32),
-                                                             __builtin_amdgcn_mbcnt_lo((uint32_t)bal, 0u));
-      if (take && pos < (uint32_t)TS_CAP) cand[pos] = key;
-    }
-  }
+  auto reserve = [&](uint32_t cnt) {
+    uint32_t wbase = 0;
+    if (lane == 0) wbase = atomicAdd(&ccount, cnt);
+    return (uint32_t)__shfl(wbase, 0, 64);
+  };
+  gather_row(row, nv, ts, (pb.Lk & 3) == 0, tid, 256, cand, (uint32_t)TS_CAP, reserve);
   __syncthreads();
   const uint32_t c = ccount;
   __syncthreads();
@@ -797,16 +851,17 @@ __device__ __forceinline__ void wave_sort_store(const uint64_t* sbuf, uint32_t k
     if (e * 64 + lane < k) out[e * 64 + lane] = r[e];
 }
 
-// Radix select on n <= CAND_REGS * 64 distinct keys held in registers (key[e] is
-// element e*64 + lane; elements >= n are ignored). Returns (shift, prefix): the
-// k_eff largest keys are exactly those with (key >> shift) >= (prefix >> shift).
-// The block is one wave (hist: 256 words of LDS).
-__device__ __forceinline__ void wave_radix_select(const uint64_t (&key)[CAND_REGS], int n, uint32_t k_eff,
-                                                  uint32_t* hist, int* shift_out, uint64_t* prefix_out) {
+// Radix select on n <= E * 64 distinct keys held in registers (key[e] is element
+// e*64 + lane; elements >= n are ignored). Returns (shift, prefix): the k_eff
+// largest keys are exactly those with (key >> shift) >= (prefix >> shift). The
+// block is one wave (hist: 256 words of LDS).
+template <int E>
+__device__ __forceinline__ void wave_radix_select(const uint64_t (&key)[E], int n, uint32_t k_eff, uint32_t* hist,
+                                                  int* shift_out, uint64_t* prefix_out) {
   const int lane = threadIdx.x & 63;
   uint64_t kmin = ~0ull, kmax = 0ull;
 #pragma unroll
-  for (int e = 0; e < CAND_REGS; ++e) {
+  for (int e = 0; e < E; ++e) {
     if (lane + 64 * e < n) {
       kmin = key[e] < kmin ? key[e] : kmin;
       kmax = key[e] > kmax ? key[e] : kmax;
@@ -829,7 +884,7 @@ __device__ __forceinline__ void wave_radix_select(const uint64_t (&key)[CAND_REG
     __syncthreads();
     const uint64_t pre_hi = shift + 8 >= 64 ? 0 : prefix >> (shift + 8);
 #pragma unroll
-    for (int e = 0; e < CAND_REGS; ++e) {
+    for (int e = 0; e < E; ++e) {
       const bool match = lane + 64 * e < n && (shift + 8 >= 64 || (key[e] >> (shift + 8)) == pre_hi);
       if (match) atomicAdd(&hist[(uint32_t)(key[e] >> shift) & 255u], 1u);
     }
@@ -864,19 +919,20 @@ __device__ __forceinline__ void wave_radix_select(const uint64_t (&key)[CAND_REG
   *prefix_out = prefix;
 }
 
-// The k_eff (<= 256) largest of n register keys, sorted descending, written as k
-// words to out (0 pads). sbuf: 256 keys of LDS.
-__device__ __forceinline__ void wave_select_store(const uint64_t (&key)[CAND_REGS], int n, uint32_t k_eff, int64_t k,
+// The k_eff (<= 256) largest of n <= E * 64 register keys, sorted descending,
+// written as k words to out (0 pads). sbuf: 256 keys of LDS.
+template <int E>
+__device__ __forceinline__ void wave_select_store(const uint64_t (&key)[E], int n, uint32_t k_eff, int64_t k,
                                                   uint64_t* sbuf, uint32_t* hist, uint64_t* out) {
   const int lane = threadIdx.x & 63;
   int shift;
   uint64_t prefix;
-  wave_radix_select(key, n, k_eff, hist, &shift, &prefix);
+  wave_radix_select<E>(key, n, k_eff, hist, &shift, &prefix);
   // selected: (key >> shift) >= (prefix >> shift); compact them into sbuf
   const uint64_t lim = prefix >> shift;
   int base = 0;
 #pragma unroll
-  for (int e = 0; e < CAND_REGS; ++e) {
+  for (int e = 0; e < E; ++e) {
     const bool take = lane + 64 * e < n && (key[e] >> shift) >= lim;
     const uint64_t m = __ballot(take);
     const int pos = base + (int)__builtin_amdgcn_mbcnt_hi((uint32_t)(m >> 32), __builtin_amdgcn_mbcnt_lo((uint32_t)m, 0u));
@@ -914,7 +970,7 @@ __device__ __forceinline__ void cand_select_row(const Problem& pb, const Pass& p
     if (i < n) wd = i < c0 ? b0[i] : b1[i - c0];
     key[e] = ((uint64_t)ord_u32(__uint_as_float((uint32_t)(wd >> 32))) << 32) | (wd & 0xFFFFFFFFull);
   }
-  wave_select_store(key, n, k_eff, pb.k, sbuf, hist, bufs.sel + p * pb.k);
+  wave_select_store<CAND_REGS>(key, n, k_eff, pb.k, sbuf, hist, bufs.sel + p * pb.k);
 }
 
 __global__ __launch_bounds__(64) void k_cand_select(Problem pb, Pass ps, PassBufs bufs) {
@@ -925,19 +981,36 @@ __global__ __launch_bounds__(64) void k_cand_select(Problem pb, Pass ps, PassBuf
 
 // ------------------------------------------------------------------ chunk-tile path: short-row select
 // One wave per query row of the score tile, for rows of at most TSW_MAX_N valid
-// keys and k <= 256. Rows of at most 64 * CAND_REGS keys are selected in
-// registers directly. Longer rows take as threshold the R-th largest of
-// 64 * CAND_REGS evenly spaced sampled keys (R a few standard deviations above the
-// sample's expected share of the top k), gather every key at or above it into LDS
-// in one pass, and select in registers; a row whose gathered set is short of k_eff
-// keys or overflows goes to the redo list (exact fallback from the tile row).
+// keys and k <= 256. The row's candidates are gathered into LDS in one pass and
+// selected in registers (radix select sized to the candidate count):
+//  * rows of at most 64 * CAND_REGS keys take every key;
+//  * longer rows take every score >= ts, ts being the R-th largest of
+//    64 * CAND_REGS evenly spaced sampled scores, R a few standard deviations
+//    above the sample's expected share of the top k. For R <= 96 (long rows) ts
+//    is the R-th largest of the per-lane top two of the sample, which leaves at
+//    least R sampled scores >= ts at a fraction of the cost;
+//  * a row whose gathered set is short of k_eff keys or overflows goes to the
+//    redo list (exact fallback from the tile row).
 constexpr int TSW_MAX_N = 8192;
+
+template <int E>
+__device__ __forceinline__ void lds_select_store(const uint64_t* cbuf, int c, uint32_t k_eff, int64_t k,
+                                                 uint64_t* sbuf, uint32_t* hist, uint64_t* out) {
+  const int lane = threadIdx.x & 63;
+  uint64_t key[E];
+#pragma unroll
+  for (int e = 0; e < E; ++e) {
+    const int i = lane + 64 * e;
+    key[e] = i < c ? cbuf[i] : 0ull;
+  }
+  __syncthreads();  // cbuf may alias sbuf
+  wave_select_store<E>(key, c, k_eff, k, sbuf, hist, out);
+}
 
 __global__ __launch_bounds__(64) void k_tile_select_wave(Problem pb, Pass ps, const float* S, uint64_t* sel,
                                                          int32_t* redo_list, int32_t* redo_count) {
   constexpr int CAPW = 64 * CAND_REGS;
-  __shared__ uint64_t sbuf[256];
-  __shared__ uint64_t cbuf[CAPW];
+  __shared__ uint64_t cbuf[CAPW];  // gathered keys; the final sort reuses its start
   __shared__ uint32_t hist[256];
   const int64_t p = blockIdx.x;
   const RowRef rr = row_of(pb, ps, p);
@@ -947,79 +1020,63 @@ __global__ __launch_bounds__(64) void k_tile_select_wave(Problem pb, Pass ps, co
   const uint32_t k_eff = (uint32_t)(pb.k < nv ? pb.k : nv);
   const float* row = S + p * pb.Lk;
   uint64_t* out = sel + p * pb.k;
-  uint64_t key[CAND_REGS];
-  if (nv <= CAPW) {
+  float ts = -INFINITY;
+  if (nv > CAPW) {
+    // sample s = lane + 64 e sits at position floor(s * nv / CAPW) (distinct: nv > CAPW)
+    float smp[CAND_REGS];
 #pragma unroll
-    for (int e = 0; e < CAND_REGS; ++e) {
-      const int64_t i = lane + 64 * e;
-      key[e] = i < nv ? make_key(row[i], (uint32_t)i) : 0ull;
-    }
-    wave_select_store(key, (int)nv, k_eff, pb.k, sbuf, hist, out);
-    return;
-  }
-  // sampled keys at positions floor(s * nv / CAPW), s = 0 .. CAPW - 1 (distinct: nv > CAPW)
+    for (int e = 0; e < CAND_REGS; ++e) smp[e] = row[((int64_t)(lane + 64 * e) * nv) / CAPW];
+    const float mu = (float)k_eff * (float)CAPW / (float)nv;
+    int R = (int)ceilf(mu + 6.0f * sqrtf(mu) + 8.0f);
+    R = R < CAPW ? R : CAPW;
+    int shift;
+    uint64_t prefix;
+    if (R <= 96) {
+      float t1 = -INFINITY, t2 = -INFINITY;  // this lane's two largest samples
 #pragma unroll
-  for (int e = 0; e < CAND_REGS; ++e) {
-    const int64_t i = ((int64_t)(lane + 64 * e) * nv) / CAPW;
-    key[e] = make_key(row[i], (uint32_t)i);
-  }
-  const float mu = (float)k_eff * (float)CAPW / (float)nv;
-  int R = (int)ceilf(mu + 6.0f * sqrtf(mu) + 8.0f);
-  R = R < CAPW ? R : CAPW;
-  int shift;
-  uint64_t prefix;
-  wave_radix_select(key, CAPW, (uint32_t)R, hist, &shift, &prefix);
-  uint64_t thr = ~0ull;  // the R-th largest sampled key = smallest selected one
-#pragma unroll
-  for (int e = 0; e < CAND_REGS; ++e)
-    if ((key[e] >> shift) >= (prefix >> shift)) thr = key[e] < thr ? key[e] : thr;
-#pragma unroll
-  for (int off = 32; off > 0; off >>= 1) {
-    const uint64_t o = shfl_xor_u64(thr, off);
-    thr = o < thr ? o : thr;
-  }
-  // gather every key >= thr (wave-level compaction; c is wave-uniform)
-  uint32_t c = 0;
-  auto offer = [&](int64_t i, float v) {
-    const uint64_t kk = make_key(v, (uint32_t)i);
-    const bool take = i < nv && kk >= thr;
-    const uint64_t bal = __ballot(take);
-    const uint32_t pos = c + __builtin_amdgcn_mbcnt_hi((uint32_t)(bal >> 32), __builtin_amdgcn_mbcnt_lo((uint32_t)bal, 0u));
-    if (take && pos < (uint32_t)CAPW) cbuf[pos] = kk;
-    c += (uint32_t)__popcll(bal);
-  };
-  if ((pb.Lk & 3) == 0) {  // 16-byte rows: four scores per lane and load
-    for (int64_t base = 0; base < nv; base += 256) {
-      const int64_t i = base + 4 * lane;
-      float4 v = make_float4(0.f, 0.f, 0.f, 0.f);
-      if (i + 3 < nv) v = *(const float4*)(row + i);
-      else {
-        if (i < nv) v.x = row[i];
-        if (i + 1 < nv) v.y = row[i + 1];
-        if (i + 2 < nv) v.z = row[i + 2];
+      for (int e = 0; e < CAND_REGS; ++e) {
+        const float hi = fmaxf(t1, smp[e]), lo = fminf(t1, smp[e]);
+        t1 = hi;
+        t2 = fmaxf(t2, lo);
       }
-      offer(i, v.x);
-      offer(i + 1, v.y);
-      offer(i + 2, v.z);
-      offer(i + 3, v.w);
-    }
-  } else {
-    for (int64_t base = 0; base < nv; base += 64) {
-      const int64_t i = base + lane;
-      offer(i, i < nv ? row[i] : 0.f);
+      uint64_t k2[2] = {make_key(t1, 2u * lane), make_key(t2, 2u * lane + 1u)};
+      wave_radix_select<2>(k2, 128, (uint32_t)R, hist, &shift, &prefix);
+      uint32_t m = 0xFFFFFFFFu;
+#pragma unroll
+      for (int e = 0; e < 2; ++e)
+        if ((k2[e] >> shift) >= (prefix >> shift)) m = min(m, (uint32_t)(k2[e] >> 32));
+      for (int off = 32; off > 0; off >>= 1) m = min(m, (uint32_t)__shfl_xor(m, off, 64));
+      ts = ord_to_f32(m);
+    } else {
+      uint64_t key[CAND_REGS];
+#pragma unroll
+      for (int e = 0; e < CAND_REGS; ++e) key[e] = make_key(smp[e], (uint32_t)(lane + 64 * e));
+      wave_radix_select<CAND_REGS>(key, CAPW, (uint32_t)R, hist, &shift, &prefix);
+      uint32_t m = 0xFFFFFFFFu;
+#pragma unroll
+      for (int e = 0; e < CAND_REGS; ++e)
+        if ((key[e] >> shift) >= (prefix >> shift)) m = min(m, (uint32_t)(key[e] >> 32));
+      for (int off = 32; off > 0; off >>= 1) m = min(m, (uint32_t)__shfl_xor(m, off, 64));
+      ts = ord_to_f32(m);
     }
   }
+  // gather (wave-level compaction; c is wave-uniform)
+  uint32_t c = 0;
+  auto reserve = [&](uint32_t cnt) {
+    const uint32_t b = c;
+    c += cnt;
+    return b;
+  };
+  gather_row(row, nv, ts, (pb.Lk & 3) == 0, lane, 64, cbuf, (uint32_t)CAPW, reserve);
   if (c < k_eff || c > (uint32_t)CAPW) {
     if (lane == 0) redo_list[atomicAdd(redo_count, 1)] = (int32_t)p;
     return;
   }
   __syncthreads();
-#pragma unroll
-  for (int e = 0; e < CAND_REGS; ++e) {
-    const uint32_t i = (uint32_t)(lane + 64 * e);
-    key[e] = i < c ? cbuf[i] : 0ull;
-  }
-  wave_select_store(key, (int)c, k_eff, pb.k, sbuf, hist, out);
+  if (c <= 128) lds_select_store<2>(cbuf, (int)c, k_eff, pb.k, cbuf, hist, out);
+  else if (c <= 256) lds_select_store<4>(cbuf, (int)c, k_eff, pb.k, cbuf, hist, out);
+  else if (c <= 512) lds_select_store<8>(cbuf, (int)c, k_eff, pb.k, cbuf, hist, out);
+  else lds_select_store<CAND_REGS>(cbuf, (int)c, k_eff, pb.k, cbuf, hist, out);
 }
 
 // Rows the short-row select could not settle: multi-pass radix select straight
