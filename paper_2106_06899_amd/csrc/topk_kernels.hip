@@ -420,22 +420,12 @@ __device__ __forceinline__ void gather_row(const float* row, int64_t nv, float t
 constexpr int TS_CAP = 4096;
 constexpr int TS_SAMPLE = 1024;
 
-__global__ __launch_bounds__(256) void k_tile_select(Problem pb, Pass ps, const float* S, uint64_t* sel) {
-  extern __shared__ uint64_t sbuf[];
-  __shared__ uint64_t cand[TS_CAP];
-  __shared__ uint32_t hist[256];
-  __shared__ uint32_t misc[8];
-  __shared__ uint32_t ccount;
-  const int64_t p = blockIdx.x;
-  const RowRef rr = row_of(pb, ps, p);
-  if (!rr.ok) return;
+// The select of one row of nv fp32 scores by a 256-thread workgroup (see above).
+// cand: TS_CAP keys of LDS; sbuf: pow2_at_least(k_eff) keys of LDS.
+__device__ void wg_row_select(const float* row, int64_t nv, uint32_t k_eff, int64_t k, bool vec, uint64_t* cand,
+                              uint64_t* sbuf, uint32_t* hist, uint32_t* misc, uint32_t* ccount, uint64_t* out) {
   const int tid = threadIdx.x, lane = tid & 63;
-  const int64_t nv = valid_keys(pb, rr.i);
-  const uint32_t k_eff = (uint32_t)(pb.k < nv ? pb.k : nv);
   const int P = pow2_at_least(k_eff);
-  const float* row = S + p * pb.Lk;
-  uint64_t* out = sel + p * pb.k;
-
   float ts = -INFINITY;  // candidates: scores >= ts
   if (nv > TS_CAP) {
     // sample: block b covers [start_b, start_b + 32), start_b = 32 * floor(b * nv / (32 * 32))
@@ -453,25 +443,39 @@ __global__ __launch_bounds__(256) void k_tile_select(Problem pb, Pass ps, const 
     ts = key_score(cand[R - 1]);
     __syncthreads();
   }
-  if (tid == 0) ccount = 0;
+  if (tid == 0) *ccount = 0;
   __syncthreads();
   // one pass: wave-level compaction, one counter update per wave and step
   auto reserve = [&](uint32_t cnt) {
     uint32_t wbase = 0;
-    if (lane == 0) wbase = atomicAdd(&ccount, cnt);
+    if (lane == 0) wbase = atomicAdd(ccount, cnt);
     return (uint32_t)__shfl(wbase, 0, 64);
   };
-  gather_row(row, nv, ts, (pb.Lk & 3) == 0, tid, 256, cand, (uint32_t)TS_CAP, reserve);
+  gather_row(row, nv, ts, vec, tid, 256, cand, (uint32_t)TS_CAP, reserve);
   __syncthreads();
-  const uint32_t c = ccount;
+  const uint32_t c = *ccount;
   __syncthreads();
   if (c >= k_eff && c <= (uint32_t)TS_CAP) {
     auto getkey = [&](int64_t e) { return cand[e]; };
-    team_topk<256>(getkey, c, k_eff, (uint32_t)pb.k, sbuf, P, hist, misc, out);
+    team_topk<256>(getkey, c, k_eff, (uint32_t)k, sbuf, P, hist, misc, out);
   } else {
     auto getkey = [&](int64_t e) { return make_key(row[e], (uint32_t)e); };
-    team_topk<256>(getkey, nv, k_eff, (uint32_t)pb.k, sbuf, P, hist, misc, out);
+    team_topk<256>(getkey, nv, k_eff, (uint32_t)k, sbuf, P, hist, misc, out);
   }
+}
+
+__global__ __launch_bounds__(256) void k_tile_select(Problem pb, Pass ps, const float* S, uint64_t* sel) {
+  extern __shared__ uint64_t sbuf[];
+  __shared__ uint64_t cand[TS_CAP];
+  __shared__ uint32_t hist[256];
+  __shared__ uint32_t misc[8];
+  __shared__ uint32_t ccount;
+  const int64_t p = blockIdx.x;
+  const RowRef rr = row_of(pb, ps, p);
+  if (!rr.ok) return;
+  const int64_t nv = valid_keys(pb, rr.i);
+  const uint32_t k_eff = (uint32_t)(pb.k < nv ? pb.k : nv);
+  wg_row_select(S + p * pb.Lk, nv, k_eff, pb.k, (pb.Lk & 3) == 0, cand, sbuf, hist, misc, &ccount, sel + p * pb.k);
 }
 
 // ------------------------------------------------------------------ fused path: scan
@@ -946,6 +950,23 @@ __device__ __forceinline__ void wave_select_store(const uint64_t (&key)[E], int 
   for (int64_t t = lane + 64 * (k_eff <= 64 ? 1 : k_eff <= 128 ? 2 : 4); t < k; t += 64) out[t] = 0ull;
 }
 
+// Reads a row's n candidate words (c0 from b0, the rest from b1) into E registers
+// per lane as order-preserving keys, then selects and stores.
+template <int E>
+__device__ __forceinline__ void cand_select_regs(const uint64_t* b0, const uint64_t* b1, int c0, int n, uint32_t k_eff,
+                                                 int64_t k, uint64_t* sbuf, uint32_t* hist, uint64_t* out) {
+  const int lane = threadIdx.x & 63;
+  uint64_t key[E];
+#pragma unroll
+  for (int e = 0; e < E; ++e) {
+    const int i = lane + 64 * e;
+    uint64_t wd = 0;
+    if (i < n) wd = i < c0 ? b0[i] : b1[i - c0];
+    key[e] = ((uint64_t)ord_u32(__uint_as_float((uint32_t)(wd >> 32))) << 32) | (wd & 0xFFFFFFFFull);
+  }
+  wave_select_store<E>(key, n, k_eff, k, sbuf, hist, out);
+}
+
 __device__ __forceinline__ void cand_select_row(const Problem& pb, const Pass& ps, const PassBufs& bufs, int64_t p,
                                                 uint64_t* sbuf, uint32_t* hist) {
   const RowRef rr = row_of(pb, ps, p);
@@ -958,19 +979,13 @@ __device__ __forceinline__ void cand_select_row(const Problem& pb, const Pass& p
     if ((threadIdx.x & 63) == 0) bufs.redo_list[atomicAdd(bufs.redo_count, 1)] = (int32_t)p;
     return;
   }
-  const int lane = threadIdx.x & 63;
   const int n = (int)(c0 + c1);
   const uint64_t* b0 = bufs.cand + (2 * p) * bufs.caph;
-  const uint64_t* b1 = b0 + bufs.caph;
-  uint64_t key[CAND_REGS];
-#pragma unroll
-  for (int e = 0; e < CAND_REGS; ++e) {
-    const int i = lane + 64 * e;
-    uint64_t wd = 0;
-    if (i < n) wd = i < c0 ? b0[i] : b1[i - c0];
-    key[e] = ((uint64_t)ord_u32(__uint_as_float((uint32_t)(wd >> 32))) << 32) | (wd & 0xFFFFFFFFull);
-  }
-  wave_select_store<CAND_REGS>(key, n, k_eff, pb.k, sbuf, hist, bufs.sel + p * pb.k);
+  uint64_t* out = bufs.sel + p * pb.k;
+  if (n <= 128) cand_select_regs<2>(b0, b0 + bufs.caph, (int)c0, n, k_eff, pb.k, sbuf, hist, out);
+  else if (n <= 256) cand_select_regs<4>(b0, b0 + bufs.caph, (int)c0, n, k_eff, pb.k, sbuf, hist, out);
+  else if (n <= 512) cand_select_regs<8>(b0, b0 + bufs.caph, (int)c0, n, k_eff, pb.k, sbuf, hist, out);
+  else cand_select_regs<CAND_REGS>(b0, b0 + bufs.caph, (int)c0, n, k_eff, pb.k, sbuf, hist, out);
 }
 
 __global__ __launch_bounds__(64) void k_cand_select(Problem pb, Pass ps, PassBufs bufs) {
@@ -1168,9 +1183,10 @@ __global__ __launch_bounds__(256) void k_redo_select(Problem pb, Pass ps, PassBu
   const RowRef rr = row_of(pb, ps, p);
   const int64_t nv = valid_keys(pb, rr.i);
   const uint32_t k_eff = (uint32_t)(pb.k < nv ? pb.k : nv);
-  const float* row = bufs.scores + r * pb.Lk;
-  auto getkey = [&](int64_t e) { return make_key(row[e], (uint32_t)e); };
-  team_topk<256>(getkey, nv, k_eff, (uint32_t)pb.k, sbuf, pow2_at_least(k_eff), hist, misc, bufs.sel + p * pb.k);
+  __shared__ uint64_t cand[TS_CAP];
+  __shared__ uint32_t ccount;
+  wg_row_select(bufs.scores + r * pb.Lk, nv, k_eff, pb.k, (pb.Lk & 3) == 0, cand, sbuf, hist, misc, &ccount,
+                bufs.sel + p * pb.k);
 }
 
 template <typename T>
