@@ -24,6 +24,10 @@ namespace topk {
 typedef __bf16 bf16x8 __attribute__((__vector_size__(16)));
 typedef float f32x16 __attribute__((__vector_size__(64)));
 
+// s_waitcnt immediate that waits until at most n vector-memory operations are
+// outstanding and does not wait on the other counters
+#define TOPK_WAIT_VM(n) (((n) & 15) | (7 << 4) | (15 << 8) | (((n) >> 4) << 14))
+
 // ------------------------------------------------------------------ scalar helpers
 __device__ __forceinline__ uint32_t ord_u32(float s) {
   uint32_t b = __float_as_uint(s);
@@ -255,21 +259,35 @@ __global__ __launch_bounds__(256) void k_tile_scores(Problem pb, Pass ps, float*
 }
 
 // ------------------------------------------------------------------ chunk-tile path: MFMA scores
-// bf16 inputs with d % 32 == 0: a 128-query x 128-key tile per workgroup, the
-// feature dimension consumed 32 at a time from LDS (double-buffered, next slice
-// prefetched into registers). Each wave owns 64 queries x 64 keys = 2 x 2 blocks of
-// v_mfma_f32_32x32x16_bf16 with A = K (rows = keys) and B = Q^T (columns =
-// queries), so lane l holds keys 8*(v/4) + 4*(l/32) + v%4 of a block for query
-// l % 32: four consecutive keys of one score row per 16-byte store. Tiles entirely
-// above the causal diagonal are skipped (never read by the select).
+// bf16 inputs with d % 32 == 0: a 128-query x 256-key tile per workgroup, the
+// feature dimension consumed 32 at a time. Each slice of Q (128 rows x 64 bytes)
+// and K (256 rows x 64 bytes) is loaded straight from global memory into one of
+// two LDS buffers (global_load_lds, no register staging); 16-byte part p of row r
+// sits at position 4r + (p ^ ((r >> 1) & 3)), so the fragment reads of 8
+// consecutive rows hit 8 different bank groups. Each wave owns 64 queries x 128
+// keys = 2 x 4 blocks of v_mfma_f32_32x32x16_bf16 with A = K (rows = keys) and
+// B = Q^T (columns = queries): per 16 features it reads 6 fragments for 8 MFMAs,
+// and lane l holds keys 8*(v/4) + 4*(l/32) + v%4 of a block for query l % 32,
+// four consecutive keys of one score row per 16-byte store. Tiles entirely above
+// the causal diagonal are skipped (never read by the select).
+constexpr int TSM_TQ = 128, TSM_TK = 256;
+
 template <int DUMMY>
 __global__ __launch_bounds__(256, 2) void k_tile_scores_mfma(Problem pb, Pass ps, float* S) {
-  constexpr int TQ = 128, TK = 128, KS = 32;     // tile rows, tile keys, features per slice
-  constexpr int ROWB = KS * 2 + 16;               // padded LDS row: 80 bytes
-  __shared__ __attribute__((aligned(16))) unsigned char qs[2][TQ * ROWB];
-  __shared__ __attribute__((aligned(16))) unsigned char ksm[2][TK * ROWB];
+  constexpr int TQ = TSM_TQ, TK = TSM_TK, KS = 32;  // tile rows, tile keys, features per slice
+  constexpr int QBYTES = TQ * KS * 2, KBYTES = TK * KS * 2;
+  constexpr int QLPW = QBYTES / 1024 / 4, KLPW = KBYTES / 1024 / 4;  // 1 KB loads per wave
+  __shared__ __attribute__((aligned(16))) unsigned char sm[2][QBYTES + KBYTES];
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63, half = lane >> 5, n = lane & 31;
-  const int64_t key0 = (int64_t)blockIdx.x * TK, r0 = (int64_t)blockIdx.y * TQ, cl = blockIdx.z;
+  // Workgroup order: query tiles fastest, then key tiles, then chunks, renumbered
+  // so each XCD runs a contiguous range. The query tiles of one chunk then read
+  // the same K tile at about the same time from their XCD's L2, and the chunk's
+  // Q stays in L2 while K streams past once per chunk.
+  const int64_t NG = gridDim.x, bid = blockIdx.x;
+  const int64_t wg = (NG % 8 == 0) ? (bid % 8) * (NG / 8) + bid / 8 : bid;
+  const int64_t nq = (pb.C + TQ - 1) / TQ, nk = (pb.Lk + TK - 1) / TK;
+  const int64_t qt = wg % nq, kt = (wg / nq) % nk, cl = wg / (nq * nk);
+  const int64_t key0 = kt * TK, r0 = qt * TQ;
   const int64_t id = ps.c0 + cl, bh = id / ps.nchunk, c = id - bh * ps.nchunk, i0 = c * pb.C;
   if (r0 >= pb.C || i0 + r0 >= pb.Lq) return;
   if (pb.causal) {
@@ -279,52 +297,58 @@ __global__ __launch_bounds__(256, 2) void k_tile_scores_mfma(Problem pb, Pass ps
   const int64_t d = pb.d;
   const uint16_t* Qb = (const uint16_t*)pb.Q;
   const uint16_t* Kh = (const uint16_t*)pb.K + bh * pb.kv_head_stride;
-  // global -> register -> LDS: each thread moves 2 x 16 bytes of Q and of K per slice
-  uint4 pq[2], pk[2];
-  auto issue = [&](int64_t f0) {
+  // rows past the chunk / sequence load the tile's first row (their scores are
+  // never stored); keys past Lk load the last key
+  auto issue = [&](int64_t f0, int buf) {
 #pragma unroll
-    for (int e = 0; e < 2; ++e) {
-      const int cidx = tid + 256 * e, row = cidx >> 2, part = cidx & 3;  // 4 pieces of 16 B per row
-      const int64_t lr = r0 + row, i = i0 + lr, key = key0 + row;
-      pq[e] = (lr < pb.C && i < pb.Lq) ? *(const uint4*)(Qb + (bh * pb.Lq + i) * d + f0 + part * 8)
-                                       : make_uint4(0u, 0u, 0u, 0u);
-      pk[e] = key < pb.Lk ? *(const uint4*)(Kh + key * d + f0 + part * 8) : make_uint4(0u, 0u, 0u, 0u);
+    for (int j = 0; j < QLPW; ++j) {
+      const int cidx = (wave * QLPW + j) * 64 + lane, r = cidx >> 2, p = (cidx & 3) ^ ((r >> 1) & 3);
+      const int64_t lr = r0 + r, i = i0 + lr;
+      const int64_t qi = (lr < pb.C && i < pb.Lq) ? i : i0 + r0;
+      __builtin_amdgcn_global_load_lds((const void*)(Qb + (bh * pb.Lq + qi) * d + f0 + p * 8),
+                                       (__attribute__((address_space(3))) void*)&sm[buf][(wave * QLPW + j) * 1024],
+                                       16, 0, 0);
+    }
+#pragma unroll
+    for (int j = 0; j < KLPW; ++j) {
+      const int cidx = (wave * KLPW + j) * 64 + lane, r = cidx >> 2, p = (cidx & 3) ^ ((r >> 1) & 3);
+      int64_t key = key0 + r;
+      key = key < pb.Lk ? key : pb.Lk - 1;
+      __builtin_amdgcn_global_load_lds(
+          (const void*)(Kh + key * d + f0 + p * 8),
+          (__attribute__((address_space(3))) void*)&sm[buf][QBYTES + (wave * KLPW + j) * 1024], 16, 0, 0);
     }
   };
-  auto stash = [&](int buf) {
-#pragma unroll
-    for (int e = 0; e < 2; ++e) {
-      const int cidx = tid + 256 * e, row = cidx >> 2, part = cidx & 3;
-      *(uint4*)(&qs[buf][row * ROWB + part * 16]) = pq[e];
-      *(uint4*)(&ksm[buf][row * ROWB + part * 16]) = pk[e];
-    }
+  auto frag = [&](const unsigned char* base, int r, int st) {  // features 16*st + 8*half .. +8 of row r
+    const int p = 2 * st + half;
+    return *(const bf16x8*)(base + (r * 4 + (p ^ ((r >> 1) & 3))) * 16);
   };
-  const int wq = (wave >> 1) * 64, wk = (wave & 1) * 64;  // this wave's 64 x 64 sub-tile
-  f32x16 acc[2][2];
+  const int wq = (wave >> 1) * 64, wk = (wave & 1) * 128;  // this wave's 64 x 128 sub-tile
+  f32x16 acc[2][4];
 #pragma unroll
   for (int a = 0; a < 2; ++a)
 #pragma unroll
-    for (int b = 0; b < 2; ++b) acc[a][b] = (f32x16){};
+    for (int b = 0; b < 4; ++b) acc[a][b] = (f32x16){};
   const int64_t nsl = d / KS;
-  issue(0);
+  issue(0, 0);
   for (int64_t sl = 0; sl < nsl; ++sl) {
     const int buf = (int)(sl & 1);
-    stash(buf);
-    __syncthreads();
-    if (sl + 1 < nsl) issue((sl + 1) * KS);
+    __builtin_amdgcn_s_waitcnt(TOPK_WAIT_VM(0));  // this wave's loads of slice sl have landed
+    __syncthreads();  // ... and every wave's; nobody reads the other buffer any more
+    if (sl + 1 < nsl) issue((sl + 1) * KS, buf ^ 1);
+    const unsigned char* qsm = &sm[buf][0];
+    const unsigned char* ksm = &sm[buf][QBYTES];
 #pragma unroll
     for (int st = 0; st < KS / 16; ++st) {
-      bf16x8 av[2], bv[2];
+      bf16x8 qf[2], kf[4];
+#pragma unroll
+      for (int a = 0; a < 2; ++a) qf[a] = frag(qsm, wq + a * 32 + n, st);
+#pragma unroll
+      for (int b = 0; b < 4; ++b) kf[b] = frag(ksm, wk + b * 32 + n, st);
 #pragma unroll
       for (int a = 0; a < 2; ++a)
-        av[a] = *(const bf16x8*)(&qs[buf][(wq + a * 32 + n) * ROWB + st * 32 + half * 16]);
 #pragma unroll
-      for (int b = 0; b < 2; ++b)
-        bv[b] = *(const bf16x8*)(&ksm[buf][(wk + b * 32 + n) * ROWB + st * 32 + half * 16]);
-#pragma unroll
-      for (int a = 0; a < 2; ++a)
-#pragma unroll
-        for (int b = 0; b < 2; ++b) acc[a][b] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(bv[b], av[a], acc[a][b], 0, 0, 0);
+        for (int b = 0; b < 4; ++b) acc[a][b] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf[b], qf[a], acc[a][b], 0, 0, 0);
     }
   }
   // D[m][n]: m = key 8*(v/4) + 4*half + v%4 of block b, n = query lane%32 of block a
@@ -336,7 +360,7 @@ __global__ __launch_bounds__(256, 2) void k_tile_scores_mfma(Problem pb, Pass ps
     const int64_t nv = valid_keys(pb, i);
     float* srow = S + (cl * pb.C + lr) * pb.Lk;
 #pragma unroll
-    for (int b = 0; b < 2; ++b) {
+    for (int b = 0; b < 4; ++b) {
 #pragma unroll
       for (int j = 0; j < 4; ++j) {
         const int64_t key = key0 + wk + b * 32 + 8 * j + 4 * half;
@@ -527,9 +551,6 @@ struct ScanShape<2> {  // 256 queries per workgroup
 template <int G>
 constexpr int scan_queries_per_wg() { return 4 * 32 * G; }
 
-// s_waitcnt immediate that waits until at most n vector-memory operations are
-// outstanding and does not wait on the other counters
-#define TOPK_WAIT_VM(n) (((n) & 15) | (7 << 4) | (15 << 8) | (((n) >> 4) << 14))
 
 template <int D, int R, int G>
 __global__ __launch_bounds__(256, ScanShape<G>::OCC) void k_fused_scan(ScanArgs a) {
@@ -1391,8 +1412,9 @@ hipError_t launch_init(const PassBufs& b, hipStream_t st) {
 
 hipError_t launch_tile_scores(const Problem& pb, const Pass& ps, const PassBufs& b, hipStream_t st) {
   if (pb.dtype == T_BF16 && pb.d % 32 == 0) {
-    dim3 g((unsigned)((pb.Lk + 127) / 128), (unsigned)((pb.C + 127) / 128), (unsigned)ps.nc);
-    k_tile_scores_mfma<0><<<g, 256, 0, st>>>(pb, ps, b.scores);
+    const int64_t g = ((pb.Lk + TSM_TK - 1) / TSM_TK) * ((pb.C + TSM_TQ - 1) / TSM_TQ) * ps.nc;
+    if (g > 0x7FFFFFFF) return hipErrorInvalidValue;
+    k_tile_scores_mfma<0><<<(unsigned)g, 256, 0, st>>>(pb, ps, b.scores);
     return hipGetLastError();
   }
   dim3 grid((unsigned)((pb.Lk + 63) / 64), (unsigned)((pb.C + 63) / 64), (unsigned)ps.nc);
