@@ -378,28 +378,48 @@ __global__ __launch_bounds__(256, 2) void k_tile_scores_mfma(Problem pb, Pass ps
 }
 
 // ------------------------------------------------------------------ row gather helper
-// Appends the key (score, index) of every element of row[0, nv) whose score is
-// >= ts to cbuf (LDS, capacity cap; positions past cap are counted but not
-// written), wave-compacted: reserve(n) returns the base position of this wave's
-// next n keys (wave-uniform). ts = -inf takes every element. Each lane loads
-// 4 x 16 bytes before testing them; rows must start 16-byte aligned when vec.
+// Appends every element of row[0, nv) whose score is >= ts to cbuf (LDS) as the
+// word (raw score bits << 32) | (0xFFFFFFFF - index) (raw_to_key turns it into
+// the order key), wave-compacted: reserve(n) returns the base position of this
+// wave's next n words (wave-uniform). A batch that would cross cap is counted but
+// not written. ts = -inf takes every element. Each lane loads 4 x 16 bytes before
+// testing them; rows must start 16-byte aligned when vec.
 // (The gathered set {score >= ts} holds the row's top k whenever it holds k keys:
 // a key outside it is below every key inside.)
+__device__ __forceinline__ uint64_t raw_to_key(uint64_t w) {
+  return ((uint64_t)ord_u32(__uint_as_float((uint32_t)(w >> 32))) << 32) | (w & 0xFFFFFFFFull);
+}
+
 template <class Reserve>
 __device__ __forceinline__ void gather_row(const float* row, int64_t nv, float ts, bool vec, int64_t lane0,
                                            int64_t lanes, uint64_t* cbuf, uint32_t cap, const Reserve& reserve) {
-  auto offer = [&](int64_t i, float v) {
-    const bool take = i < nv && v >= ts;
+  auto offer = [&](bool take, uint32_t i, float v) {
     const uint64_t bal = __ballot(take);
     if (bal == 0) return;
-    const uint32_t base = reserve((uint32_t)__popcll(bal));
+    const uint32_t cnt = (uint32_t)__popcll(bal);
+    const uint32_t base = reserve(cnt);
+    if (base + cnt > cap) return;  // wave-uniform: the set overflows, nothing is written
     const uint32_t pos = base + __builtin_amdgcn_mbcnt_hi((uint32_t)(bal >> 32), __builtin_amdgcn_mbcnt_lo((uint32_t)bal, 0u));
-    if (take && pos < cap) cbuf[pos] = make_key(v, (uint32_t)i);
+    if (take) cbuf[pos] = ((uint64_t)__float_as_uint(v) << 32) | (uint64_t)(0xFFFFFFFFu - i);
   };
   if (vec) {
     constexpr int U = 4;  // float4 loads in flight per lane
     const int64_t step = 4 * lanes * U;
-    for (int64_t base = 0; base < nv; base += step) {
+    int64_t base = 0;
+    for (; base + step <= nv; base += step) {  // full steps: every element is in the row
+      float4 v[U];
+#pragma unroll
+      for (int u = 0; u < U; ++u) v[u] = *(const float4*)(row + base + 4 * (lane0 + lanes * u));
+#pragma unroll
+      for (int u = 0; u < U; ++u) {
+        const uint32_t i = (uint32_t)(base + 4 * (lane0 + lanes * u));
+        offer(v[u].x >= ts, i, v[u].x);
+        offer(v[u].y >= ts, i + 1, v[u].y);
+        offer(v[u].z >= ts, i + 2, v[u].z);
+        offer(v[u].w >= ts, i + 3, v[u].w);
+      }
+    }
+    for (; base < nv; base += step) {  // the last, partial step
       float4 v[U];
 #pragma unroll
       for (int u = 0; u < U; ++u) {
@@ -416,16 +436,17 @@ __device__ __forceinline__ void gather_row(const float* row, int64_t nv, float t
 #pragma unroll
       for (int u = 0; u < U; ++u) {
         const int64_t i = base + 4 * (lane0 + lanes * u);
-        offer(i, v[u].x);
-        offer(i + 1, v[u].y);
-        offer(i + 2, v[u].z);
-        offer(i + 3, v[u].w);
+        offer(i < nv && v[u].x >= ts, (uint32_t)i, v[u].x);
+        offer(i + 1 < nv && v[u].y >= ts, (uint32_t)i + 1, v[u].y);
+        offer(i + 2 < nv && v[u].z >= ts, (uint32_t)i + 2, v[u].z);
+        offer(i + 3 < nv && v[u].w >= ts, (uint32_t)i + 3, v[u].w);
       }
     }
   } else {
     for (int64_t base = 0; base < nv; base += lanes) {
       const int64_t i = base + lane0;
-      offer(i, i < nv ? row[i] : 0.f);
+      const float v = i < nv ? row[i] : 0.f;
+      offer(i < nv && v >= ts, (uint32_t)i, v);
     }
   }
 }
@@ -480,7 +501,7 @@ __device__ void wg_row_select(const float* row, int64_t nv, uint32_t k_eff, int6
   const uint32_t c = *ccount;
   __syncthreads();
   if (c >= k_eff && c <= (uint32_t)TS_CAP) {
-    auto getkey = [&](int64_t e) { return cand[e]; };
+    auto getkey = [&](int64_t e) { return raw_to_key(cand[e]); };
     team_topk<256>(getkey, c, k_eff, (uint32_t)k, sbuf, P, hist, misc, out);
   } else {
     auto getkey = [&](int64_t e) { return make_key(row[e], (uint32_t)e); };
@@ -1037,7 +1058,7 @@ __device__ __forceinline__ void lds_select_store(const uint64_t* cbuf, int c, ui
 #pragma unroll
   for (int e = 0; e < E; ++e) {
     const int i = lane + 64 * e;
-    key[e] = i < c ? cbuf[i] : 0ull;
+    key[e] = i < c ? raw_to_key(cbuf[i]) : 0ull;
   }
   __syncthreads();  // cbuf may alias sbuf
   wave_select_store<E>(key, c, k_eff, k, sbuf, hist, out);
@@ -1060,8 +1081,9 @@ __global__ __launch_bounds__(64) void k_tile_select_wave(Problem pb, Pass ps, co
   if (nv > CAPW) {
     // sample s = lane + 64 e sits at position floor(s * nv / CAPW) (distinct: nv > CAPW)
     float smp[CAND_REGS];
+    static_assert((int64_t)TSW_MAX_N * CAPW < (int64_t(1) << 31), "sample positions fit 32 bits");
 #pragma unroll
-    for (int e = 0; e < CAND_REGS; ++e) smp[e] = row[((int64_t)(lane + 64 * e) * nv) / CAPW];
+    for (int e = 0; e < CAND_REGS; ++e) smp[e] = row[((uint32_t)(lane + 64 * e) * (uint32_t)nv) / CAPW];
     const float mu = (float)k_eff * (float)CAPW / (float)nv;
     int R = (int)ceilf(mu + 6.0f * sqrtf(mu) + 8.0f);
     R = R < CAPW ? R : CAPW;
