@@ -158,6 +158,16 @@ int topk_profile_begin(void);
 int topk_profile_end(double* stage_ms, int64_t* stage_launches, int n_stages);
 
 /*
+ * Test hook: the number of query rows that the last topk_attn_debug /
+ * topk_ffn_debug call on the calling thread selected through a fallback path
+ * (rows whose sampled threshold or candidate buffers could not prove the
+ * candidate set complete, and were selected from all their keys instead). Debug
+ * calls read this count back from the device, so they wait for their stream.
+ * Returns -1 when the thread's last debug call failed or none was made.
+ */
+int64_t topk_last_fallback_rows(void);
+
+/*
  * Test hook: run one wave of the bf16 MFMA used by the fused path on inputs that
  * tag each operand element with its row or column, and write, for every lane l
  * and accumulator register v, the output row (key) into rows_out[l*16+v] and

@@ -58,6 +58,7 @@ def lib() -> ctypes.CDLL:
         "topk_ffn_workspace_bytes": ([i64] * 5 + [i32], ctypes.c_size_t),
         "topk_set_workspace": ([vp, ctypes.c_size_t], i32),
         "topk_last_error": ([], ctypes.c_char_p),
+        "topk_last_fallback_rows": ([], i64),
         "topk_attn_path": ([i64] * 7 + [i32, i32], i32),
         "topk_ffn_path": ([i64] * 5 + [i32], i32),
         "topk_selftest_mfma_layout": ([vp, vp, vp], i32),
@@ -211,6 +212,11 @@ def profile_end():
     n = (ctypes.c_int64 * len(STAGES))()
     _raise(lib().topk_profile_end(ms, n, len(STAGES)))
     return {s: (ms[i], n[i]) for i, s in enumerate(STAGES)}
+
+
+def last_fallback_rows() -> int:
+    """Rows the last debug call on this thread selected through a fallback path (-1: none / failed)."""
+    return int(lib().topk_last_fallback_rows())
 
 
 def mfma_layout(device="cuda"):

@@ -18,6 +18,7 @@ namespace {
 thread_local std::string g_err;
 thread_local void* g_ws = nullptr;
 thread_local size_t g_ws_bytes = 0;
+thread_local int64_t g_fallback_rows = -1;  // rows a fallback selected in the last debug call
 
 // Optional per-stage timing (topk_profile_begin/end): an event pair around every
 // launch group of the calling thread's calls, on the call's own stream.
@@ -204,6 +205,8 @@ int run(Problem pb, hipStream_t st) {
     own = true;
   }
   hipError_t e = hipSuccess;
+  int64_t fallback = 0;
+  if (pb.idx_out) g_fallback_rows = -1;
   for (int64_t c0 = 0; c0 < pl.total_chunks && e == hipSuccess; c0 += pl.per_pass) {
     Pass ps;
     ps.c0 = c0;
@@ -239,7 +242,14 @@ int run(Problem pb, hipStream_t st) {
       StageTimer t(st, ST_FINAL);
       e = launch_finalize(pb, ps, b, st);
     }
+    if (e == hipSuccess && pb.idx_out) {  // debug calls report the fallback rows (synchronously)
+      int32_t h = 0;
+      e = hipMemcpyAsync(&h, b.redo_count, sizeof(h), hipMemcpyDeviceToHost, st);
+      if (e == hipSuccess) e = hipStreamSynchronize(st);
+      fallback += h;
+    }
   }
+  if (pb.idx_out) g_fallback_rows = e == hipSuccess ? fallback : -1;
   if (own) hipFreeAsync(ws, st);
   if (e != hipSuccess) return fail(TOPK_E_HIP, "kernel launch failed: %s", hipGetErrorString(e));
   return TOPK_OK;
@@ -384,6 +394,8 @@ int topk_set_workspace(void* dev_ptr, size_t bytes) {
 }
 
 const char* topk_last_error(void) { return g_err.c_str(); }
+
+int64_t topk_last_fallback_rows(void) { return g_fallback_rows; }
 
 int topk_attn_path(int64_t B, int64_t H, int64_t Lq, int64_t Lk, int64_t d, int64_t k, int64_t chunk, int causal,
                    int dtype) {

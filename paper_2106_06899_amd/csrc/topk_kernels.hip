@@ -467,8 +467,10 @@ constexpr int TS_SAMPLE = 1024;
 
 // The select of one row of nv fp32 scores by a 256-thread workgroup (see above).
 // cand: TS_CAP keys of LDS; sbuf: pow2_at_least(k_eff) keys of LDS.
+// fallbacks (optional, may be NULL) counts the rows selected by the multi-pass path.
 __device__ void wg_row_select(const float* row, int64_t nv, uint32_t k_eff, int64_t k, bool vec, uint64_t* cand,
-                              uint64_t* sbuf, uint32_t* hist, uint32_t* misc, uint32_t* ccount, uint64_t* out) {
+                              uint64_t* sbuf, uint32_t* hist, uint32_t* misc, uint32_t* ccount, uint64_t* out,
+                              int32_t* fallbacks) {
   const int tid = threadIdx.x, lane = tid & 63;
   const int P = pow2_at_least(k_eff);
   float ts = -INFINITY;  // candidates: scores >= ts
@@ -504,12 +506,14 @@ __device__ void wg_row_select(const float* row, int64_t nv, uint32_t k_eff, int6
     auto getkey = [&](int64_t e) { return raw_to_key(cand[e]); };
     team_topk<256>(getkey, c, k_eff, (uint32_t)k, sbuf, P, hist, misc, out);
   } else {
+    if (fallbacks && tid == 0) atomicAdd(fallbacks, 1);
     auto getkey = [&](int64_t e) { return make_key(row[e], (uint32_t)e); };
     team_topk<256>(getkey, nv, k_eff, (uint32_t)k, sbuf, P, hist, misc, out);
   }
 }
 
-__global__ __launch_bounds__(256) void k_tile_select(Problem pb, Pass ps, const float* S, uint64_t* sel) {
+__global__ __launch_bounds__(256) void k_tile_select(Problem pb, Pass ps, const float* S, uint64_t* sel,
+                                                     int32_t* fallbacks) {
   extern __shared__ uint64_t sbuf[];
   __shared__ uint64_t cand[TS_CAP];
   __shared__ uint32_t hist[256];
@@ -520,7 +524,8 @@ __global__ __launch_bounds__(256) void k_tile_select(Problem pb, Pass ps, const 
   if (!rr.ok) return;
   const int64_t nv = valid_keys(pb, rr.i);
   const uint32_t k_eff = (uint32_t)(pb.k < nv ? pb.k : nv);
-  wg_row_select(S + p * pb.Lk, nv, k_eff, pb.k, (pb.Lk & 3) == 0, cand, sbuf, hist, misc, &ccount, sel + p * pb.k);
+  wg_row_select(S + p * pb.Lk, nv, k_eff, pb.k, (pb.Lk & 3) == 0, cand, sbuf, hist, misc, &ccount, sel + p * pb.k,
+                fallbacks);
 }
 
 // ------------------------------------------------------------------ fused path: scan
@@ -1229,7 +1234,7 @@ __global__ __launch_bounds__(256) void k_redo_select(Problem pb, Pass ps, PassBu
   __shared__ uint64_t cand[TS_CAP];
   __shared__ uint32_t ccount;
   wg_row_select(bufs.scores + r * pb.Lk, nv, k_eff, pb.k, (pb.Lk & 3) == 0, cand, sbuf, hist, misc, &ccount,
-                bufs.sel + p * pb.k);
+                bufs.sel + p * pb.k, nullptr);
 }
 
 template <typename T>
@@ -1454,7 +1459,7 @@ hipError_t launch_tile_select(const Problem& pb, const Pass& ps, const PassBufs&
                                                                     b.redo_count);
     k_tile_select_redo<<<REDO_BLOCKS, 256, (size_t)P * 8, st>>>(pb, ps, b.scores, b.sel, b.redo_list, b.redo_count);
   } else {
-    k_tile_select<<<(unsigned)pass_rows(pb, ps), 256, (size_t)P * 8, st>>>(pb, ps, b.scores, b.sel);
+    k_tile_select<<<(unsigned)pass_rows(pb, ps), 256, (size_t)P * 8, st>>>(pb, ps, b.scores, b.sel, b.redo_count);
   }
   return hipGetLastError();
 }

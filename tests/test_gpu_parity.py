@@ -56,6 +56,14 @@ ATTN_CASES = {
     "c4_d128_fused_all": ("c4", dict(B=1, H=2, Lq=150, Lk=700, causal=False, chunk=64)),
     "bf16_tile_d96": ("c2", dict(B=1, H=2, Lq=70, Lk=300, d=96, k=40, chunk=32)),
     "fp32_causal_tile": ("c1", dict(Lq=200, Lk=260, causal=True, k=20, chunk=64)),
+    # chunk-tile short-row select past 1024 keys: exact sampled rank (R > 96) and
+    # the per-lane top-two threshold (R <= 96)
+    "tile_sampled_exact_rank": ("c2", dict(B=1, H=1, Lq=90, Lk=1500, d=96, k=128, chunk=64)),
+    "tile_sampled_top_two": ("c2", dict(B=1, H=1, Lq=90, Lk=6000, d=96, k=64, chunk=64)),
+    # chunk-tile long-row select (workgroup per row, sampled blocks) and a causal
+    # case whose rows cross 1024 keys
+    "tile_long_rows": ("c2", dict(B=1, H=1, Lq=40, Lk=9500, d=96, k=300, chunk=40)),
+    "c4_causal_long": ("c4", dict(B=1, H=1, Lq=2100, Lk=2100, chunk=1024)),
 }
 
 
@@ -66,7 +74,7 @@ def test_attn_parity(name):
     _say(name, w)
     x = wl.make_inputs(w)
     out, idx, sc = parity.run_attn(w, x)
-    rep = {}
+    rep = {"fallback_rows": tk.last_fallback_rows()}
     parity.check_attn(w, x, out, idx, report=rep)
     _say(name, "ok", rep, "path", tk.attn_path(w.B, w.H, w.Lq, w.Lk, w.d, w.k, w.chunk, w.causal,
                                                 tk.TOPK_BF16 if w.dtype == wl.BF16 else tk.TOPK_F32))
@@ -229,3 +237,70 @@ def test_worked_examples_on_gpu(ex, dtype):
     got = out.float().cpu().numpy()[:, : want.shape[1]]
     tol = 1e-6 if dtype == torch.float32 else 1e-2
     np.testing.assert_allclose(got, want, rtol=tol, atol=tol)
+
+
+def _planted(w: wl.Workload, alpha: np.ndarray, seed: int) -> dict:
+    """Q = e0 + noise, K[j] = alpha[j] e0 + noise, V ~ N(0,1): score(i, j) is about
+    alpha[j], so the test decides which keys win (bf16 storage)."""
+    rng = np.random.Generator(np.random.PCG64(seed))
+    q = 0.3 * rng.standard_normal((w.B, w.H, w.Lq, w.d)).astype(np.float32)
+    q[..., 0] = 1.0
+    k = 0.3 * rng.standard_normal((w.B, w.H, w.Lk, w.d)).astype(np.float32)
+    k[..., 0] = alpha.astype(np.float32)
+    v = rng.standard_normal((w.B, w.H, w.Lk, w.d)).astype(np.float32)
+
+    def t(a):
+        bits = wl.f32_to_bf16_bits(a)
+        return wl.Tensor(wl.bf16_bits_to_f32(bits), bits, wl.BF16)
+
+    return {"Q": t(q), "K": t(k), "V": t(v)}
+
+
+def test_fused_fallback_for_every_row():
+    """Every key of the 1-in-16 sampled tiles scores high, the rest lower: each row's
+    threshold lands above its k-th score, every row is recomputed by the fallback
+    kernels, including more rows than the first fallback kernel takes (1024)."""
+    w = wl.WORKLOADS["c3"].scaled(H=1, Lq=1200, Lk=6000, chunk=1024)
+    assert tk.attn_path(w.B, w.H, w.Lq, w.Lk, w.d, w.k, w.chunk, w.causal, tk.TOPK_BF16) == 1
+    j = np.arange(w.Lk)
+    alpha = np.where((j // 64) % 16 == 0, 10.0, 3.0)
+    _say("fused fallback", w)
+    x = _planted(w, alpha, 7)
+    out, idx, _ = parity.run_attn(w, x)
+    assert tk.last_fallback_rows() == w.Lq
+    parity.check_attn(w, x, out, idx)
+
+
+def test_tile_short_row_fallback():
+    """Only 100 of the 1024 sampled keys score high (the rest of the sample lowest),
+    so the per-lane top-two threshold keeps about 76 < k keys: every row goes to the
+    short-row select's fallback list."""
+    w = wl.WORKLOADS["c2"].scaled(B=1, H=1, Lq=120, Lk=4000, d=96, k=128, chunk=64)
+    assert tk.attn_path(w.B, w.H, w.Lq, w.Lk, w.d, w.k, w.chunk, w.causal, tk.TOPK_BF16) == 2
+    alpha = np.full(w.Lk, 3.0)
+    pos = (np.arange(1024) * w.Lk) // 1024
+    alpha[pos] = -10.0
+    alpha[pos[:100]] = 10.0
+    _say("tile short-row fallback", w)
+    x = _planted(w, alpha, 8)
+    out, idx, _ = parity.run_attn(w, x)
+    assert tk.last_fallback_rows() == w.Lq
+    parity.check_attn(w, x, out, idx)
+
+
+def test_tile_long_row_fallback():
+    """Rows over 8192 keys: 30 of the 1024 sampled keys score high, the rest of the
+    sample lowest; the threshold (24th sampled key) keeps 24 < k keys, and the row is
+    selected by the multi-pass radix select from the tile row."""
+    w = wl.WORKLOADS["c2"].scaled(B=1, H=1, Lq=60, Lk=9000, d=96, k=32, chunk=64)
+    assert tk.attn_path(w.B, w.H, w.Lq, w.Lk, w.d, w.k, w.chunk, w.causal, tk.TOPK_BF16) == 2
+    alpha = np.full(w.Lk, 3.0)
+    s = np.arange(1024)
+    pos = 32 * ((s >> 5) * w.Lk // 1024) + (s & 31)
+    alpha[pos] = -10.0
+    alpha[pos[:30]] = 10.0
+    _say("tile long-row fallback", w)
+    x = _planted(w, alpha, 9)
+    out, idx, _ = parity.run_attn(w, x)
+    assert tk.last_fallback_rows() == w.Lq
+    parity.check_attn(w, x, out, idx)
