@@ -563,7 +563,7 @@ struct ScanArgs {
 constexpr int SCAN_KT = 64;  // keys per K tile
 
 // Launch shape of the scan: G = 32-query groups per wave, NB = K tiles resident
-// in the LDS ring, CAP = staged 16-score blocks per wave (a wave drains its ring
+// in the LDS ring, CAP = staged 8-score half blocks per wave (a wave drains its ring
 // when the next block's dirty lanes would not fit, so a drain is one 64-lane
 // round), OCC = waves per SIMD the register and LDS sizes allow (36 KB of LDS per
 // workgroup: four workgroups per CU).
@@ -571,7 +571,7 @@ template <int G>
 struct ScanShape;
 template <>
 struct ScanShape<2> {  // 256 queries per workgroup
-  static constexpr int NB = 2, CAP = 64, OCC = 4;
+  static constexpr int NB = 2, CAP = 128, OCC = 4;
 };
 
 template <int G>
@@ -580,7 +580,7 @@ constexpr int scan_queries_per_wg() { return 4 * 32 * G; }
 
 template <int D, int R, int G>
 __global__ __launch_bounds__(256, ScanShape<G>::OCC) void k_fused_scan(ScanArgs a) {
-  static_assert(ScanShape<G>::CAP >= 64, "a ring holds at least one block's 64 lanes");
+  static_assert(ScanShape<G>::CAP >= 128, "a ring holds one block's 64 lanes, both halves");
   constexpr int SCAN_NB = ScanShape<G>::NB;
   constexpr int STAGE_CAP = ScanShape<G>::CAP;
   constexpr int KT = SCAN_KT;
@@ -592,8 +592,8 @@ __global__ __launch_bounds__(256, ScanShape<G>::OCC) void k_fused_scan(ScanArgs 
   constexpr int QB = scan_queries_per_wg<G>();
   static_assert(LPW >= 1 && TILEB % 4096 == 0, "tile must split evenly over the 4 waves");
   __shared__ __attribute__((aligned(16))) unsigned char ks[SCAN_NB][TILEB];
-  // staging slot = the 16 scores (64 bytes) of one dirty lane block
-  __shared__ __attribute__((aligned(16))) float stage[4][STAGE_CAP][16];
+  // staging slot = 8 scores (32 bytes): one dirty half of a lane block
+  __shared__ __attribute__((aligned(16))) float stage[4][STAGE_CAP][8];
   __shared__ uint32_t stage_meta[4][STAGE_CAP];
   __shared__ float tau_lds[4][32 * G];
   __shared__ uint32_t cnt_lds[4][64 * G];
@@ -731,7 +731,9 @@ __global__ __launch_bounds__(256, ScanShape<G>::OCC) void k_fused_scan(ScanArgs 
   }
 
   // ---- staging ring and its drain (all per wave; LDS ops of one wave execute in order)
-  // slot meta = (32-key block index << 8) | (group << 6) | lane
+  // A slot holds one dirty half (8 scores) of a lane block: scores 8*hb .. 8*hb+7.
+  // slot meta = (32-key block index << 8) | (hb << 7) | (group << 6) | lane
+  static_assert(G <= 2, "the slot meta holds one group bit");
   int scount = 0;  // wave-uniform
   auto drain = [&]() {
     __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
@@ -743,20 +745,20 @@ __global__ __launch_bounds__(256, ScanShape<G>::OCC) void k_fused_scan(ScanArgs 
       const float* sp = &stage[wave][slot < STAGE_CAP ? slot : 0][0];
       if (slot < scount) {
         meta = stage_meta[wave][slot];
-        const float t = tau_lds[wave][(meta >> 6 & 3) * 32 + (meta & 31)];
-        // neighbouring slots start their four 16-byte reads at different chunks,
+        const float t = tau_lds[wave][(meta >> 6 & 1) * 32 + (meta & 31)];
+        // slots 4..7 of every 8 read their two 16-byte chunks in the other order,
         // so the 8 lanes one LDS cycle serves hit 8 different bank groups
-        const uint32_t r = (uint32_t)(slot >> 1) & 3u;
+        const uint32_t r = (uint32_t)(slot >> 2) & 1u;
 #pragma unroll
-        for (uint32_t q4 = 0; q4 < 4; ++q4) {
-          const uint32_t cc = (q4 + r) & 3u;
+        for (uint32_t q4 = 0; q4 < 2; ++q4) {
+          const uint32_t cc = q4 ^ r;
           const float4 x = *(const float4*)(sp + 4 * cc);
           const uint32_t m4 = (x.x > t ? 1u : 0u) | (x.y > t ? 2u : 0u) | (x.z > t ? 4u : 0u) | (x.w > t ? 8u : 0u);
           mask |= m4 << (4 * cc);
         }
       }
       if (mask) {
-        const uint32_t ql = meta & 63, g = meta >> 6 & 3, h = ql >> 5;
+        const uint32_t ql = meta & 63, g = meta >> 6 & 1, h = ql >> 5, hb = meta >> 7 & 1;
         // one counter update per slot reserves room for all its passing scores
         uint32_t pos = atomicAdd(&cnt_lds[wave][g * 64 + ql], (uint32_t)__builtin_popcount(mask));
         const uint32_t nj = 0xFFFFFFFFu - ((meta >> 8) * 32u + 4u * h);
@@ -764,9 +766,11 @@ __global__ __launch_bounds__(256, ScanShape<G>::OCC) void k_fused_scan(ScanArgs 
         do {
           const uint32_t v = __builtin_ctz(mask);
           mask &= mask - 1;
-          // score v of the block is key 8*(v/4) + v%4 = v + (v & ~3) past the block's first key
+          // score u = 8*hb + v of the block is key 8*(u/4) + u%4 = u + (u & ~3) past the block's first key
+          const uint32_t u = 8u * hb + v;
+          const float sc = sp[v];
           if (pos < (uint32_t)a.caph)
-            dst[pos] = ((uint64_t)__float_as_uint(sp[v]) << 32) | (uint64_t)(nj - (v + (v & 12u)));
+            dst[pos] = ((uint64_t)__float_as_uint(sc) << 32) | (uint64_t)(nj - (u + (u & 12u)));
           ++pos;
         } while (mask);
       }
@@ -776,23 +780,52 @@ __global__ __launch_bounds__(256, ScanShape<G>::OCC) void k_fused_scan(ScanArgs 
     __builtin_amdgcn_wave_barrier();
     __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
   };
+  // A lane whose block maximum beats its query's threshold stages its dirty half
+  // (the lower one when both are dirty); lanes with both halves dirty stage the
+  // upper half in a second, rarely needed, round. Two 16-byte writes per lane and
+  // round instead of four.
   auto filter = [&](int g, const f32x16& acc, int64_t t, int rb) {
-    const bool dirty = block_max(acc) > tau[g];
+    float hA = fmaxf(acc[0], acc[1]), hB = fmaxf(acc[8], acc[9]);
+#pragma unroll
+    for (int v = 2; v < 8; ++v) {
+      hA = fmaxf(hA, acc[v]);
+      hB = fmaxf(hB, acc[8 + v]);
+    }
+    const bool dA = hA > tau[g], dB = hB > tau[g];
+    const bool dirty = dA || dB;
     const uint64_t bal = __ballot(dirty);
     if (bal == 0) return;
-    const int nd = __popcll(bal);
-    if (scount + nd > STAGE_CAP) drain();
+    const bool both = dA && dB;
+    const uint64_t bal2 = __ballot(both);
+    const int n1 = __popcll(bal), n2 = __popcll(bal2);
+    if (scount + n1 + n2 > STAGE_CAP) drain();
+    const uint32_t mb = (uint32_t)((t * KT + rb * 32) / 32) << 8 | (uint32_t)(g << 6) | (uint32_t)lane;
     if (dirty) {
-      const int rank = __builtin_amdgcn_mbcnt_hi((uint32_t)(bal >> 32), __builtin_amdgcn_mbcnt_lo((uint32_t)bal, 0u));
-      const int slot = scount + rank;
+      const int slot = scount + (int)__builtin_amdgcn_mbcnt_hi((uint32_t)(bal >> 32),
+                                                               __builtin_amdgcn_mbcnt_lo((uint32_t)bal, 0u));
       float4* sp = (float4*)&stage[wave][slot][0];
-      sp[0] = make_float4(acc[0], acc[1], acc[2], acc[3]);
-      sp[1] = make_float4(acc[4], acc[5], acc[6], acc[7]);
-      sp[2] = make_float4(acc[8], acc[9], acc[10], acc[11]);
-      sp[3] = make_float4(acc[12], acc[13], acc[14], acc[15]);
-      stage_meta[wave][slot] = (uint32_t)((t * KT + rb * 32) / 32) << 8 | (uint32_t)(g << 6) | (uint32_t)lane;
+      // the half to stage, selected in registers (a bitwise mux per score, so the
+      // compiler does not turn it into an indexed read of the accumulator)
+      const uint32_t sel = dA ? 0xFFFFFFFFu : 0u;
+      float x[8];
+#pragma unroll
+      for (int v = 0; v < 8; ++v)
+        x[v] = __uint_as_float((__float_as_uint(acc[v]) & sel) | (__float_as_uint(acc[8 + v]) & ~sel));
+      sp[0] = make_float4(x[0], x[1], x[2], x[3]);
+      sp[1] = make_float4(x[4], x[5], x[6], x[7]);
+      stage_meta[wave][slot] = mb | (dA ? 0u : 128u);
     }
-    scount += nd;
+    if (bal2) {
+      if (both) {
+        const int slot = scount + n1 + (int)__builtin_amdgcn_mbcnt_hi((uint32_t)(bal2 >> 32),
+                                                                      __builtin_amdgcn_mbcnt_lo((uint32_t)bal2, 0u));
+        float4* sp = (float4*)&stage[wave][slot][0];
+        sp[0] = make_float4(acc[8], acc[9], acc[10], acc[11]);
+        sp[1] = make_float4(acc[12], acc[13], acc[14], acc[15]);
+        stage_meta[wave][slot] = mb | 128u;
+      }
+    }
+    scount += n1 + n2;
   };
   // Main scan: a stream of 32-key blocks. When a block opens a new tile, that
   // tile's wait and barrier (and the loads of the tile SCAN_NB - 1 further on,
