@@ -94,3 +94,13 @@ def test_workspace_is_linear_in_length_and_capped():
     assert tile[1] > tile[0]
     assert tk.attn_workspace_bytes(1, 1, 10, 10, 64, 0) == 0
     assert tk.ffn_workspace_bytes(16384, 1024, 65536, 512, 1024) <= (8 << 30) + (64 << 20)
+
+
+def test_bench_refuses_more_than_one_gpu():
+    """bench.py measures one GPU; asking for more exits with a message before touching a GPU."""
+    import subprocess
+    import sys
+    r = subprocess.run([sys.executable, os.path.join(ROOT, "bench.py"), "--gpus", "2"], capture_output=True, text=True,
+                       timeout=120)
+    assert r.returncode != 0
+    assert "one GPU" in r.stderr
