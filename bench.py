@@ -140,7 +140,7 @@ def main():
         print(json.dumps({"copy_probe_bytes": src.numel() * 4, "launches": 5}))
         return
     if args.gpus != 1:
-        print(f"bench.py measures one GPU only (asked for {args.gpus}); this build has no multi-GPU path.",
+        print(f"bench.py measures one GPU only (asked for {args.gpus}); there is no multi-GPU path.",
               file=sys.stderr)
         sys.exit(2)
 

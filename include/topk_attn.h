@@ -48,7 +48,7 @@ extern "C" {
 #define TOPK_E_INVAL -1       /* a size, k, chunk, scale, flag or dtype is out of range */
 #define TOPK_E_NULL -2        /* a required pointer is NULL */
 #define TOPK_E_ALIGN -3       /* a tensor pointer is not 16-byte aligned */
-#define TOPK_E_UNSUPPORTED -4 /* valid arguments outside what this build implements */
+#define TOPK_E_UNSUPPORTED -4 /* valid arguments outside what the library implements */
 #define TOPK_E_NOMEM -5       /* the registered workspace is too small / allocation failed */
 #define TOPK_E_HIP -6         /* a HIP runtime call or kernel launch failed */
 

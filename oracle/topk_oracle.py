@@ -20,7 +20,7 @@ the paper gives the steps:
 Query chunking (Section 2.2, "Query chunking") only bounds memory; each chunk is
 computed from ``Q_C, K, V`` alone, so the result does not depend on the chunk size.
 
-Readings of points the paper leaves open (each is listed in the design doc):
+Readings of points the paper leaves open:
 
 * selection uses the raw score ``q.k``; the temperature ``scale`` (= 1/lambda of
   Eq. 1) multiplies scores only inside the softmax, and is the float32 value the

@@ -94,8 +94,8 @@ int validate_shape(int64_t BH_a, int64_t BH_b, int64_t Lq, int64_t Lk, int64_t d
   if (attn && !(isfinite(scale) && scale > 0.f)) return fail(TOPK_E_INVAL, "scale must be finite and > 0");
   if (dtype != TOPK_F32 && dtype != TOPK_BF16) return fail(TOPK_E_INVAL, "dtype must be TOPK_F32 or TOPK_BF16");
   if (d % 8 != 0 || d > 1024)
-    return fail(TOPK_E_UNSUPPORTED, "feature size %lld: this build needs a multiple of 8, at most 1024", (long long)d);
-  if (k > MAX_SELECT_K) return fail(TOPK_E_UNSUPPORTED, "k = %lld exceeds this build's limit %d", (long long)k, MAX_SELECT_K);
+    return fail(TOPK_E_UNSUPPORTED, "feature size %lld: the library needs a multiple of 8, at most 1024", (long long)d);
+  if (k > MAX_SELECT_K) return fail(TOPK_E_UNSUPPORTED, "k = %lld exceeds the library's limit %d", (long long)k, MAX_SELECT_K);
   if (Lk > 0x7FFFFFFFLL) return fail(TOPK_E_UNSUPPORTED, "more than 2^31 - 1 keys");
   return TOPK_OK;
 }
