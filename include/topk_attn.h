@@ -149,13 +149,54 @@ int topk_ffn_path(int64_t N, int64_t d_model, int64_t d_ff, int64_t k,
  * the calling thread records a pair of HIP events on its own stream around each
  * launch group: stage 0 = score tiles (fused scan, or chunk-tile scores),
  * 1 = row select, 2 = fallback recomputation (fused path only), 3 = activation
- * and gather. topk_profile_end() waits for those events, writes the summed
+ * and gather, 4 = a backward call. topk_profile_end() waits for those events, writes the summed
  * milliseconds and the number of timed launches of the first n_stages stages
  * into stage_ms / stage_launches (host arrays, either may be NULL) and stops
  * recording. Returns TOPK_OK or TOPK_E_HIP.
  */
 int topk_profile_begin(void);
 int topk_profile_end(double* stage_ms, int64_t* stage_launches, int n_stages);
+
+/*
+ * Backward pass of top-k attention with input checkpointing (Section 2.2, "Input
+ * checkpointing", and the backward pseudo-code that follows it). The forward pass
+ * caches only its inputs and each row's selection: top_idx (int32 [B, H, Lq, k],
+ * -1 pads) and top_dots (float [B, H, Lq, k], the raw fp32 scores q . k of the
+ * selected keys), exactly what topk_attn_debug writes as idx_out / score_out.
+ * Given d_out = dLoss/d(out) ([B, H, Lq, d]), this recomputes the softmax with
+ * temperature `scale` over the k survivors from the cached scores, backpropagates
+ * through it, and writes
+ *   d_Q [B, H, Lq, d] = sum_m d_top_dots[m] K[j_m]             (per query row),
+ *   d_K [B, H, Lk, d] = sum over the rows that selected key j of d_top_dots * Q[row],
+ *   d_V [B, H, Lk, d] = sum over the rows that selected key j of weight * d_out[row],
+ * keys selected by no row get zeros. All tensors are caller-owned device memory,
+ * contiguous, in `dtype` (fp32 accumulation; bf16 results rounded to nearest even);
+ * every output element is written. Entries of top_idx outside [0, Lk) are padding.
+ * The sums over a key's rows run in increasing (row, slot) order when at most 1024
+ * rows selected the key, so results do not depend on scheduling. Workspace:
+ * topk_attn_backward_workspace_bytes() bytes, O(B*H*(Lq*k + Lk)) (the registered
+ * workspace, or one allocated on the stream). Errors as topk_attn; additionally
+ * TOPK_E_UNSUPPORTED when B*H*Lq*k or B*H*Lk reaches 2^31.
+ */
+int topk_attn_backward(const void* Q, const void* K, const void* V, const int32_t* top_idx, const float* top_dots,
+                       const void* d_out, void* d_Q, void* d_K, void* d_V, int64_t B, int64_t H, int64_t Lq,
+                       int64_t Lk, int64_t d, int64_t k, float scale, int dtype, void* hip_stream);
+
+/*
+ * Backward pass of the top-k feed-forward layer (Eq. 3 as top-k attention: keys
+ * W1, values W2, ReLU, no temperature), with the same cache (top_idx, top_dots:
+ * [N, k], as topk_ffn_debug writes them) and d_out [N, d_model]. Writes
+ * d_X [N, d_model], d_W1 [d_ff, d_model], d_W2 [d_ff, d_model]; the ReLU gradient is
+ * zero where the cached score is <= 0. Same conventions as topk_attn_backward.
+ */
+int topk_ffn_backward(const void* X, const void* W1, const void* W2, const int32_t* top_idx, const float* top_dots,
+                      const void* d_out, void* d_X, void* d_W1, void* d_W2, int64_t N, int64_t d_model, int64_t d_ff,
+                      int64_t k, int dtype, void* hip_stream);
+
+/* Workspace the backward calls need (0 for invalid arguments). */
+size_t topk_attn_backward_workspace_bytes(int64_t B, int64_t H, int64_t Lq, int64_t Lk, int64_t d, int64_t k,
+                                          int dtype);
+size_t topk_ffn_backward_workspace_bytes(int64_t N, int64_t d_model, int64_t d_ff, int64_t k, int dtype);
 
 /*
  * Test hook: the number of query rows that the last topk_attn_debug /

@@ -59,6 +59,10 @@ def lib() -> ctypes.CDLL:
         "topk_set_workspace": ([vp, ctypes.c_size_t], i32),
         "topk_last_error": ([], ctypes.c_char_p),
         "topk_last_fallback_rows": ([], i64),
+        "topk_attn_backward": ([vp] * 9 + [i64] * 6 + [ctypes.c_float, i32, vp], i32),
+        "topk_ffn_backward": ([vp] * 9 + [i64] * 4 + [i32, vp], i32),
+        "topk_attn_backward_workspace_bytes": ([i64] * 6 + [i32], ctypes.c_size_t),
+        "topk_ffn_backward_workspace_bytes": ([i64] * 4 + [i32], ctypes.c_size_t),
         "topk_attn_path": ([i64] * 7 + [i32, i32], i32),
         "topk_ffn_path": ([i64] * 5 + [i32], i32),
         "topk_selftest_mfma_layout": ([vp, vp, vp], i32),
@@ -198,7 +202,66 @@ def ffn(x, w1, w2, topk: int, chunk: int = 0, debug: bool = False):
     return out
 
 
-STAGES = ("score", "select", "redo", "finalize")
+def attn_backward(q, k, v, idx, dots, d_out, scale: float | None = None):
+    """Gradients (d_q, d_k, d_v) of top-k attention from the forward's cache: idx and
+    dots are what ``attn(..., debug=True)`` returns (selected keys, their raw scores).
+    Input checkpointing (Section 2.2): no Lq x Lk matrix is formed."""
+    import torch
+    device = q.device
+    _check(q, "q", 4, q.dtype, device)
+    _check(k, "k", 4, q.dtype, device)
+    _check(v, "v", 4, q.dtype, device)
+    _check(d_out, "d_out", 4, q.dtype, device)
+    B, H, Lq, d = q.shape
+    Lk = k.shape[2]
+    topk = idx.shape[-1]
+    if tuple(k.shape) != (B, H, Lk, d) or tuple(v.shape) != (B, H, Lk, d) or tuple(d_out.shape) != (B, H, Lq, d):
+        raise ValueError("shape mismatch")
+    if idx.dtype != torch.int32 or dots.dtype != torch.float32 or tuple(idx.shape) != (B, H, Lq, topk) \
+            or tuple(dots.shape) != (B, H, Lq, topk) or not idx.is_contiguous() or not dots.is_contiguous():
+        raise ValueError("idx (int32) and dots (float32) must be contiguous [B, H, Lq, k]")
+    dt = _dtype_code(q)
+    if scale is None:
+        scale = 1.0 / math.sqrt(d)
+    dq, dk, dv = torch.empty_like(q), torch.empty_like(k), torch.empty_like(v)
+    L = lib()
+    nbytes = L.topk_attn_backward_workspace_bytes(B, H, Lq, Lk, d, topk, dt)
+    args = (q.data_ptr(), k.data_ptr(), v.data_ptr(), idx.data_ptr(), dots.data_ptr(), d_out.data_ptr(),
+            dq.data_ptr(), dk.data_ptr(), dv.data_ptr(), B, H, Lq, Lk, d, topk, float(scale), dt, _stream_ptr(device))
+    if nbytes == 0:
+        _raise(L.topk_attn_backward(*args))
+    _with_workspace(nbytes, device, lambda: L.topk_attn_backward(*args))
+    return dq, dk, dv
+
+
+def ffn_backward(x, w1, w2, idx, dots, d_out):
+    """Gradients (d_x, d_w1, d_w2) of the top-k feed-forward layer from the forward's
+    cache (idx, dots as ``ffn(..., debug=True)`` returns them)."""
+    import torch
+    device = x.device
+    for t, n in ((x, "x"), (w1, "w1"), (w2, "w2"), (d_out, "d_out")):
+        _check(t, n, 2, x.dtype, device)
+    N, dm = x.shape
+    dff = w1.shape[0]
+    topk = idx.shape[-1]
+    if tuple(w1.shape) != (dff, dm) or tuple(w2.shape) != (dff, dm) or tuple(d_out.shape) != (N, dm):
+        raise ValueError("shape mismatch")
+    if idx.dtype != torch.int32 or dots.dtype != torch.float32 or tuple(idx.shape) != (N, topk) \
+            or tuple(dots.shape) != (N, topk) or not idx.is_contiguous() or not dots.is_contiguous():
+        raise ValueError("idx (int32) and dots (float32) must be contiguous [N, k]")
+    dt = _dtype_code(x)
+    dx, dw1, dw2 = torch.empty_like(x), torch.empty_like(w1), torch.empty_like(w2)
+    L = lib()
+    nbytes = L.topk_ffn_backward_workspace_bytes(N, dm, dff, topk, dt)
+    args = (x.data_ptr(), w1.data_ptr(), w2.data_ptr(), idx.data_ptr(), dots.data_ptr(), d_out.data_ptr(),
+            dx.data_ptr(), dw1.data_ptr(), dw2.data_ptr(), N, dm, dff, topk, dt, _stream_ptr(device))
+    if nbytes == 0:
+        _raise(L.topk_ffn_backward(*args))
+    _with_workspace(nbytes, device, lambda: L.topk_ffn_backward(*args))
+    return dx, dw1, dw2
+
+
+STAGES = ("score", "select", "redo", "finalize", "backward")
 
 
 def profile_begin():

@@ -22,7 +22,7 @@ thread_local int64_t g_fallback_rows = -1;  // rows a fallback selected in the l
 
 // Optional per-stage timing (topk_profile_begin/end): an event pair around every
 // launch group of the calling thread's calls, on the call's own stream.
-enum Stage { ST_SCORE = 0, ST_SELECT = 1, ST_REDO = 2, ST_FINAL = 3, N_STAGES = 4 };
+enum Stage { ST_SCORE = 0, ST_SELECT = 1, ST_REDO = 2, ST_FINAL = 3, ST_BWD = 4, N_STAGES = 5 };
 struct Mark {
   hipEvent_t a, b;
   int stage;
@@ -329,6 +329,88 @@ size_t workspace_for(const Problem& pb) {
   return plan_total(pl, pb);
 }
 
+// ---------------------------------------------------------------- backward
+size_t bwd_bytes(const BwdProblem& bp) {
+  const int64_t nkeys = bp.BH * bp.Lk, npairs = bp.BH * bp.Lq * bp.k, nb = (nkeys + 1 + 1023) / 1024;
+  return up((size_t)npairs * 8) + up((size_t)(nkeys + 1) * 4) + up((size_t)nkeys * 4) + up((size_t)npairs * 4) +
+         up((size_t)nb * 4);
+}
+
+BwdBufs bwd_carve(const BwdProblem& bp, char* ws) {
+  const int64_t nkeys = bp.BH * bp.Lk, npairs = bp.BH * bp.Lq * bp.k;
+  BwdBufs b;
+  size_t off = 0;
+  b.pair = (float2*)(ws + off);
+  off += up((size_t)npairs * 8);
+  b.count = (int32_t*)(ws + off);
+  off += up((size_t)(nkeys + 1) * 4);
+  b.fill = (int32_t*)(ws + off);
+  off += up((size_t)nkeys * 4);
+  b.list = (int32_t*)(ws + off);
+  off += up((size_t)npairs * 4);
+  b.block_sums = (int32_t*)(ws + off);
+  return b;
+}
+
+int bwd_problem(BwdProblem* bp, const void* Q, const void* K, const void* V, const int32_t* idx, const float* dots,
+                const void* dout, void* dQ, void* dK, void* dV, int64_t BH, int64_t Lq, int64_t Lk, int64_t d,
+                int64_t k, int64_t kv_head_stride, float scale, int dtype, int act, bool check_ptrs) {
+  int rc = validate_shape(BH, 1, Lq, Lk, d, k, 0, 0, scale, dtype, act == ACT_SOFTMAX);
+  if (rc) return rc;
+  if (BH * Lq > (int64_t(1) << 31) / k || BH * Lk >= (int64_t(1) << 31) - 1)
+    return fail(TOPK_E_UNSUPPORTED, "the backward pass needs rows * k and heads * keys below 2^31");
+  if (check_ptrs) {
+    if ((rc = check_ptr(Q, "queries")) || (rc = check_ptr(K, "keys")) || (rc = check_ptr(V, "values")) ||
+        (rc = check_ptr(dout, "d_out")) || (rc = check_ptr(dQ, "d_queries")) || (rc = check_ptr(dK, "d_keys")) ||
+        (rc = check_ptr(dV, "d_values")))
+      return rc;
+    if (!idx || !dots) return fail(TOPK_E_NULL, "top_idx and top_dots are required");
+    if (((uintptr_t)idx) % 4 || ((uintptr_t)dots) % 4) return fail(TOPK_E_ALIGN, "top_idx / top_dots not 4-byte aligned");
+  }
+  bp->Q = Q;
+  bp->K = K;
+  bp->V = V;
+  bp->idx = idx;
+  bp->dots = dots;
+  bp->dout = dout;
+  bp->dQ = dQ;
+  bp->dK = dK;
+  bp->dV = dV;
+  bp->BH = BH;
+  bp->Lq = Lq;
+  bp->Lk = Lk;
+  bp->d = d;
+  bp->k = k;
+  bp->kv_head_stride = kv_head_stride;
+  bp->scale = scale;
+  bp->dtype = dtype == TOPK_BF16 ? T_BF16 : T_F32;
+  bp->act = act;
+  return TOPK_OK;
+}
+
+int run_backward(const BwdProblem& bp, hipStream_t st) {
+  const size_t need = bwd_bytes(bp);
+  char* ws = (char*)g_ws;
+  bool own = false;
+  if (g_ws) {
+    if (need > g_ws_bytes)
+      return fail(TOPK_E_NOMEM, "registered workspace of %zu bytes is below the %zu bytes the backward pass needs",
+                  g_ws_bytes, need);
+  } else {
+    if (hipMallocAsync((void**)&ws, need, st) != hipSuccess)
+      return fail(TOPK_E_NOMEM, "could not allocate %zu bytes of workspace", need);
+    own = true;
+  }
+  hipError_t e;
+  {
+    StageTimer t(st, ST_BWD);
+    e = launch_backward(bp, bwd_carve(bp, ws), st);
+  }
+  if (own) hipFreeAsync(ws, st);
+  if (e != hipSuccess) return fail(TOPK_E_HIP, "kernel launch failed: %s", hipGetErrorString(e));
+  return TOPK_OK;
+}
+
 }  // namespace
 }  // namespace topk
 
@@ -391,6 +473,47 @@ int topk_set_workspace(void* dev_ptr, size_t bytes) {
   g_ws = bytes ? dev_ptr : nullptr;
   g_ws_bytes = dev_ptr ? bytes : 0;
   return TOPK_OK;
+}
+
+int topk_attn_backward(const void* Q, const void* K, const void* V, const int32_t* top_idx, const float* top_dots,
+                       const void* d_out, void* d_Q, void* d_K, void* d_V, int64_t B, int64_t H, int64_t Lq,
+                       int64_t Lk, int64_t d, int64_t k, float scale, int dtype, void* hip_stream) {
+  g_err.clear();
+  if (B < 1 || H < 1 || B > (int64_t(1) << 31) / H) return fail(TOPK_E_INVAL, "B and H must be >= 1, B*H < 2^31");
+  BwdProblem bp;
+  int rc = bwd_problem(&bp, Q, K, V, top_idx, top_dots, d_out, d_Q, d_K, d_V, B * H, Lq, Lk, d, k, Lk * d, scale,
+                       dtype, ACT_SOFTMAX, true);
+  if (rc) return rc;
+  return run_backward(bp, (hipStream_t)hip_stream);
+}
+
+int topk_ffn_backward(const void* X, const void* W1, const void* W2, const int32_t* top_idx, const float* top_dots,
+                      const void* d_out, void* d_X, void* d_W1, void* d_W2, int64_t N, int64_t d_model, int64_t d_ff,
+                      int64_t k, int dtype, void* hip_stream) {
+  g_err.clear();
+  BwdProblem bp;
+  int rc = bwd_problem(&bp, X, W1, W2, top_idx, top_dots, d_out, d_X, d_W1, d_W2, 1, N, d_ff, d_model, k, 0, 1.f,
+                       dtype, ACT_RELU, true);
+  if (rc) return rc;
+  return run_backward(bp, (hipStream_t)hip_stream);
+}
+
+size_t topk_attn_backward_workspace_bytes(int64_t B, int64_t H, int64_t Lq, int64_t Lk, int64_t d, int64_t k,
+                                          int dtype) {
+  if (B < 1 || H < 1 || B > (int64_t(1) << 31) / H) return 0;
+  BwdProblem bp;
+  if (bwd_problem(&bp, nullptr, nullptr, nullptr, nullptr, nullptr, nullptr, nullptr, nullptr, nullptr, B * H, Lq,
+                  Lk, d, k, Lk * d, 1.f, dtype, ACT_SOFTMAX, false))
+    return 0;
+  return bwd_bytes(bp);
+}
+
+size_t topk_ffn_backward_workspace_bytes(int64_t N, int64_t d_model, int64_t d_ff, int64_t k, int dtype) {
+  BwdProblem bp;
+  if (bwd_problem(&bp, nullptr, nullptr, nullptr, nullptr, nullptr, nullptr, nullptr, nullptr, nullptr, 1, N, d_ff,
+                  d_model, k, 0, 1.f, dtype, ACT_RELU, false))
+    return 0;
+  return bwd_bytes(bp);
 }
 
 const char* topk_last_error(void) { return g_err.c_str(); }

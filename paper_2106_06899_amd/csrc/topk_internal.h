@@ -72,4 +72,33 @@ hipError_t launch_redo(const Problem& pb, const Pass& ps, const PassBufs& b, hip
 hipError_t launch_finalize(const Problem& pb, const Pass& ps, const PassBufs& b, hipStream_t st);
 hipError_t launch_mfma_probe(int32_t* rows, int32_t* cols, hipStream_t st);
 
+// Backward pass with input checkpointing. Rows of Q / dQ / d_out / idx / dots are
+// (bh * Lq + i); keys (bh, j) of K, V, dK, dV sit at (bh * kv_head_stride + j * d)
+// (the FFN is one head with kv_head_stride = 0 and X, W1, W2 as Q, K, V).
+struct BwdProblem {
+  const void* Q;
+  const void* K;
+  const void* V;
+  const int32_t* idx;   // [rows, k] selected keys, entries outside [0, Lk) are padding
+  const float* dots;    // [rows, k] their raw scores
+  const void* dout;     // [rows, d]
+  void* dQ;
+  void* dK;
+  void* dV;
+  int64_t BH, Lq, Lk, d, k, kv_head_stride;
+  float scale;
+  int dtype;
+  int act;
+};
+
+struct BwdBufs {
+  float2* pair;         // [rows * k]: (activation weight, score gradient)
+  int32_t* count;       // [BH * Lk + 1]: pairs per key, then exclusive offsets
+  int32_t* fill;        // [BH * Lk]: per-key fill cursors
+  int32_t* list;        // [rows * k]: pair ids grouped by key
+  int32_t* block_sums;  // [ceil((BH * Lk + 1) / 1024)] scan scratch
+};
+
+hipError_t launch_backward(const BwdProblem& bp, const BwdBufs& b, hipStream_t st);
+
 }  // namespace topk

@@ -19,6 +19,8 @@
 
 #include <math.h>
 
+#include <type_traits>
+
 namespace topk {
 
 typedef __bf16 bf16x8 __attribute__((__vector_size__(16)));
@@ -1559,6 +1561,315 @@ hipError_t launch_finalize(const Problem& pb, const Pass& ps, const PassBufs& b,
 
 hipError_t launch_mfma_probe(int32_t* rows, int32_t* cols, hipStream_t st) {
   k_mfma_probe<<<1, 64, 0, st>>>(rows, cols);
+  return hipGetLastError();
+}
+
+
+// ------------------------------------------------------------------ backward pass
+// Input checkpointing (Section 2.2, "Input checkpointing", and the backward
+// pseudo-code): the forward caches only its inputs and each row's selected keys
+// with their raw scores. The backward pass recomputes the activation on the k
+// survivors, backpropagates through it, and forms the three gradients by gathers,
+// never an Lq x Lk matrix:
+//  1. k_bwd_rows (one wave per query row): d_top_actv[m] = d_out . V[j_m] for the
+//     k selected keys; the activation (softmax with temperature, or ReLU)
+//     recomputed from the cached scores and backpropagated to d_top_dots;
+//     d_Q = sum_m d_top_dots[m] K[j_m]; each pair's (weight, score gradient) is
+//     kept and the pairs per key are counted;
+//  2. an exclusive scan of the per-key counts (k_bwd_scan_*);
+//  3. k_bwd_fill: each pair's id into its key's list;
+//  4. k_bwd_keys (one wave per key): d_V[j] = sum weight * d_out[row] and
+//     d_K[j] = sum score gradient * Q[row] over the key's list, in increasing pair
+//     order (lists of up to 1024 pairs are sorted first). No floating-point
+//     atomics: the sums do not depend on scheduling.
+constexpr int BWD_MAXF = 16;  // features per lane (d <= 1024)
+
+__global__ void k_bwd_zero(int32_t* p, int64_t n) {
+  for (int64_t e = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; e < n; e += (int64_t)gridDim.x * blockDim.x)
+    p[e] = 0;
+}
+
+__device__ __forceinline__ void wave_sync_lds() {
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+  __builtin_amdgcn_wave_barrier();
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+}
+
+__device__ __forceinline__ float wave_sum(float x) {
+#pragma unroll
+  for (int off = 32; off > 0; off >>= 1) x += __shfl_xor(x, off, 64);
+  return x;
+}
+__device__ __forceinline__ float wave_max(float x) {
+#pragma unroll
+  for (int off = 32; off > 0; off >>= 1) x = fmaxf(x, __shfl_xor(x, off, 64));
+  return x;
+}
+
+// sum_t x[t] * row[off + t] over n features (n % 8 == 0, off % 8 == 0)
+template <typename T>
+__device__ __forceinline__ float dot_row(const void* base, int64_t off, const float* x, int n);
+template <>
+__device__ __forceinline__ float dot_row<uint16_t>(const void* base, int64_t off, const float* x, int n) {
+  const uint16_t* p = (const uint16_t*)base + off;
+  float acc = 0.f;
+  for (int t = 0; t < n; t += 8) {
+    const uint4 v = *(const uint4*)(p + t);
+    const uint32_t w[4] = {v.x, v.y, v.z, v.w};
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      acc = fmaf(__uint_as_float(w[e] << 16), x[t + 2 * e], acc);
+      acc = fmaf(__uint_as_float(w[e] & 0xFFFF0000u), x[t + 2 * e + 1], acc);
+    }
+  }
+  return acc;
+}
+template <>
+__device__ __forceinline__ float dot_row<float>(const void* base, int64_t off, const float* x, int n) {
+  const float* p = (const float*)base + off;
+  float acc = 0.f;
+  for (int t = 0; t < n; t += 4) {
+    const float4 v = *(const float4*)(p + t);
+    acc = fmaf(v.x, x[t], acc);
+    acc = fmaf(v.y, x[t + 1], acc);
+    acc = fmaf(v.z, x[t + 2], acc);
+    acc = fmaf(v.w, x[t + 3], acc);
+  }
+  return acc;
+}
+
+template <typename T>
+__global__ __launch_bounds__(256) void k_bwd_rows(BwdProblem bp, BwdBufs b) {
+  __shared__ float dout_s[4][1024];
+  __shared__ int32_t js[4][64];
+  __shared__ float dss[4][64];
+  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  const int64_t r = (int64_t)blockIdx.x * 4 + wave;
+  if (r >= bp.BH * bp.Lq) return;  // whole wave; the kernel syncs waves only
+  const int64_t bh = r / bp.Lq, d = bp.d, k = bp.k;
+  const int32_t* idx = bp.idx + r * k;
+  const float* dots = bp.dots + r * k;
+  float2* pair = b.pair + r * k;
+  const int64_t kv0 = bh * bp.kv_head_stride;
+  const bool softmax = bp.act == ACT_SOFTMAX;
+  auto valid_key = [&](int32_t j) { return j >= 0 && (int64_t)j < bp.Lk; };
+
+  for (int64_t t = lane; t < d; t += 64) dout_s[wave][t] = load_elem<T>(bp.dout, r * d + t);
+  wave_sync_lds();
+
+  // pass 1: the softmax's maximum and normaliser over the survivors' cached scores
+  float mx = -INFINITY, z = 0.f;
+  if (softmax) {
+    for (int64_t m = lane; m < k; m += 64)
+      if (valid_key(idx[m])) mx = fmaxf(mx, dots[m]);
+    mx = wave_max(mx);
+    for (int64_t m = lane; m < k; m += 64)
+      if (valid_key(idx[m])) z += __expf(bp.scale * (dots[m] - mx));
+    z = wave_sum(z);
+  }
+  const float inv_z = softmax ? 1.f / z : 0.f;
+
+  // pass 2: d_top_actv[m] = d_out . V[j_m]; LP lanes (a power of two) share one
+  // pair, F = d / LP features each
+  int LP = 1;
+  if (d % 64 == 0 && (((d / 64) & (d / 64 - 1)) == 0)) LP = (int)(d / 64);
+  const int F = (int)(d / LP), EPI = 64 / LP;
+  const int part = lane % LP;
+  float gpart = 0.f;
+  for (int64_t m0 = 0; m0 < k; m0 += EPI) {
+    const int64_t m = m0 + lane / LP;
+    const int32_t j = m < k ? idx[m] : -1;
+    const bool ok = valid_key(j);
+    float dw = ok ? dot_row<T>(bp.V, kv0 + (int64_t)j * d + part * F, &dout_s[wave][part * F], F) : 0.f;
+    for (int off = 1; off < LP; off <<= 1) dw += __shfl_xor(dw, off, 64);
+    if (ok && part == 0) {
+      const float s = dots[m];
+      const float w = softmax ? __expf(bp.scale * (s - mx)) * inv_z : fmaxf(s, 0.f);
+      pair[m] = make_float2(w, dw);
+      gpart += w * dw;
+    }
+  }
+  const float g = wave_sum(gpart);
+  __threadfence_block();  // this wave's pair writes are visible to its own reads below
+
+  // pass 3: d_top_dots, the per-key counts, and d_Q = sum_m d_top_dots[m] K[j_m]
+  float dq[BWD_MAXF];
+#pragma unroll
+  for (int f = 0; f < BWD_MAXF; ++f) dq[f] = 0.f;
+  for (int64_t c0 = 0; c0 < k; c0 += 64) {
+    const int64_t m = c0 + lane;
+    const int32_t j = m < k ? idx[m] : -1;
+    const bool ok = valid_key(j);
+    float ds = 0.f;
+    if (ok) {
+      const float2 wdw = pair[m];
+      ds = softmax ? bp.scale * wdw.x * (wdw.y - g) : (dots[m] > 0.f ? wdw.y : 0.f);
+      pair[m] = make_float2(wdw.x, ds);
+      atomicAdd(&b.count[bh * bp.Lk + j], 1);
+    }
+    js[wave][lane] = ok ? j : -1;
+    dss[wave][lane] = ds;
+    wave_sync_lds();
+    const int n = (int)(k - c0 < 64 ? k - c0 : 64);
+    for (int e = 0; e < n; ++e) {
+      const int32_t je = js[wave][e];
+      if (je < 0) continue;
+      const float dse = dss[wave][e];
+      const int64_t kr = kv0 + (int64_t)je * d;
+#pragma unroll
+      for (int f = 0; f < BWD_MAXF; ++f) {
+        const int64_t t = lane + 64 * f;
+        if (t < d) dq[f] = fmaf(dse, load_elem<T>(bp.K, kr + t), dq[f]);
+      }
+    }
+    wave_sync_lds();
+  }
+#pragma unroll
+  for (int f = 0; f < BWD_MAXF; ++f) {
+    const int64_t t = lane + 64 * f;
+    if (t < d) store_elem<T>(bp.dQ, r * d + t, dq[f]);
+  }
+}
+
+// exclusive scan, in place: 1024 elements per block, block totals to sums
+__global__ __launch_bounds__(256) void k_bwd_scan_local(int32_t* a, int64_t n, int32_t* sums) {
+  __shared__ uint32_t tmp[4];
+  const int64_t base = (int64_t)blockIdx.x * 1024 + threadIdx.x * 4;
+  uint32_t v[4], s = 0;
+#pragma unroll
+  for (int e = 0; e < 4; ++e) {
+    v[e] = base + e < n ? (uint32_t)a[base + e] : 0u;
+    s += v[e];
+  }
+  const uint32_t ex = team_excl_scan<256>(s, tmp);
+  uint32_t run = ex;
+#pragma unroll
+  for (int e = 0; e < 4; ++e) {
+    if (base + e < n) a[base + e] = (int32_t)run;
+    run += v[e];
+  }
+  if (threadIdx.x == 255) sums[blockIdx.x] = (int32_t)run;
+}
+
+// exclusive scan of the nb block totals by one workgroup, 1024 at a time
+__global__ __launch_bounds__(256) void k_bwd_scan_sums(int32_t* sums, int64_t nb) {
+  __shared__ uint32_t tmp[4];
+  __shared__ uint32_t carry;
+  if (threadIdx.x == 0) carry = 0;
+  __syncthreads();
+  for (int64_t c0 = 0; c0 < nb; c0 += 1024) {
+    const int64_t base = c0 + threadIdx.x * 4;
+    uint32_t v[4], s = 0;
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      v[e] = base + e < nb ? (uint32_t)sums[base + e] : 0u;
+      s += v[e];
+    }
+    const uint32_t ex = team_excl_scan<256>(s, tmp);
+    const uint32_t c = carry;
+    uint32_t run = c + ex;
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      if (base + e < nb) sums[base + e] = (int32_t)run;
+      run += v[e];
+    }
+    __syncthreads();
+    if (threadIdx.x == 255) carry = run;
+    __syncthreads();
+  }
+}
+
+__global__ __launch_bounds__(256) void k_bwd_scan_add(int32_t* a, int64_t n, const int32_t* sums) {
+  const int64_t base = (int64_t)blockIdx.x * 1024 + threadIdx.x * 4;
+  const int32_t add = sums[blockIdx.x];
+#pragma unroll
+  for (int e = 0; e < 4; ++e)
+    if (base + e < n) a[base + e] += add;
+}
+
+__global__ __launch_bounds__(256) void k_bwd_fill(BwdProblem bp, BwdBufs b) {
+  const int64_t npairs = bp.BH * bp.Lq * bp.k;
+  for (int64_t p = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; p < npairs; p += (int64_t)gridDim.x * blockDim.x) {
+    const int32_t j = bp.idx[p];
+    if (j < 0 || (int64_t)j >= bp.Lk) continue;
+    const int64_t key = (p / bp.k / bp.Lq) * bp.Lk + j;
+    const int32_t pos = b.count[key] + atomicAdd(&b.fill[key], 1);
+    b.list[pos] = (int32_t)p;
+  }
+}
+
+template <typename T>
+__global__ __launch_bounds__(256) void k_bwd_keys(BwdProblem bp, BwdBufs b) {
+  __shared__ int32_t lst[4][1024];
+  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  const int64_t key = (int64_t)blockIdx.x * 4 + wave;
+  if (key >= bp.BH * bp.Lk) return;  // whole wave
+  const int64_t bh = key / bp.Lk, j = key - bh * bp.Lk, d = bp.d;
+  const int32_t beg = b.count[key], n = b.count[key + 1] - beg;
+  float dv[BWD_MAXF], dk[BWD_MAXF];
+#pragma unroll
+  for (int f = 0; f < BWD_MAXF; ++f) dv[f] = dk[f] = 0.f;
+  auto accumulate = [&](int32_t p) {
+    p = __builtin_amdgcn_readfirstlane(p);
+    const float2 c = b.pair[p];
+    const int64_t row = (int64_t)p / bp.k;
+#pragma unroll
+    for (int f = 0; f < BWD_MAXF; ++f) {
+      const int64_t t = lane + 64 * f;
+      if (t < d) {
+        dv[f] = fmaf(c.x, load_elem<T>(bp.dout, row * d + t), dv[f]);
+        dk[f] = fmaf(c.y, load_elem<T>(bp.Q, row * d + t), dk[f]);
+      }
+    }
+  };
+  // increasing pair order: a fixed summation order whatever order the fill took
+  auto sorted = [&](auto tag) {
+    constexpr int E = decltype(tag)::value;
+    uint64_t r[E];
+#pragma unroll
+    for (int e = 0; e < E; ++e) {
+      const int i = e * 64 + lane;
+      r[e] = i < n ? (uint64_t)(0xFFFFFFFFu - (uint32_t)b.list[beg + i]) : 0ull;
+    }
+    wave_sort_desc<E>(r);  // descending in 0xFFFFFFFF - p: ascending p
+#pragma unroll
+    for (int e = 0; e < E; ++e) lst[wave][e * 64 + lane] = (int32_t)(0xFFFFFFFFu - (uint32_t)r[e]);
+    wave_sync_lds();
+    for (int e = 0; e < n; ++e) accumulate(lst[wave][e]);
+  };
+  if (n <= 64) sorted(std::integral_constant<int, 1>{});
+  else if (n <= 128) sorted(std::integral_constant<int, 2>{});
+  else if (n <= 256) sorted(std::integral_constant<int, 4>{});
+  else if (n <= 512) sorted(std::integral_constant<int, 8>{});
+  else if (n <= 1024) sorted(std::integral_constant<int, 16>{});
+  else
+    for (int e = 0; e < n; ++e) accumulate(b.list[beg + e]);
+  const int64_t o = bh * bp.kv_head_stride + j * d;
+#pragma unroll
+  for (int f = 0; f < BWD_MAXF; ++f) {
+    const int64_t t = lane + 64 * f;
+    if (t < d) {
+      store_elem<T>(bp.dV, o + t, dv[f]);
+      store_elem<T>(bp.dK, o + t, dk[f]);
+    }
+  }
+}
+
+hipError_t launch_backward(const BwdProblem& bp, const BwdBufs& b, hipStream_t st) {
+  const int64_t nkeys = bp.BH * bp.Lk, rows = bp.BH * bp.Lq, npairs = rows * bp.k;
+  const int64_t nb = (nkeys + 1 + 1023) / 1024;
+  k_bwd_zero<<<1024, 256, 0, st>>>(b.count, nkeys + 1);
+  k_bwd_zero<<<1024, 256, 0, st>>>(b.fill, nkeys);
+  const unsigned grid_rows = (unsigned)((rows + 3) / 4), grid_keys = (unsigned)((nkeys + 3) / 4);
+  if (bp.dtype == T_BF16) k_bwd_rows<uint16_t><<<grid_rows, 256, 0, st>>>(bp, b);
+  else k_bwd_rows<float><<<grid_rows, 256, 0, st>>>(bp, b);
+  k_bwd_scan_local<<<(unsigned)nb, 256, 0, st>>>(b.count, nkeys + 1, b.block_sums);
+  k_bwd_scan_sums<<<1, 256, 0, st>>>(b.block_sums, nb);
+  k_bwd_scan_add<<<(unsigned)nb, 256, 0, st>>>(b.count, nkeys + 1, b.block_sums);
+  const int64_t gf = (npairs + 255) / 256;
+  k_bwd_fill<<<(unsigned)(gf < 65536 ? gf : 65536), 256, 0, st>>>(bp, b);
+  if (bp.dtype == T_BF16) k_bwd_keys<uint16_t><<<grid_keys, 256, 0, st>>>(bp, b);
+  else k_bwd_keys<float><<<grid_keys, 256, 0, st>>>(bp, b);
   return hipGetLastError();
 }
 

@@ -1,0 +1,119 @@
+"""GPU parity of the backward pass (input checkpointing) against the fp64 oracle.
+
+The forward runs on the GPU in debug mode to produce its cache (selected keys and
+their raw scores); the backward then runs through the C ABI, and the oracle computes
+the gradients for the same selected keys in fp64 (its scores recomputed exactly).
+Outputs are compared per row (per key for d_K, d_V) in the max norm, relative to
+the largest reference entry of the tensor: 2e-2 for bf16, 1e-5 for fp32.
+"""
+import math
+
+import numpy as np
+import pytest
+import torch
+
+import paper_2106_06899_amd as tk
+from oracle import topk_backward as bo
+from paper_2106_06899_amd import workloads as wl
+from tests import parity
+
+pytestmark = pytest.mark.gpu
+
+RTOL = {wl.F32: 1e-5, wl.BF16: 2e-2}
+
+
+def _say(*a):
+    print("[case]", *a, flush=True)
+
+
+@pytest.fixture(autouse=True, scope="module")
+def _gpu():
+    assert torch.cuda.is_available(), "GPU tests need a GPU"
+    tk.lib()
+    yield
+
+
+def _grad_out(shape, dtype, seed):
+    rng = np.random.Generator(np.random.PCG64(seed))
+    g = rng.standard_normal(shape).astype(np.float32)
+    if dtype == wl.BF16:
+        bits = wl.f32_to_bf16_bits(g)
+        return wl.Tensor(wl.bf16_bits_to_f32(bits), bits, wl.BF16)
+    return wl.Tensor(g, None, wl.F32)
+
+
+def _check(name, got, ref, dtype):
+    g = got.float().cpu().numpy().astype(np.float64).reshape(-1, got.shape[-1])
+    r = ref.reshape(-1, ref.shape[-1])
+    scale = max(float(np.abs(r).max()), 1e-30)
+    err = np.abs(g - r).max(axis=1) / scale
+    rtol = RTOL[dtype]
+    assert np.all(err <= rtol), f"{name}: error {err.max():.3e} > {rtol} at row {int(np.argmax(err))}"
+    return float(err.max())
+
+
+ATTN_CASES = {
+    "c1_fp32": ("c1", dict(Lq=300, Lk=500, chunk=100)),
+    "c2_bf16_fused": ("c2", dict(B=1, H=2, Lq=200, Lk=512, chunk=128)),
+    "c3_bf16_fused_sample": ("c3", dict(H=2, Lq=300, Lk=6000, chunk=256)),
+    "c4_bf16_causal": ("c4", dict(B=1, H=2, Lq=400, Lk=400, chunk=128)),
+    "bf16_d96_k200": ("c2", dict(B=1, H=1, Lq=150, Lk=700, d=96, k=200, chunk=64)),
+    "fp32_causal_k1": ("c1", dict(Lq=120, Lk=120, causal=True, k=1, chunk=50)),
+}
+
+
+@pytest.mark.parametrize("name", sorted(ATTN_CASES))
+def test_attn_backward_parity(name):
+    base, kw = ATTN_CASES[name]
+    w = wl.WORKLOADS[base].scaled(**kw)
+    _say(name, w)
+    x = wl.make_inputs(w)
+    q, k, v = (parity.to_dev(x[n]) for n in ("Q", "K", "V"))
+    _, idx, dots = tk.attn(q, k, v, w.k, w.chunk, w.causal, w.scale, debug=True)
+    g = _grad_out((w.B, w.H, w.Lq, w.d), w.dtype, 77)
+    dq, dk, dv = tk.attn_backward(q, k, v, idx, dots, parity.to_dev(g), w.scale)
+    torch.cuda.synchronize()
+    rq, rk, rv = bo.oracle_attn_backward(x["Q"].values, x["K"].values, x["V"].values, idx.cpu().numpy(),
+                                         g.values, w.scale, chunk=w.chunk)
+    errs = [_check(n, a, b, w.dtype) for n, a, b in (("d_Q", dq, rq), ("d_K", dk, rk), ("d_V", dv, rv))]
+    _say(name, "ok", dict(zip(("dQ", "dK", "dV"), errs)))
+    if w.k == 1:  # a lone survivor's softmax weight is 1 whatever its score: no score gradient
+        assert torch.count_nonzero(dq) == 0 and torch.count_nonzero(dk) == 0
+
+
+FFN_CASES = {
+    "c5_bf16": dict(N=200, d_model=256, d_ff=3000, k=256, chunk=64),
+    "c5_bf16_d1024": dict(N=64, d_model=1024, d_ff=2048, k=100, chunk=64),
+    "fp32_small_k": dict(N=90, d_model=64, d_ff=800, k=9, chunk=40, dtype=wl.F32),
+}
+
+
+@pytest.mark.parametrize("name", sorted(FFN_CASES))
+def test_ffn_backward_parity(name):
+    w = wl.WORKLOADS["c5"].scaled(**FFN_CASES[name])
+    _say(name, w)
+    x = wl.make_inputs(w)
+    a, b1, b2 = (parity.to_dev(x[n]) for n in ("X", "W1", "W2"))
+    _, idx, dots = tk.ffn(a, b1, b2, w.k, w.chunk, debug=True)
+    g = _grad_out((w.N, w.d_model), w.dtype, 78)
+    dx, dw1, dw2 = tk.ffn_backward(a, b1, b2, idx, dots, parity.to_dev(g))
+    torch.cuda.synchronize()
+    rx, r1, r2 = bo.oracle_ffn_backward(x["X"].values, x["W1"].values, x["W2"].values, idx.cpu().numpy(), g.values,
+                                        chunk=w.chunk)
+    errs = [_check(n, a_, b_, w.dtype) for n, a_, b_ in (("d_X", dx, rx), ("d_W1", dw1, r1), ("d_W2", dw2, r2))]
+    _say(name, "ok", dict(zip(("dX", "dW1", "dW2"), errs)))
+
+
+def test_backward_is_deterministic():
+    """Two backward calls on the same inputs give bit-identical gradients (no
+    floating-point atomics; per-key sums in a fixed order)."""
+    w = wl.WORKLOADS["c3"].scaled(H=1, Lq=512, Lk=4096, chunk=256)
+    x = wl.make_inputs(w)
+    q, k, v = (parity.to_dev(x[n]) for n in ("Q", "K", "V"))
+    _, idx, dots = tk.attn(q, k, v, w.k, w.chunk, w.causal, w.scale, debug=True)
+    g = parity.to_dev(_grad_out((w.B, w.H, w.Lq, w.d), w.dtype, 79))
+    first = tk.attn_backward(q, k, v, idx, dots, g, w.scale)
+    second = tk.attn_backward(q, k, v, idx, dots, g, w.scale)
+    torch.cuda.synchronize()
+    for a, b in zip(first, second):
+        assert torch.equal(a, b)
