@@ -112,6 +112,57 @@ def cpu_baseline(w, x, budget_s: float):
                       f"workload (fp64 NumPy, {el:.1f} s)"}
 
 
+def bench_backward(args, w, x, dev_tensor):
+    """Time the backward pass of one workload: the forward runs once in debug mode to
+    produce its cache (selected keys, their raw scores); each timed step is one
+    backward call. Roofline: the gathered rows (4 rows of d elements per selected
+    (query, key) pair: V and K per query, d_out and Q per key) plus the cache read
+    and the three gradients written, against the HBM peak."""
+    import torch
+    import paper_2106_06899_amd as tk
+    from paper_2106_06899_amd import workloads as wl
+    elem = 2 if w.dtype == wl.BF16 else 4
+    if w.kind == "attn":
+        q, k, v = (dev_tensor(x[n]) for n in ("Q", "K", "V"))
+        _, idx, dots = tk.attn(q, k, v, w.k, w.chunk, w.causal, w.scale, debug=True)
+        g = torch.randn(q.shape, generator=torch.Generator().manual_seed(5), dtype=torch.float32).to(q.dtype).to(q.device)
+        step = lambda: tk.attn_backward(q, k, v, idx, dots, g, w.scale)  # noqa: E731
+        rows, keys, d = w.B * w.H * w.Lq, w.B * w.H * w.Lk, w.d
+    else:
+        a, b1, b2 = (dev_tensor(x[n]) for n in ("X", "W1", "W2"))
+        _, idx, dots = tk.ffn(a, b1, b2, w.k, w.chunk, debug=True)
+        g = torch.randn(a.shape, generator=torch.Generator().manual_seed(5), dtype=torch.float32).to(a.dtype).to(a.device)
+        step = lambda: tk.ffn_backward(a, b1, b2, idx, dots, g)  # noqa: E731
+        rows, keys, d = w.N, w.d_ff, w.d_model
+    pairs = int((idx >= 0).sum().item())
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    tk.profile_begin()
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(args.steps):
+        step()
+    torch.cuda.synchronize()
+    elapsed = time.perf_counter() - t0
+    stages = tk.profile_end()
+    ms_step = 1e3 * elapsed / args.steps
+    bwd_ms = stages["backward"][0] / max(stages["backward"][1], 1)
+    algo_bytes = pairs * (4 * d * elem + 8) + (rows + 2 * keys) * d * elem
+    achieved = algo_bytes / (bwd_ms / 1e3) / 1e9
+    rec = {
+        "metric": "top-k attention backward (input checkpointing) queries/s",
+        "value": rows / (ms_step / 1e3), "unit": "queries/s", "n_gpus": 1, "steps": args.steps,
+        "warmup": args.warmup, "ms_per_step": ms_step, "higher_is_better": True, "scaling": "weak",
+        "vs_baseline": None, "dtype": "bf16" if w.dtype == wl.BF16 else "f32", "data": "synthetic",
+        "config": {"workload": f"{w.name}: {w.note}", "selected_pairs": pairs},
+        "roofline": {"kernel": "backward call (rows, scan, fill, keys)", "bound": "hbm", "achieved": achieved,
+                     "peak": PEAK_HBM_GBS, "unit": "GB/s", "frac": achieved / PEAK_HBM_GBS, "traffic": None,
+                     "algorithmic_bytes_per_launch": algo_bytes, "avg_launch_ms": bwd_ms},
+    }
+    print(json.dumps(rec), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -126,6 +177,8 @@ def main():
                     help="write the scan's HBM bytes per launch from four rocprofv3 counter_collection.csv files")
     ap.add_argument("--copy-bytes", type=int, default=1 << 30)
     ap.add_argument("--traffic-command", default="")
+    ap.add_argument("--backward", action="store_true",
+                    help="time the backward pass (input checkpointing) instead of the forward")
     args = ap.parse_args()
     if args.write_traffic:
         print(json.dumps(write_traffic(*args.write_traffic, args.copy_bytes, args.traffic_command)))
@@ -169,6 +222,9 @@ def main():
         flops = 2.0 * w.d_model * w.N * w.d_ff
         path = tk.ffn_path(w.N, w.d_model, w.d_ff, w.k, w.chunk)
     queries = w.queries
+    if args.backward:
+        bench_backward(args, w, x, dev_tensor)
+        return
 
     for _ in range(args.warmup):
         step()
