@@ -1582,7 +1582,6 @@ hipError_t launch_mfma_probe(int32_t* rows, int32_t* cols, hipStream_t st) {
 //     d_K[j] = sum score gradient * Q[row] over the key's list, in increasing pair
 //     order (lists of up to 1024 pairs are sorted first). No floating-point
 //     atomics: the sums do not depend on scheduling.
-constexpr int BWD_MAXF = 16;  // features per lane (d <= 1024)
 
 __global__ void k_bwd_zero(int32_t* p, int64_t n) {
   for (int64_t e = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; e < n; e += (int64_t)gridDim.x * blockDim.x)
@@ -1606,45 +1605,80 @@ __device__ __forceinline__ float wave_max(float x) {
   return x;
 }
 
-// sum_t x[t] * row[off + t] over n features (n % 8 == 0, off % 8 == 0)
-template <typename T>
-__device__ __forceinline__ float dot_row(const void* base, int64_t off, const float* x, int n);
-template <>
-__device__ __forceinline__ float dot_row<uint16_t>(const void* base, int64_t off, const float* x, int n) {
-  const uint16_t* p = (const uint16_t*)base + off;
-  float acc = 0.f;
-  for (int t = 0; t < n; t += 8) {
-    const uint4 v = *(const uint4*)(p + t);
-    const uint32_t w[4] = {v.x, v.y, v.z, v.w};
-#pragma unroll
-    for (int e = 0; e < 4; ++e) {
-      acc = fmaf(__uint_as_float(w[e] << 16), x[t + 2 * e], acc);
-      acc = fmaf(__uint_as_float(w[e] & 0xFFFF0000u), x[t + 2 * e + 1], acc);
-    }
-  }
-  return acc;
+// Rows are read in 16-byte chunks of EPC elements (8 bf16 or 4 fp32). G lanes (the
+// smallest power of two >= the row's chunk count, at most 64) share one row, lane
+// part = lane % G taking chunks part, part + G, ...; one wave step covers S = 64 / G
+// rows. A lane holds at most NCL chunks, 16 floats in all (d <= 1024).
+template <typename T> struct RowChunks {
+  static constexpr int EPC = 16 / (int)sizeof(T);
+  static constexpr int NCL = 16 / EPC;
+};
+
+struct LaneMap {
+  int CH, G, S, slot, part;
+};
+__device__ __forceinline__ LaneMap lane_map(int64_t d, int bytes, int lane) {
+  LaneMap m;
+  m.CH = (int)(d * bytes / 16);
+  m.G = 1;
+  while (m.G < m.CH && m.G < 64) m.G <<= 1;
+  m.S = 64 / m.G;
+  m.slot = lane / m.G;
+  m.part = lane & (m.G - 1);
+  return m;
 }
-template <>
-__device__ __forceinline__ float dot_row<float>(const void* base, int64_t off, const float* x, int n) {
-  const float* p = (const float*)base + off;
-  float acc = 0.f;
-  for (int t = 0; t < n; t += 4) {
-    const float4 v = *(const float4*)(p + t);
-    acc = fmaf(v.x, x[t], acc);
-    acc = fmaf(v.y, x[t + 1], acc);
-    acc = fmaf(v.z, x[t + 2], acc);
-    acc = fmaf(v.w, x[t + 3], acc);
+
+template <typename T> __device__ __forceinline__ void load_chunk(const void* base, int64_t e, float (&x)[RowChunks<T>::EPC]);
+template <> __device__ __forceinline__ void load_chunk<uint16_t>(const void* base, int64_t e, float (&x)[8]) {
+  const uint4 v = *(const uint4*)((const uint16_t*)base + e);
+  const uint32_t w[4] = {v.x, v.y, v.z, v.w};
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    x[2 * i] = __uint_as_float(w[i] << 16);
+    x[2 * i + 1] = __uint_as_float(w[i] & 0xFFFF0000u);
   }
-  return acc;
+}
+template <> __device__ __forceinline__ void load_chunk<float>(const void* base, int64_t e, float (&x)[4]) {
+  const float4 v = *(const float4*)((const float*)base + e);
+  x[0] = v.x, x[1] = v.y, x[2] = v.z, x[3] = v.w;
+}
+template <typename T> __device__ __forceinline__ void store_chunk(void* base, int64_t e, const float (&x)[RowChunks<T>::EPC]);
+template <> __device__ __forceinline__ void store_chunk<uint16_t>(void* base, int64_t e, const float (&x)[8]) {
+  uint32_t w[4];
+#pragma unroll
+  for (int i = 0; i < 4; ++i) w[i] = (uint32_t)f32_to_bf16(x[2 * i]) | ((uint32_t)f32_to_bf16(x[2 * i + 1]) << 16);
+  *(uint4*)((uint16_t*)base + e) = make_uint4(w[0], w[1], w[2], w[3]);
+}
+template <> __device__ __forceinline__ void store_chunk<float>(void* base, int64_t e, const float (&x)[4]) {
+  *(float4*)((float*)base + e) = make_float4(x[0], x[1], x[2], x[3]);
+}
+
+// sum the S row slots' partial rows: afterwards every lane holds the total of its part
+template <int NCL, int EPC>
+__device__ __forceinline__ void slot_reduce(float (&acc)[NCL][EPC], const LaneMap& lm) {
+  for (int off = lm.G; off < 64; off <<= 1) {
+#pragma unroll
+    for (int u = 0; u < NCL; ++u)
+#pragma unroll
+      for (int e = 0; e < EPC; ++e) acc[u][e] += __shfl_xor(acc[u][e], off, 64);
+  }
+}
+
+// XCD-aware renumbering: the hardware deals workgroups round-robin over the 8 XCDs;
+// with a grid that is a multiple of 8, each XCD runs a contiguous range of logical
+// workgroups (neighbouring rows or keys of one head share that XCD's L2).
+__device__ __forceinline__ int64_t xcd_workgroup() {
+  const int64_t NG = gridDim.x, bid = blockIdx.x;
+  return (NG % 8 == 0) ? (bid % 8) * (NG / 8) + bid / 8 : bid;
 }
 
 template <typename T>
 __global__ __launch_bounds__(256) void k_bwd_rows(BwdProblem bp, BwdBufs b) {
-  __shared__ float dout_s[4][1024];
+  constexpr int EPC = RowChunks<T>::EPC, NCL = RowChunks<T>::NCL;
   __shared__ int32_t js[4][64];
   __shared__ float dss[4][64];
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
-  const int64_t r = (int64_t)blockIdx.x * 4 + wave;
+  const int64_t r = xcd_workgroup() * 4 + wave;
   if (r >= bp.BH * bp.Lq) return;  // whole wave; the kernel syncs waves only
   const int64_t bh = r / bp.Lq, d = bp.d, k = bp.k;
   const int32_t* idx = bp.idx + r * k;
@@ -1653,9 +1687,18 @@ __global__ __launch_bounds__(256) void k_bwd_rows(BwdProblem bp, BwdBufs b) {
   const int64_t kv0 = bh * bp.kv_head_stride;
   const bool softmax = bp.act == ACT_SOFTMAX;
   auto valid_key = [&](int32_t j) { return j >= 0 && (int64_t)j < bp.Lk; };
+  const LaneMap lm = lane_map(d, (int)sizeof(T), lane);
 
-  for (int64_t t = lane; t < d; t += 64) dout_s[wave][t] = load_elem<T>(bp.dout, r * d + t);
-  wave_sync_lds();
+  // this lane's chunks of d_out[r]
+  float gout[NCL][EPC];
+#pragma unroll
+  for (int u = 0; u < NCL; ++u) {
+    const int c = lm.part + lm.G * u;
+    if (c < lm.CH) load_chunk<T>(bp.dout, r * d + (int64_t)c * EPC, gout[u]);
+    else
+#pragma unroll
+      for (int e = 0; e < EPC; ++e) gout[u][e] = 0.f;
+  }
 
   // pass 1: the softmax's maximum and normaliser over the survivors' cached scores
   float mx = -INFINITY, z = 0.f;
@@ -1669,20 +1712,28 @@ __global__ __launch_bounds__(256) void k_bwd_rows(BwdProblem bp, BwdBufs b) {
   }
   const float inv_z = softmax ? 1.f / z : 0.f;
 
-  // pass 2: d_top_actv[m] = d_out . V[j_m]; LP lanes (a power of two) share one
-  // pair, F = d / LP features each
-  int LP = 1;
-  if (d % 64 == 0 && (((d / 64) & (d / 64 - 1)) == 0)) LP = (int)(d / 64);
-  const int F = (int)(d / LP), EPI = 64 / LP;
-  const int part = lane % LP;
+  // pass 2: d_top_actv[m] = d_out . V[j_m], one selected pair per row slot
   float gpart = 0.f;
-  for (int64_t m0 = 0; m0 < k; m0 += EPI) {
-    const int64_t m = m0 + lane / LP;
+  for (int64_t m0 = 0; m0 < k; m0 += lm.S) {
+    const int64_t m = m0 + lm.slot;
     const int32_t j = m < k ? idx[m] : -1;
     const bool ok = valid_key(j);
-    float dw = ok ? dot_row<T>(bp.V, kv0 + (int64_t)j * d + part * F, &dout_s[wave][part * F], F) : 0.f;
-    for (int off = 1; off < LP; off <<= 1) dw += __shfl_xor(dw, off, 64);
-    if (ok && part == 0) {
+    float dw = 0.f;
+    if (ok) {
+      const int64_t row = kv0 + (int64_t)j * d;
+#pragma unroll
+      for (int u = 0; u < NCL; ++u) {
+        const int c = lm.part + lm.G * u;
+        if (c < lm.CH) {
+          float x[EPC];
+          load_chunk<T>(bp.V, row + (int64_t)c * EPC, x);
+#pragma unroll
+          for (int e = 0; e < EPC; ++e) dw = fmaf(x[e], gout[u][e], dw);
+        }
+      }
+    }
+    for (int off = 1; off < lm.G; off <<= 1) dw += __shfl_xor(dw, off, 64);
+    if (ok && lm.part == 0) {
       const float s = dots[m];
       const float w = softmax ? __expf(bp.scale * (s - mx)) * inv_z : fmaxf(s, 0.f);
       pair[m] = make_float2(w, dw);
@@ -1692,10 +1743,13 @@ __global__ __launch_bounds__(256) void k_bwd_rows(BwdProblem bp, BwdBufs b) {
   const float g = wave_sum(gpart);
   __threadfence_block();  // this wave's pair writes are visible to its own reads below
 
-  // pass 3: d_top_dots, the per-key counts, and d_Q = sum_m d_top_dots[m] K[j_m]
-  float dq[BWD_MAXF];
+  // pass 3: d_top_dots and the per-key counts (one pair per lane), then
+  // d_Q = sum_m d_top_dots[m] K[j_m] (one pair per row slot)
+  float acc[NCL][EPC];
 #pragma unroll
-  for (int f = 0; f < BWD_MAXF; ++f) dq[f] = 0.f;
+  for (int u = 0; u < NCL; ++u)
+#pragma unroll
+    for (int e = 0; e < EPC; ++e) acc[u][e] = 0.f;
   for (int64_t c0 = 0; c0 < k; c0 += 64) {
     const int64_t m = c0 + lane;
     const int32_t j = m < k ? idx[m] : -1;
@@ -1707,27 +1761,37 @@ __global__ __launch_bounds__(256) void k_bwd_rows(BwdProblem bp, BwdBufs b) {
       pair[m] = make_float2(wdw.x, ds);
       atomicAdd(&b.count[bh * bp.Lk + j], 1);
     }
-    js[wave][lane] = ok ? j : -1;
+    js[wave][lane] = ok && ds != 0.f ? j : -1;  // a zero score gradient adds nothing
     dss[wave][lane] = ds;
     wave_sync_lds();
     const int n = (int)(k - c0 < 64 ? k - c0 : 64);
-    for (int e = 0; e < n; ++e) {
-      const int32_t je = js[wave][e];
-      if (je < 0) continue;
-      const float dse = dss[wave][e];
-      const int64_t kr = kv0 + (int64_t)je * d;
+    for (int e0 = 0; e0 < n; e0 += lm.S) {
+      const int e = e0 + lm.slot;
+      const int32_t je = e < n ? js[wave][e] : -1;
+      if (je >= 0) {
+        const float dse = dss[wave][e];
+        const int64_t row = kv0 + (int64_t)je * d;
 #pragma unroll
-      for (int f = 0; f < BWD_MAXF; ++f) {
-        const int64_t t = lane + 64 * f;
-        if (t < d) dq[f] = fmaf(dse, load_elem<T>(bp.K, kr + t), dq[f]);
+        for (int u = 0; u < NCL; ++u) {
+          const int c = lm.part + lm.G * u;
+          if (c < lm.CH) {
+            float x[EPC];
+            load_chunk<T>(bp.K, row + (int64_t)c * EPC, x);
+#pragma unroll
+            for (int e2 = 0; e2 < EPC; ++e2) acc[u][e2] = fmaf(dse, x[e2], acc[u][e2]);
+          }
+        }
       }
     }
     wave_sync_lds();
   }
+  slot_reduce(acc, lm);
+  if (lm.slot == 0) {
 #pragma unroll
-  for (int f = 0; f < BWD_MAXF; ++f) {
-    const int64_t t = lane + 64 * f;
-    if (t < d) store_elem<T>(bp.dQ, r * d + t, dq[f]);
+    for (int u = 0; u < NCL; ++u) {
+      const int c = lm.part + lm.G * u;
+      if (c < lm.CH) store_chunk<T>(bp.dQ, r * d + (int64_t)c * EPC, acc[u]);
+    }
   }
 }
 
@@ -1800,25 +1864,42 @@ __global__ __launch_bounds__(256) void k_bwd_fill(BwdProblem bp, BwdBufs b) {
 
 template <typename T>
 __global__ __launch_bounds__(256) void k_bwd_keys(BwdProblem bp, BwdBufs b) {
+  constexpr int EPC = RowChunks<T>::EPC, NCL = RowChunks<T>::NCL;
   __shared__ int32_t lst[4][1024];
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
-  const int64_t key = (int64_t)blockIdx.x * 4 + wave;
+  const int64_t key = xcd_workgroup() * 4 + wave;
   if (key >= bp.BH * bp.Lk) return;  // whole wave
   const int64_t bh = key / bp.Lk, j = key - bh * bp.Lk, d = bp.d;
+  const uint32_t kk = (uint32_t)bp.k;
   const int32_t beg = b.count[key], n = b.count[key + 1] - beg;
-  float dv[BWD_MAXF], dk[BWD_MAXF];
+  const LaneMap lm = lane_map(d, (int)sizeof(T), lane);
+  float dv[NCL][EPC], dk[NCL][EPC];
 #pragma unroll
-  for (int f = 0; f < BWD_MAXF; ++f) dv[f] = dk[f] = 0.f;
-  auto accumulate = [&](int32_t p) {
-    p = __builtin_amdgcn_readfirstlane(p);
-    const float2 c = b.pair[p];
-    const int64_t row = (int64_t)p / bp.k;
+  for (int u = 0; u < NCL; ++u)
 #pragma unroll
-    for (int f = 0; f < BWD_MAXF; ++f) {
-      const int64_t t = lane + 64 * f;
-      if (t < d) {
-        dv[f] = fmaf(c.x, load_elem<T>(bp.dout, row * d + t), dv[f]);
-        dk[f] = fmaf(c.y, load_elem<T>(bp.Q, row * d + t), dk[f]);
+    for (int e = 0; e < EPC; ++e) dv[u][e] = dk[u][e] = 0.f;
+  // one listed pair per row slot: slot s sums entries s, s + S, ... of the list
+  auto accumulate = [&](auto get) {
+    for (int e0 = 0; e0 < n; e0 += lm.S) {
+      const int e = e0 + lm.slot;
+      if (e < n) {
+        const int32_t p = get(e);
+        const float2 c = b.pair[p];
+        const int64_t row = (int64_t)((uint32_t)p / kk) * d;
+#pragma unroll
+        for (int u = 0; u < NCL; ++u) {
+          const int ch = lm.part + lm.G * u;
+          if (ch < lm.CH) {
+            float x[EPC], y[EPC];
+            load_chunk<T>(bp.dout, row + (int64_t)ch * EPC, x);
+            load_chunk<T>(bp.Q, row + (int64_t)ch * EPC, y);
+#pragma unroll
+            for (int e2 = 0; e2 < EPC; ++e2) {
+              dv[u][e2] = fmaf(c.x, x[e2], dv[u][e2]);
+              dk[u][e2] = fmaf(c.y, y[e2], dk[u][e2]);
+            }
+          }
+        }
       }
     }
   };
@@ -1835,22 +1916,25 @@ __global__ __launch_bounds__(256) void k_bwd_keys(BwdProblem bp, BwdBufs b) {
 #pragma unroll
     for (int e = 0; e < E; ++e) lst[wave][e * 64 + lane] = (int32_t)(0xFFFFFFFFu - (uint32_t)r[e]);
     wave_sync_lds();
-    for (int e = 0; e < n; ++e) accumulate(lst[wave][e]);
+    accumulate([&](int e) { return lst[wave][e]; });
   };
   if (n <= 64) sorted(std::integral_constant<int, 1>{});
   else if (n <= 128) sorted(std::integral_constant<int, 2>{});
   else if (n <= 256) sorted(std::integral_constant<int, 4>{});
   else if (n <= 512) sorted(std::integral_constant<int, 8>{});
   else if (n <= 1024) sorted(std::integral_constant<int, 16>{});
-  else
-    for (int e = 0; e < n; ++e) accumulate(b.list[beg + e]);
-  const int64_t o = bh * bp.kv_head_stride + j * d;
+  else accumulate([&](int e) { return b.list[beg + e]; });
+  slot_reduce(dv, lm);
+  slot_reduce(dk, lm);
+  if (lm.slot == 0) {
+    const int64_t o = bh * bp.kv_head_stride + j * d;
 #pragma unroll
-  for (int f = 0; f < BWD_MAXF; ++f) {
-    const int64_t t = lane + 64 * f;
-    if (t < d) {
-      store_elem<T>(bp.dV, o + t, dv[f]);
-      store_elem<T>(bp.dK, o + t, dk[f]);
+    for (int u = 0; u < NCL; ++u) {
+      const int ch = lm.part + lm.G * u;
+      if (ch < lm.CH) {
+        store_chunk<T>(bp.dV, o + (int64_t)ch * EPC, dv[u]);
+        store_chunk<T>(bp.dK, o + (int64_t)ch * EPC, dk[u]);
+      }
     }
   }
 }
@@ -1860,7 +1944,9 @@ hipError_t launch_backward(const BwdProblem& bp, const BwdBufs& b, hipStream_t s
   const int64_t nb = (nkeys + 1 + 1023) / 1024;
   k_bwd_zero<<<1024, 256, 0, st>>>(b.count, nkeys + 1);
   k_bwd_zero<<<1024, 256, 0, st>>>(b.fill, nkeys);
-  const unsigned grid_rows = (unsigned)((rows + 3) / 4), grid_keys = (unsigned)((nkeys + 3) / 4);
+  // grids rounded up to a multiple of 8 for the XCD-aware renumbering
+  const unsigned grid_rows = (unsigned)(((rows + 3) / 4 + 7) / 8 * 8);
+  const unsigned grid_keys = (unsigned)(((nkeys + 3) / 4 + 7) / 8 * 8);
   if (bp.dtype == T_BF16) k_bwd_rows<uint16_t><<<grid_rows, 256, 0, st>>>(bp, b);
   else k_bwd_rows<float><<<grid_rows, 256, 0, st>>>(bp, b);
   k_bwd_scan_local<<<(unsigned)nb, 256, 0, st>>>(b.count, nkeys + 1, b.block_sums);
