@@ -332,8 +332,7 @@ size_t workspace_for(const Problem& pb) {
 // ---------------------------------------------------------------- backward
 size_t bwd_bytes(const BwdProblem& bp) {
   const int64_t nkeys = bp.BH * bp.Lk, npairs = bp.BH * bp.Lq * bp.k, nb = (nkeys + 1 + 1023) / 1024;
-  return up((size_t)npairs * 8) + up((size_t)(nkeys + 1) * 4) + up((size_t)nkeys * 4) + up((size_t)npairs * 4) +
-         up((size_t)nb * 4);
+  return up((size_t)npairs * 8) + up((size_t)(nkeys + 1) * 4) + 2 * up((size_t)npairs * 4) + up((size_t)nb * 4);
 }
 
 BwdBufs bwd_carve(const BwdProblem& bp, char* ws) {
@@ -344,8 +343,8 @@ BwdBufs bwd_carve(const BwdProblem& bp, char* ws) {
   off += up((size_t)npairs * 8);
   b.count = (int32_t*)(ws + off);
   off += up((size_t)(nkeys + 1) * 4);
-  b.fill = (int32_t*)(ws + off);
-  off += up((size_t)nkeys * 4);
+  b.rank = (int32_t*)(ws + off);
+  off += up((size_t)npairs * 4);
   b.list = (int32_t*)(ws + off);
   off += up((size_t)npairs * 4);
   b.block_sums = (int32_t*)(ws + off);

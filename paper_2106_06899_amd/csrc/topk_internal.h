@@ -94,7 +94,7 @@ struct BwdProblem {
 struct BwdBufs {
   float2* pair;         // [rows * k]: (activation weight, score gradient)
   int32_t* count;       // [BH * Lk + 1]: pairs per key, then exclusive offsets
-  int32_t* fill;        // [BH * Lk]: per-key fill cursors
+  int32_t* rank;        // [rows * k]: each pair's place among its key's pairs
   int32_t* list;        // [rows * k]: pair ids grouped by key
   int32_t* block_sums;  // [ceil((BH * Lk + 1) / 1024)] scan scratch
 };

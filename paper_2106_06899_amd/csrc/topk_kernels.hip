@@ -1575,9 +1575,9 @@ hipError_t launch_mfma_probe(int32_t* rows, int32_t* cols, hipStream_t st) {
 //     k selected keys; the activation (softmax with temperature, or ReLU)
 //     recomputed from the cached scores and backpropagated to d_top_dots;
 //     d_Q = sum_m d_top_dots[m] K[j_m]; each pair's (weight, score gradient) is
-//     kept and the pairs per key are counted;
+//     kept, and its key's counter gives the pair its place among the key's pairs;
 //  2. an exclusive scan of the per-key counts (k_bwd_scan_*);
-//  3. k_bwd_fill: each pair's id into its key's list;
+//  3. k_bwd_fill: each pair's id into its key's list at that place;
 //  4. k_bwd_keys (one wave per key): d_V[j] = sum weight * d_out[row] and
 //     d_K[j] = sum score gradient * Q[row] over the key's list, in increasing pair
 //     order (lists of up to 1024 pairs are sorted first). No floating-point
@@ -1759,7 +1759,7 @@ __global__ __launch_bounds__(256) void k_bwd_rows(BwdProblem bp, BwdBufs b) {
       const float2 wdw = pair[m];
       ds = softmax ? bp.scale * wdw.x * (wdw.y - g) : (dots[m] > 0.f ? wdw.y : 0.f);
       pair[m] = make_float2(wdw.x, ds);
-      atomicAdd(&b.count[bh * bp.Lk + j], 1);
+      b.rank[r * k + m] = atomicAdd(&b.count[bh * bp.Lk + j], 1);
     }
     js[wave][lane] = ok && ds != 0.f ? j : -1;  // a zero score gradient adds nothing
     dss[wave][lane] = ds;
@@ -1852,13 +1852,13 @@ __global__ __launch_bounds__(256) void k_bwd_scan_add(int32_t* a, int64_t n, con
 }
 
 __global__ __launch_bounds__(256) void k_bwd_fill(BwdProblem bp, BwdBufs b) {
-  const int64_t npairs = bp.BH * bp.Lq * bp.k;
-  for (int64_t p = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; p < npairs; p += (int64_t)gridDim.x * blockDim.x) {
+  // pair ids, rows * k and heads * keys are below 2^31 (checked by the host)
+  const uint32_t npairs = (uint32_t)(bp.BH * bp.Lq * bp.k), per_head = (uint32_t)(bp.Lq * bp.k);
+  for (uint32_t p = blockIdx.x * blockDim.x + threadIdx.x; p < npairs; p += gridDim.x * blockDim.x) {
     const int32_t j = bp.idx[p];
     if (j < 0 || (int64_t)j >= bp.Lk) continue;
-    const int64_t key = (p / bp.k / bp.Lq) * bp.Lk + j;
-    const int32_t pos = b.count[key] + atomicAdd(&b.fill[key], 1);
-    b.list[pos] = (int32_t)p;
+    const int64_t key = (int64_t)(p / per_head) * bp.Lk + j;
+    b.list[b.count[key] + b.rank[p]] = (int32_t)p;
   }
 }
 
@@ -1943,7 +1943,6 @@ hipError_t launch_backward(const BwdProblem& bp, const BwdBufs& b, hipStream_t s
   const int64_t nkeys = bp.BH * bp.Lk, rows = bp.BH * bp.Lq, npairs = rows * bp.k;
   const int64_t nb = (nkeys + 1 + 1023) / 1024;
   k_bwd_zero<<<1024, 256, 0, st>>>(b.count, nkeys + 1);
-  k_bwd_zero<<<1024, 256, 0, st>>>(b.fill, nkeys);
   // grids rounded up to a multiple of 8 for the XCD-aware renumbering
   const unsigned grid_rows = (unsigned)(((rows + 3) / 4 + 7) / 8 * 8);
   const unsigned grid_keys = (unsigned)(((nkeys + 3) / 4 + 7) / 8 * 8);
