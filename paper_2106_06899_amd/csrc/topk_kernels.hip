@@ -1606,12 +1606,11 @@ __device__ __forceinline__ float wave_max(float x) {
 }
 
 // Rows are read in 16-byte chunks of EPC elements (8 bf16 or 4 fp32). G lanes (the
-// smallest power of two >= the row's chunk count, at most 64) share one row, lane
+// smallest power of two >= the row's chunk count CH, at most 64) share one row, lane
 // part = lane % G taking chunks part, part + G, ...; one wave step covers S = 64 / G
-// rows. A lane holds at most NCL chunks, 16 floats in all (d <= 1024).
+// rows. A lane holds NCL = ceil(CH / G) chunks: 1, 2 or 4 (d <= 1024).
 template <typename T> struct RowChunks {
   static constexpr int EPC = 16 / (int)sizeof(T);
-  static constexpr int NCL = 16 / EPC;
 };
 
 struct LaneMap {
@@ -1627,10 +1626,19 @@ __device__ __forceinline__ LaneMap lane_map(int64_t d, int bytes, int lane) {
   m.part = lane & (m.G - 1);
   return m;
 }
+inline int lane_chunks(int64_t d, int bytes) {  // NCL for the host's kernel choice
+  const int64_t CH = d * bytes / 16;
+  int64_t G = 1;
+  while (G < CH && G < 64) G <<= 1;
+  return (int)((CH + G - 1) / G);
+}
 
-template <typename T> __device__ __forceinline__ void load_chunk(const void* base, int64_t e, float (&x)[RowChunks<T>::EPC]);
-template <> __device__ __forceinline__ void load_chunk<uint16_t>(const void* base, int64_t e, float (&x)[8]) {
-  const uint4 v = *(const uint4*)((const uint16_t*)base + e);
+// 16 raw bytes at element offset e of a row-major tensor of T
+template <typename T> __device__ __forceinline__ uint4 load16(const void* base, int64_t e) {
+  return *(const uint4*)((const T*)base + e);
+}
+template <typename T> __device__ __forceinline__ void unpack(const uint4& v, float (&x)[RowChunks<T>::EPC]);
+template <> __device__ __forceinline__ void unpack<uint16_t>(const uint4& v, float (&x)[8]) {
   const uint32_t w[4] = {v.x, v.y, v.z, v.w};
 #pragma unroll
   for (int i = 0; i < 4; ++i) {
@@ -1638,9 +1646,8 @@ template <> __device__ __forceinline__ void load_chunk<uint16_t>(const void* bas
     x[2 * i + 1] = __uint_as_float(w[i] & 0xFFFF0000u);
   }
 }
-template <> __device__ __forceinline__ void load_chunk<float>(const void* base, int64_t e, float (&x)[4]) {
-  const float4 v = *(const float4*)((const float*)base + e);
-  x[0] = v.x, x[1] = v.y, x[2] = v.z, x[3] = v.w;
+template <> __device__ __forceinline__ void unpack<float>(const uint4& v, float (&x)[4]) {
+  x[0] = __uint_as_float(v.x), x[1] = __uint_as_float(v.y), x[2] = __uint_as_float(v.z), x[3] = __uint_as_float(v.w);
 }
 template <typename T> __device__ __forceinline__ void store_chunk(void* base, int64_t e, const float (&x)[RowChunks<T>::EPC]);
 template <> __device__ __forceinline__ void store_chunk<uint16_t>(void* base, int64_t e, const float (&x)[8]) {
@@ -1672,11 +1679,11 @@ __device__ __forceinline__ int64_t xcd_workgroup() {
   return (NG % 8 == 0) ? (bid % 8) * (NG / 8) + bid / 8 : bid;
 }
 
-template <typename T>
+constexpr int BWD_UNROLL = 4;  // row steps whose gathers are in flight together
+
+template <typename T, int NCL>
 __global__ __launch_bounds__(256) void k_bwd_rows(BwdProblem bp, BwdBufs b) {
-  constexpr int EPC = RowChunks<T>::EPC, NCL = RowChunks<T>::NCL;
-  __shared__ int32_t js[4][64];
-  __shared__ float dss[4][64];
+  constexpr int EPC = RowChunks<T>::EPC, U = BWD_UNROLL;
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
   const int64_t r = xcd_workgroup() * 4 + wave;
   if (r >= bp.BH * bp.Lq) return;  // whole wave; the kernel syncs waves only
@@ -1694,7 +1701,7 @@ __global__ __launch_bounds__(256) void k_bwd_rows(BwdProblem bp, BwdBufs b) {
 #pragma unroll
   for (int u = 0; u < NCL; ++u) {
     const int c = lm.part + lm.G * u;
-    if (c < lm.CH) load_chunk<T>(bp.dout, r * d + (int64_t)c * EPC, gout[u]);
+    if (c < lm.CH) unpack<T>(load16<T>(bp.dout, r * d + (int64_t)c * EPC), gout[u]);
     else
 #pragma unroll
       for (int e = 0; e < EPC; ++e) gout[u][e] = 0.f;
@@ -1712,39 +1719,60 @@ __global__ __launch_bounds__(256) void k_bwd_rows(BwdProblem bp, BwdBufs b) {
   }
   const float inv_z = softmax ? 1.f / z : 0.f;
 
-  // pass 2: d_top_actv[m] = d_out . V[j_m], one selected pair per row slot
+  // pass 2: d_top_actv[m] = d_out . V[j_m]. 64 pairs at a time sit one per lane;
+  // shuffles deal them to the row slots, U steps of gathers in flight together
   float gpart = 0.f;
-  for (int64_t m0 = 0; m0 < k; m0 += lm.S) {
-    const int64_t m = m0 + lm.slot;
-    const int32_t j = m < k ? idx[m] : -1;
-    const bool ok = valid_key(j);
-    float dw = 0.f;
-    if (ok) {
-      const int64_t row = kv0 + (int64_t)j * d;
+  for (int64_t c0 = 0; c0 < k; c0 += 64) {
+    const int32_t jl = c0 + lane < k ? idx[c0 + lane] : -1;
+    const float sl = c0 + lane < k ? dots[c0 + lane] : 0.f;
+    const int n = (int)(k - c0 < 64 ? k - c0 : 64);
+    for (int e0 = 0; e0 < n; e0 += U * lm.S) {
+      uint4 xv[U][NCL];
+      int32_t jq[U];
 #pragma unroll
-      for (int u = 0; u < NCL; ++u) {
-        const int c = lm.part + lm.G * u;
-        if (c < lm.CH) {
-          float x[EPC];
-          load_chunk<T>(bp.V, row + (int64_t)c * EPC, x);
+      for (int q = 0; q < U; ++q) {
+        const int e = e0 + q * lm.S + lm.slot;
+        jq[q] = __shfl(jl, e & 63, 64);
+        if (e < n && valid_key(jq[q])) {
 #pragma unroll
-          for (int e = 0; e < EPC; ++e) dw = fmaf(x[e], gout[u][e], dw);
+          for (int u = 0; u < NCL; ++u) {
+            const int c = lm.part + lm.G * u;
+            if (c < lm.CH) xv[q][u] = load16<T>(bp.V, kv0 + (int64_t)jq[q] * d + (int64_t)c * EPC);
+          }
         }
       }
-    }
-    for (int off = 1; off < lm.G; off <<= 1) dw += __shfl_xor(dw, off, 64);
-    if (ok && lm.part == 0) {
-      const float s = dots[m];
-      const float w = softmax ? __expf(bp.scale * (s - mx)) * inv_z : fmaxf(s, 0.f);
-      pair[m] = make_float2(w, dw);
-      gpart += w * dw;
+#pragma unroll
+      for (int q = 0; q < U; ++q) {
+        const int e = e0 + q * lm.S + lm.slot;
+        const bool ok = e < n && valid_key(jq[q]);
+        float dw = 0.f;
+        if (ok) {
+#pragma unroll
+          for (int u = 0; u < NCL; ++u) {
+            const int c = lm.part + lm.G * u;
+            if (c < lm.CH) {
+              float x[EPC];
+              unpack<T>(xv[q][u], x);
+#pragma unroll
+              for (int t = 0; t < EPC; ++t) dw = fmaf(x[t], gout[u][t], dw);
+            }
+          }
+        }
+        for (int off = 1; off < lm.G; off <<= 1) dw += __shfl_xor(dw, off, 64);
+        const float s = __shfl(sl, e & 63, 64);
+        if (ok && lm.part == 0) {
+          const float w = softmax ? __expf(bp.scale * (s - mx)) * inv_z : fmaxf(s, 0.f);
+          pair[c0 + e] = make_float2(w, dw);
+          gpart += w * dw;
+        }
+      }
     }
   }
   const float g = wave_sum(gpart);
   __threadfence_block();  // this wave's pair writes are visible to its own reads below
 
-  // pass 3: d_top_dots and the per-key counts (one pair per lane), then
-  // d_Q = sum_m d_top_dots[m] K[j_m] (one pair per row slot)
+  // pass 3: d_top_dots and each pair's place among its key's pairs (one pair per
+  // lane), then d_Q = sum_m d_top_dots[m] K[j_m] (pairs dealt to the row slots)
   float acc[NCL][EPC];
 #pragma unroll
   for (int u = 0; u < NCL; ++u)
@@ -1752,38 +1780,53 @@ __global__ __launch_bounds__(256) void k_bwd_rows(BwdProblem bp, BwdBufs b) {
     for (int e = 0; e < EPC; ++e) acc[u][e] = 0.f;
   for (int64_t c0 = 0; c0 < k; c0 += 64) {
     const int64_t m = c0 + lane;
-    const int32_t j = m < k ? idx[m] : -1;
-    const bool ok = valid_key(j);
-    float ds = 0.f;
-    if (ok) {
+    const int32_t jl = m < k ? idx[m] : -1;
+    const bool okl = valid_key(jl);
+    float dsl = 0.f;
+    int32_t place = 0;
+    if (okl) {
       const float2 wdw = pair[m];
-      ds = softmax ? bp.scale * wdw.x * (wdw.y - g) : (dots[m] > 0.f ? wdw.y : 0.f);
-      pair[m] = make_float2(wdw.x, ds);
-      b.rank[r * k + m] = atomicAdd(&b.count[bh * bp.Lk + j], 1);
+      dsl = softmax ? bp.scale * wdw.x * (wdw.y - g) : (dots[m] > 0.f ? wdw.y : 0.f);
+      pair[m] = make_float2(wdw.x, dsl);
+      place = atomicAdd(&b.count[bh * bp.Lk + jl], 1);
     }
-    js[wave][lane] = ok && ds != 0.f ? j : -1;  // a zero score gradient adds nothing
-    dss[wave][lane] = ds;
-    wave_sync_lds();
+    const int32_t jg = okl && dsl != 0.f ? jl : -1;  // a zero score gradient adds nothing
     const int n = (int)(k - c0 < 64 ? k - c0 : 64);
-    for (int e0 = 0; e0 < n; e0 += lm.S) {
-      const int e = e0 + lm.slot;
-      const int32_t je = e < n ? js[wave][e] : -1;
-      if (je >= 0) {
-        const float dse = dss[wave][e];
-        const int64_t row = kv0 + (int64_t)je * d;
+    for (int e0 = 0; e0 < n; e0 += U * lm.S) {
+      uint4 xk[U][NCL];
+      int32_t jq[U];
+      float dq[U];
 #pragma unroll
-        for (int u = 0; u < NCL; ++u) {
-          const int c = lm.part + lm.G * u;
-          if (c < lm.CH) {
-            float x[EPC];
-            load_chunk<T>(bp.K, row + (int64_t)c * EPC, x);
+      for (int q = 0; q < U; ++q) {
+        const int e = e0 + q * lm.S + lm.slot;
+        jq[q] = __shfl(jg, e & 63, 64);
+        dq[q] = __shfl(dsl, e & 63, 64);
+        if (e < n && jq[q] >= 0) {
 #pragma unroll
-            for (int e2 = 0; e2 < EPC; ++e2) acc[u][e2] = fmaf(dse, x[e2], acc[u][e2]);
+          for (int u = 0; u < NCL; ++u) {
+            const int c = lm.part + lm.G * u;
+            if (c < lm.CH) xk[q][u] = load16<T>(bp.K, kv0 + (int64_t)jq[q] * d + (int64_t)c * EPC);
+          }
+        }
+      }
+#pragma unroll
+      for (int q = 0; q < U; ++q) {
+        const int e = e0 + q * lm.S + lm.slot;
+        if (e < n && jq[q] >= 0) {
+#pragma unroll
+          for (int u = 0; u < NCL; ++u) {
+            const int c = lm.part + lm.G * u;
+            if (c < lm.CH) {
+              float x[EPC];
+              unpack<T>(xk[q][u], x);
+#pragma unroll
+              for (int t = 0; t < EPC; ++t) acc[u][t] = fmaf(dq[q], x[t], acc[u][t]);
+            }
           }
         }
       }
     }
-    wave_sync_lds();
+    if (okl) b.rank[r * k + m] = place;
   }
   slot_reduce(acc, lm);
   if (lm.slot == 0) {
@@ -1862,9 +1905,9 @@ __global__ __launch_bounds__(256) void k_bwd_fill(BwdProblem bp, BwdBufs b) {
   }
 }
 
-template <typename T>
+template <typename T, int NCL>
 __global__ __launch_bounds__(256) void k_bwd_keys(BwdProblem bp, BwdBufs b) {
-  constexpr int EPC = RowChunks<T>::EPC, NCL = RowChunks<T>::NCL;
+  constexpr int EPC = RowChunks<T>::EPC, U = BWD_UNROLL;
   __shared__ int32_t lst[4][1024];
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
   const int64_t key = xcd_workgroup() * 4 + wave;
@@ -1878,32 +1921,52 @@ __global__ __launch_bounds__(256) void k_bwd_keys(BwdProblem bp, BwdBufs b) {
   for (int u = 0; u < NCL; ++u)
 #pragma unroll
     for (int e = 0; e < EPC; ++e) dv[u][e] = dk[u][e] = 0.f;
-  // one listed pair per row slot: slot s sums entries s, s + S, ... of the list
+  // one listed pair per row slot: slot s sums entries s, s + S, ... of the list,
+  // U steps of gathers in flight together
   auto accumulate = [&](auto get) {
-    for (int e0 = 0; e0 < n; e0 += lm.S) {
-      const int e = e0 + lm.slot;
-      if (e < n) {
-        const int32_t p = get(e);
-        const float2 c = b.pair[p];
-        const int64_t row = (int64_t)((uint32_t)p / kk) * d;
+    for (int e0 = 0; e0 < n; e0 += U * lm.S) {
+      uint4 xo[U][NCL], xq[U][NCL];
+      float2 c[U];
 #pragma unroll
-        for (int u = 0; u < NCL; ++u) {
-          const int ch = lm.part + lm.G * u;
-          if (ch < lm.CH) {
-            float x[EPC], y[EPC];
-            load_chunk<T>(bp.dout, row + (int64_t)ch * EPC, x);
-            load_chunk<T>(bp.Q, row + (int64_t)ch * EPC, y);
+      for (int q = 0; q < U; ++q) {
+        const int e = e0 + q * lm.S + lm.slot;
+        if (e < n) {
+          const int32_t p = get(e);
+          c[q] = b.pair[p];
+          const int64_t row = (int64_t)((uint32_t)p / kk) * d;
 #pragma unroll
-            for (int e2 = 0; e2 < EPC; ++e2) {
-              dv[u][e2] = fmaf(c.x, x[e2], dv[u][e2]);
-              dk[u][e2] = fmaf(c.y, y[e2], dk[u][e2]);
+          for (int u = 0; u < NCL; ++u) {
+            const int ch = lm.part + lm.G * u;
+            if (ch < lm.CH) {
+              xo[q][u] = load16<T>(bp.dout, row + (int64_t)ch * EPC);
+              xq[q][u] = load16<T>(bp.Q, row + (int64_t)ch * EPC);
+            }
+          }
+        }
+      }
+#pragma unroll
+      for (int q = 0; q < U; ++q) {
+        const int e = e0 + q * lm.S + lm.slot;
+        if (e < n) {
+#pragma unroll
+          for (int u = 0; u < NCL; ++u) {
+            const int ch = lm.part + lm.G * u;
+            if (ch < lm.CH) {
+              float x[EPC], y[EPC];
+              unpack<T>(xo[q][u], x);
+              unpack<T>(xq[q][u], y);
+#pragma unroll
+              for (int t = 0; t < EPC; ++t) {
+                dv[u][t] = fmaf(c[q].x, x[t], dv[u][t]);
+                dk[u][t] = fmaf(c[q].y, y[t], dk[u][t]);
+              }
             }
           }
         }
       }
     }
   };
-  // increasing pair order: a fixed summation order whatever order the fill took
+  // increasing pair order: a fixed summation order whatever order the places took
   auto sorted = [&](auto tag) {
     constexpr int E = decltype(tag)::value;
     uint64_t r[E];
@@ -1946,15 +2009,22 @@ hipError_t launch_backward(const BwdProblem& bp, const BwdBufs& b, hipStream_t s
   // grids rounded up to a multiple of 8 for the XCD-aware renumbering
   const unsigned grid_rows = (unsigned)(((rows + 3) / 4 + 7) / 8 * 8);
   const unsigned grid_keys = (unsigned)(((nkeys + 3) / 4 + 7) / 8 * 8);
-  if (bp.dtype == T_BF16) k_bwd_rows<uint16_t><<<grid_rows, 256, 0, st>>>(bp, b);
-  else k_bwd_rows<float><<<grid_rows, 256, 0, st>>>(bp, b);
+  const int ncl = lane_chunks(bp.d, bp.dtype == T_BF16 ? 2 : 4);
+#define TOPK_BWD(KERNEL, GRID)                                                                  \
+  if (bp.dtype == T_BF16 && ncl == 1) KERNEL<uint16_t, 1><<<GRID, 256, 0, st>>>(bp, b);          \
+  else if (bp.dtype == T_BF16 && ncl == 2) KERNEL<uint16_t, 2><<<GRID, 256, 0, st>>>(bp, b);     \
+  else if (bp.dtype == T_F32 && ncl == 1) KERNEL<float, 1><<<GRID, 256, 0, st>>>(bp, b);         \
+  else if (bp.dtype == T_F32 && ncl == 2) KERNEL<float, 2><<<GRID, 256, 0, st>>>(bp, b);         \
+  else if (bp.dtype == T_F32 && ncl == 4) KERNEL<float, 4><<<GRID, 256, 0, st>>>(bp, b);         \
+  else return hipErrorInvalidValue;
+  TOPK_BWD(k_bwd_rows, grid_rows)
   k_bwd_scan_local<<<(unsigned)nb, 256, 0, st>>>(b.count, nkeys + 1, b.block_sums);
   k_bwd_scan_sums<<<1, 256, 0, st>>>(b.block_sums, nb);
   k_bwd_scan_add<<<(unsigned)nb, 256, 0, st>>>(b.count, nkeys + 1, b.block_sums);
   const int64_t gf = (npairs + 255) / 256;
   k_bwd_fill<<<(unsigned)(gf < 65536 ? gf : 65536), 256, 0, st>>>(bp, b);
-  if (bp.dtype == T_BF16) k_bwd_keys<uint16_t><<<grid_keys, 256, 0, st>>>(bp, b);
-  else k_bwd_keys<float><<<grid_keys, 256, 0, st>>>(bp, b);
+  TOPK_BWD(k_bwd_keys, grid_keys)
+#undef TOPK_BWD
   return hipGetLastError();
 }
 
