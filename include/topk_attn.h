@@ -172,8 +172,9 @@ int topk_profile_end(double* stage_ms, int64_t* stage_launches, int n_stages);
  * keys selected by no row get zeros. All tensors are caller-owned device memory,
  * contiguous, in `dtype` (fp32 accumulation; bf16 results rounded to nearest even);
  * every output element is written. Entries of top_idx outside [0, Lk) are padding.
- * The sums over a key's rows run in increasing (row, slot) order when at most 1024
- * rows selected the key, so results do not depend on scheduling. Workspace:
+ * The sums over a key's rows run in increasing (row, slot) order, so results do
+ * not depend on scheduling (with atomic lists, see topk_set_backward_lists, only
+ * for keys that at most 1024 rows selected). Workspace:
  * topk_attn_backward_workspace_bytes() bytes, O(B*H*(Lq*k + Lk)) (the registered
  * workspace, or one allocated on the stream). Errors as topk_attn; additionally
  * TOPK_E_UNSUPPORTED when B*H*Lq*k or B*H*Lk reaches 2^31.
@@ -192,6 +193,23 @@ int topk_attn_backward(const void* Q, const void* K, const void* V, const int32_
 int topk_ffn_backward(const void* X, const void* W1, const void* W2, const int32_t* top_idx, const float* top_dots,
                       const void* d_out, void* d_X, void* d_W1, void* d_W2, int64_t N, int64_t d_model, int64_t d_ff,
                       int64_t k, int dtype, void* hip_stream);
+
+/*
+ * How the backward calls group the selected (row, key) pairs by key, process-wide:
+ * TOPK_LISTS_AUTO (default) takes the bucket sort for heads of up to 2^21 keys
+ * and atomic counters beyond; TOPK_LISTS_BUCKET asks for the bucket sort (a
+ * backward call on a larger head then fails with TOPK_E_UNSUPPORTED);
+ * TOPK_LISTS_ATOMIC asks for the atomic counters. The bucket sort (a two-level
+ * stable counting sort in LDS) writes every list in increasing pair order; atomic
+ * counters fill lists in arbitrary order and sort lists of up to 1024 pairs before
+ * summing. Both give the same gradients, bit for bit, where the atomic lists are
+ * sorted. The workspace size depends on the setting. Returns TOPK_OK, or
+ * TOPK_E_INVAL for another mode.
+ */
+#define TOPK_LISTS_AUTO 0
+#define TOPK_LISTS_BUCKET 1
+#define TOPK_LISTS_ATOMIC 2
+int topk_set_backward_lists(int mode);
 
 /* Workspace the backward calls need (0 for invalid arguments). */
 size_t topk_attn_backward_workspace_bytes(int64_t B, int64_t H, int64_t Lq, int64_t Lk, int64_t d, int64_t k,

@@ -19,11 +19,13 @@ import math
 import os
 
 __all__ = ["attn", "ffn", "attn_workspace_bytes", "ffn_workspace_bytes", "attn_path", "ffn_path",
-           "mfma_layout", "lib", "TopkError", "LIB_PATH", "profile_begin", "profile_end", "STAGES"]
+           "mfma_layout", "lib", "TopkError", "LIB_PATH", "profile_begin", "profile_end", "STAGES",
+           "attn_backward", "ffn_backward", "set_backward_lists", "last_fallback_rows"]
 
 LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libtopk.so")
 
 TOPK_F32, TOPK_BF16 = 0, 1
+TOPK_LISTS_AUTO, TOPK_LISTS_BUCKET, TOPK_LISTS_ATOMIC = 0, 1, 2
 _STATUS = {0: "OK", -1: "TOPK_E_INVAL", -2: "TOPK_E_NULL", -3: "TOPK_E_ALIGN", -4: "TOPK_E_UNSUPPORTED",
            -5: "TOPK_E_NOMEM", -6: "TOPK_E_HIP"}
 
@@ -59,6 +61,7 @@ def lib() -> ctypes.CDLL:
         "topk_set_workspace": ([vp, ctypes.c_size_t], i32),
         "topk_last_error": ([], ctypes.c_char_p),
         "topk_last_fallback_rows": ([], i64),
+        "topk_set_backward_lists": ([i32], i32),
         "topk_attn_backward": ([vp] * 9 + [i64] * 6 + [ctypes.c_float, i32, vp], i32),
         "topk_ffn_backward": ([vp] * 9 + [i64] * 4 + [i32, vp], i32),
         "topk_attn_backward_workspace_bytes": ([i64] * 6 + [i32], ctypes.c_size_t),
@@ -275,6 +278,12 @@ def profile_end():
     n = (ctypes.c_int64 * len(STAGES))()
     _raise(lib().topk_profile_end(ms, n, len(STAGES)))
     return {s: (ms[i], n[i]) for i, s in enumerate(STAGES)}
+
+
+def set_backward_lists(mode: int) -> None:
+    """How backward calls group the selected pairs by key (process-wide):
+    TOPK_LISTS_AUTO, TOPK_LISTS_BUCKET (stable bucket sort) or TOPK_LISTS_ATOMIC."""
+    _raise(lib().topk_set_backward_lists(int(mode)))
 
 
 def last_fallback_rows() -> int:

@@ -9,6 +9,7 @@
 #include <stdio.h>
 #include <string.h>
 
+#include <algorithm>
 #include <string>
 #include <vector>
 
@@ -330,24 +331,39 @@ size_t workspace_for(const Problem& pb) {
 }
 
 // ---------------------------------------------------------------- backward
+int g_list_mode = TOPK_LISTS_AUTO;  // process-wide, set by topk_set_backward_lists
+
 size_t bwd_bytes(const BwdProblem& bp) {
-  const int64_t nkeys = bp.BH * bp.Lk, npairs = bp.BH * bp.Lq * bp.k, nb = (nkeys + 1 + 1023) / 1024;
-  return up((size_t)npairs * 8) + up((size_t)(nkeys + 1) * 4) + 2 * up((size_t)npairs * 4) + up((size_t)nb * 4);
+  const int64_t nkeys = bp.BH * bp.Lk, npairs = bp.BH * bp.Lq * bp.k;
+  const BwdLayout L = bwd_layout(bp.BH, bp.Lq, bp.Lk, bp.k, g_list_mode);
+  const int64_t scanned = std::max(nkeys + 1, L.nhist + 1), nb = (scanned + 1023) / 1024;
+  size_t total = up((size_t)npairs * 8) + up((size_t)(nkeys + 1) * 4) + up((size_t)npairs * 4) + up((size_t)nb * 4);
+  if (L.bucketed) total += up((size_t)npairs * 8) + up((size_t)(L.nhist + 1) * 4);
+  else total += up((size_t)npairs * 4);
+  return total;
 }
 
 BwdBufs bwd_carve(const BwdProblem& bp, char* ws) {
   const int64_t nkeys = bp.BH * bp.Lk, npairs = bp.BH * bp.Lq * bp.k;
-  BwdBufs b;
+  BwdBufs b{};
+  b.L = bwd_layout(bp.BH, bp.Lq, bp.Lk, bp.k, g_list_mode);
+  const int64_t scanned = std::max(nkeys + 1, b.L.nhist + 1), nb = (scanned + 1023) / 1024;
   size_t off = 0;
   b.pair = (float2*)(ws + off);
   off += up((size_t)npairs * 8);
   b.count = (int32_t*)(ws + off);
   off += up((size_t)(nkeys + 1) * 4);
-  b.rank = (int32_t*)(ws + off);
-  off += up((size_t)npairs * 4);
   b.list = (int32_t*)(ws + off);
   off += up((size_t)npairs * 4);
   b.block_sums = (int32_t*)(ws + off);
+  off += up((size_t)nb * 4);
+  if (b.L.bucketed) {
+    b.stage = (uint64_t*)(ws + off);
+    off += up((size_t)npairs * 8);
+    b.hist = (int32_t*)(ws + off);
+  } else {
+    b.rank = (int32_t*)(ws + off);
+  }
   return b;
 }
 
@@ -358,6 +374,9 @@ int bwd_problem(BwdProblem* bp, const void* Q, const void* K, const void* V, con
   if (rc) return rc;
   if (BH * Lq > (int64_t(1) << 31) / k || BH * Lk >= (int64_t(1) << 31) - 1)
     return fail(TOPK_E_UNSUPPORTED, "the backward pass needs rows * k and heads * keys below 2^31");
+  if (g_list_mode == TOPK_LISTS_BUCKET && !bwd_layout(BH, Lq, Lk, k, g_list_mode).bucketed)
+    return fail(TOPK_E_UNSUPPORTED, "bucket-sorted backward lists need at most 2^21 keys per head (got %lld)",
+                (long long)Lk);
   if (check_ptrs) {
     if ((rc = check_ptr(Q, "queries")) || (rc = check_ptr(K, "keys")) || (rc = check_ptr(V, "values")) ||
         (rc = check_ptr(dout, "d_out")) || (rc = check_ptr(dQ, "d_queries")) || (rc = check_ptr(dK, "d_keys")) ||
@@ -513,6 +532,14 @@ size_t topk_ffn_backward_workspace_bytes(int64_t N, int64_t d_model, int64_t d_f
                   d_model, k, 0, 1.f, dtype, ACT_RELU, false))
     return 0;
   return bwd_bytes(bp);
+}
+
+int topk_set_backward_lists(int mode) {
+  g_err.clear();
+  if (mode != TOPK_LISTS_AUTO && mode != TOPK_LISTS_BUCKET && mode != TOPK_LISTS_ATOMIC)
+    return fail(TOPK_E_INVAL, "backward list mode must be TOPK_LISTS_AUTO, _BUCKET or _ATOMIC (got %d)", mode);
+  g_list_mode = mode;
+  return TOPK_OK;
 }
 
 const char* topk_last_error(void) { return g_err.c_str(); }

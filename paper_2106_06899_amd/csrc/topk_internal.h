@@ -91,12 +91,43 @@ struct BwdProblem {
   int act;
 };
 
+// How the backward pass groups the selected pairs by key. Heads of up to 2^21 keys
+// take a two-level stable bucket sort in LDS (keys in buckets of 1 << shift, at most
+// BK_MAXB buckets per head, the pairs of a head in tiles of BK_TILE); the lists come
+// out in increasing pair order. Larger heads count pairs with atomics on global
+// counters and sort each list before summing.
+constexpr int BK_TILE = 4096;
+constexpr int BK_MAXB = 256;
+constexpr int BK_MAXSHIFT = 13;  // at most 8192 keys per bucket
+struct BwdLayout {
+  bool bucketed;
+  int shift;        // keys per bucket = 1 << shift
+  int64_t nb;       // buckets per head
+  int64_t tiles;    // tiles per head
+  int64_t nhist;    // BH * nb * tiles tile counts
+};
+// list_mode: 0 automatic, 1 bucket sort, 2 atomic counters (as TOPK_LISTS_*)
+inline BwdLayout bwd_layout(int64_t BH, int64_t Lq, int64_t Lk, int64_t k, int list_mode) {
+  BwdLayout L{};
+  int s = 0;
+  while (((Lk + (int64_t(1) << s) - 1) >> s) > BK_MAXB) ++s;
+  L.bucketed = list_mode != 2 && s <= BK_MAXSHIFT;
+  L.shift = s;
+  L.nb = (Lk + (int64_t(1) << s) - 1) >> s;
+  L.tiles = (Lq * k + BK_TILE - 1) / BK_TILE;
+  L.nhist = L.bucketed ? BH * L.nb * L.tiles : 0;
+  return L;
+}
+
 struct BwdBufs {
+  BwdLayout L;
   float2* pair;         // [rows * k]: (activation weight, score gradient)
-  int32_t* count;       // [BH * Lk + 1]: pairs per key, then exclusive offsets
-  int32_t* rank;        // [rows * k]: each pair's place among its key's pairs
+  int32_t* count;       // [BH * Lk + 1]: exclusive offsets of the per-key lists
   int32_t* list;        // [rows * k]: pair ids grouped by key
-  int32_t* block_sums;  // [ceil((BH * Lk + 1) / 1024)] scan scratch
+  int32_t* block_sums;  // scan scratch, one entry per 1024 scanned values
+  int32_t* rank;        // atomic path, [rows * k]: each pair's place among its key's pairs
+  uint64_t* stage;      // bucketed path, [rows * k]: pairs grouped by bucket
+  int32_t* hist;        // bucketed path, [nhist + 1]: per-tile bucket counts, then offsets
 };
 
 hipError_t launch_backward(const BwdProblem& bp, const BwdBufs& b, hipStream_t st);

@@ -1571,17 +1571,19 @@ hipError_t launch_mfma_probe(int32_t* rows, int32_t* cols, hipStream_t st) {
 // with their raw scores. The backward pass recomputes the activation on the k
 // survivors, backpropagates through it, and forms the three gradients by gathers,
 // never an Lq x Lk matrix:
+//  0. the pairs grouped by key into per-key lists (see the bucket kernels below;
+//     heads of more than 2^21 keys use per-key atomic counters, steps 2-3);
 //  1. k_bwd_rows (one wave per query row): d_top_actv[m] = d_out . V[j_m] for the
 //     k selected keys; the activation (softmax with temperature, or ReLU)
 //     recomputed from the cached scores and backpropagated to d_top_dots;
 //     d_Q = sum_m d_top_dots[m] K[j_m]; each pair's (weight, score gradient) is
-//     kept, and its key's counter gives the pair its place among the key's pairs;
+//     kept (on the atomic path its key's counter also gives the pair its place);
 //  2. an exclusive scan of the per-key counts (k_bwd_scan_*);
 //  3. k_bwd_fill: each pair's id into its key's list at that place;
 //  4. k_bwd_keys (one wave per key): d_V[j] = sum weight * d_out[row] and
 //     d_K[j] = sum score gradient * Q[row] over the key's list, in increasing pair
-//     order (lists of up to 1024 pairs are sorted first). No floating-point
-//     atomics: the sums do not depend on scheduling.
+//     order (on the atomic path lists of up to 1024 pairs are sorted first). No
+//     floating-point atomics: the sums do not depend on scheduling.
 
 __global__ void k_bwd_zero(int32_t* p, int64_t n) {
   for (int64_t e = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; e < n; e += (int64_t)gridDim.x * blockDim.x)
@@ -1788,7 +1790,7 @@ __global__ __launch_bounds__(256) void k_bwd_rows(BwdProblem bp, BwdBufs b) {
       const float2 wdw = pair[m];
       dsl = softmax ? bp.scale * wdw.x * (wdw.y - g) : (dots[m] > 0.f ? wdw.y : 0.f);
       pair[m] = make_float2(wdw.x, dsl);
-      place = atomicAdd(&b.count[bh * bp.Lk + jl], 1);
+      if (!b.L.bucketed) place = atomicAdd(&b.count[bh * bp.Lk + jl], 1);
     }
     const int32_t jg = okl && dsl != 0.f ? jl : -1;  // a zero score gradient adds nothing
     const int n = (int)(k - c0 < 64 ? k - c0 : 64);
@@ -1826,7 +1828,7 @@ __global__ __launch_bounds__(256) void k_bwd_rows(BwdProblem bp, BwdBufs b) {
         }
       }
     }
-    if (okl) b.rank[r * k + m] = place;
+    if (okl && !b.L.bucketed) b.rank[r * k + m] = place;
   }
   slot_reduce(acc, lm);
   if (lm.slot == 0) {
@@ -1902,6 +1904,177 @@ __global__ __launch_bounds__(256) void k_bwd_fill(BwdProblem bp, BwdBufs b) {
     if (j < 0 || (int64_t)j >= bp.Lk) continue;
     const int64_t key = (int64_t)(p / per_head) * bp.Lk + j;
     b.list[b.count[key] + b.rank[p]] = (int32_t)p;
+  }
+}
+
+// ---- per-key lists by a two-level stable bucket sort (heads of up to 2^21 keys)
+// Level 1 groups each head's pairs by bucket (key >> shift): k_bwd_bucket_count
+// counts every tile's pairs per bucket, a scan over (head, bucket, tile) gives each
+// tile's run of every bucket, k_bwd_bucket_scatter places the tile's pairs in LDS
+// grouped by bucket and writes the runs out. Level 2, k_bwd_bucket_lists (one
+// workgroup per bucket), counts the bucket's pairs per key, writes the keys' list
+// offsets, and places each pair in its key's list. Ranks within a wave come from
+// ballots over the digit bits and pairs are taken in increasing order, so every
+// list is in increasing pair order. One wave per workgroup: the order of its LDS
+// updates is program order.
+
+// lanes among `active` whose v agrees with this lane's v on the low `bits` bits
+__device__ __forceinline__ uint64_t match_low_bits(uint32_t v, int bits, uint64_t active) {
+  uint64_t peers = active;
+  for (int t = 0; t < bits; ++t) {
+    const bool bit = (v >> t) & 1u;
+    const uint64_t bal = __ballot(bit);
+    peers &= bit ? bal : ~bal;
+  }
+  return peers;
+}
+__device__ __forceinline__ uint32_t lanes_below(uint64_t m) {
+  return __builtin_amdgcn_mbcnt_hi((uint32_t)(m >> 32), __builtin_amdgcn_mbcnt_lo((uint32_t)m, 0u));
+}
+__device__ __forceinline__ int digit_bits(int64_t n) {  // bits that tell apart 0 .. n - 1
+  int t = 0;
+  while ((int64_t(1) << t) < n) ++t;
+  return t;
+}
+// exclusive scan of a[0 .. n) in LDS by one wave, plus `base`; returns the total
+__device__ __forceinline__ uint32_t wave_excl_scan_lds(uint32_t* a, int n, uint32_t base) {
+  const int lane = threadIdx.x & 63;
+  uint32_t carry = base;
+  for (int c0 = 0; c0 < n; c0 += 64) {
+    const int i = c0 + lane;
+    const uint32_t v = i < n ? a[i] : 0u;
+    uint32_t x = v;
+#pragma unroll
+    for (int off = 1; off < 64; off <<= 1) {
+      const uint32_t y = __shfl_up(x, off, 64);
+      if (lane >= off) x += y;
+    }
+    if (i < n) a[i] = carry + x - v;
+    carry += __shfl(x, 63, 64);
+  }
+  wave_sync_lds();
+  return carry;
+}
+
+constexpr int BK_PER_LANE = BK_TILE / 64;  // a tile's pair ids per lane, loaded up front
+constexpr int BK_BATCH = 8;                  // chunks of 64 stage entries loaded together
+
+__global__ __launch_bounds__(64) void k_bwd_bucket_count(BwdProblem bp, BwdLayout L, int32_t* hist) {
+  __shared__ uint32_t cnt[BK_MAXB];
+  const int lane = threadIdx.x;
+  const int64_t head = blockIdx.x / L.tiles, t = blockIdx.x - head * L.tiles;
+  const int64_t per_head = bp.Lq * bp.k, e_beg = t * BK_TILE;
+  const int n = (int)(per_head - e_beg < BK_TILE ? per_head - e_beg : BK_TILE);
+  const int32_t* idx = bp.idx + head * per_head + e_beg;
+  for (int i = lane; i < L.nb; i += 64) cnt[i] = 0;
+  int32_t jj[BK_PER_LANE];
+#pragma unroll
+  for (int u = 0; u < BK_PER_LANE; ++u) jj[u] = u * 64 + lane < n ? idx[u * 64 + lane] : -1;
+  wave_sync_lds();
+#pragma unroll
+  for (int u = 0; u < BK_PER_LANE; ++u)
+    if (jj[u] >= 0 && (int64_t)jj[u] < bp.Lk) atomicAdd(&cnt[jj[u] >> L.shift], 1u);
+  wave_sync_lds();
+  for (int i = lane; i < L.nb; i += 64) hist[(head * L.nb + i) * L.tiles + t] = (int32_t)cnt[i];
+  if (blockIdx.x == 0 && lane == 0) hist[L.nhist] = 0;
+}
+
+// stage entry: bits 0..30 pair id, 32..44 key within its bucket, 48..55 bucket
+__global__ __launch_bounds__(64) void k_bwd_bucket_scatter(BwdProblem bp, BwdLayout L, const int32_t* off,
+                                                           uint64_t* stage) {
+  __shared__ uint32_t start[BK_MAXB], cur[BK_MAXB];
+  __shared__ int32_t gpos[BK_MAXB];
+  __shared__ uint64_t buf[BK_TILE];
+  const int lane = threadIdx.x;
+  const int64_t head = blockIdx.x / L.tiles, t = blockIdx.x - head * L.tiles;
+  const int64_t per_head = bp.Lq * bp.k, e_beg = t * BK_TILE, p_beg = head * per_head + e_beg;
+  const int n = (int)(per_head - e_beg < BK_TILE ? per_head - e_beg : BK_TILE);
+  int32_t jj[BK_PER_LANE];
+#pragma unroll
+  for (int u = 0; u < BK_PER_LANE; ++u) jj[u] = u * 64 + lane < n ? bp.idx[p_beg + u * 64 + lane] : -1;
+  for (int i = lane; i < L.nb; i += 64) {
+    const int64_t h = (head * L.nb + i) * L.tiles + t;
+    gpos[i] = off[h];
+    start[i] = (uint32_t)(off[h + 1] - off[h]);  // this tile's count, scanned below
+  }
+  wave_sync_lds();
+  const uint32_t nvalid = wave_excl_scan_lds(start, (int)L.nb, 0u);
+  for (int i = lane; i < L.nb; i += 64) cur[i] = start[i];
+  wave_sync_lds();
+  const int bbits = digit_bits(L.nb);
+  const uint32_t kmask = (1u << L.shift) - 1u;
+#pragma unroll
+  for (int u = 0; u < BK_PER_LANE; ++u) {
+    const int32_t j = jj[u];
+    const bool ok = j >= 0 && (int64_t)j < bp.Lk;
+    const uint32_t bk = ok ? (uint32_t)j >> L.shift : 0u;
+    const uint64_t peers = match_low_bits(bk, bbits, __ballot(ok));
+    const uint32_t prior = ok ? cur[bk] : 0u;
+    const uint32_t rank = lanes_below(peers);
+    if (ok) {
+      buf[prior + rank] = ((uint64_t)bk << 48) | ((uint64_t)((uint32_t)j & kmask) << 32) |
+                          (uint64_t)(p_beg + u * 64 + lane);
+      if (rank == 0) cur[bk] = prior + (uint32_t)__popcll(peers);
+    }
+    wave_sync_lds();
+  }
+  // write the runs: consecutive lanes write consecutive entries of a run
+  for (uint32_t i = lane; i < nvalid; i += 64) {
+    const uint64_t v = buf[i];
+    const uint32_t bk = (uint32_t)(v >> 48);
+    stage[gpos[bk] + (i - start[bk])] = v;
+  }
+}
+
+__global__ __launch_bounds__(64) void k_bwd_bucket_lists(BwdProblem bp, BwdLayout L, const int32_t* off,
+                                                         const uint64_t* stage, BwdBufs b) {
+  extern __shared__ uint32_t cur[];  // [1 << shift]: per-key counts, then list cursors
+  const int lane = threadIdx.x;
+  const int64_t head = blockIdx.x / L.nb, bk = blockIdx.x - head * L.nb, hb = head * L.nb + bk;
+  const int32_t beg = off[hb * L.tiles], end = off[(hb + 1) * L.tiles];
+  const int KB = 1 << L.shift;
+  const int64_t key0 = bk * KB;
+  const int nkb = (int)(bp.Lk - key0 < KB ? bp.Lk - key0 : KB);
+  const uint32_t kmask = (uint32_t)KB - 1u;
+  for (int i = lane; i < KB; i += 64) cur[i] = 0;
+  wave_sync_lds();
+  // pairs per key; BK_BATCH chunks of loads in flight
+  for (int32_t e0 = beg; e0 < end; e0 += 64 * BK_BATCH) {
+    uint32_t kq[BK_BATCH];
+#pragma unroll
+    for (int u = 0; u < BK_BATCH; ++u) {
+      const int32_t e = e0 + u * 64 + lane;
+      kq[u] = e < end ? (uint32_t)(stage[e] >> 32) & kmask : 0xFFFFFFFFu;
+    }
+#pragma unroll
+    for (int u = 0; u < BK_BATCH; ++u)
+      if (kq[u] != 0xFFFFFFFFu) atomicAdd(&cur[kq[u]], 1u);
+  }
+  wave_sync_lds();
+  wave_excl_scan_lds(cur, KB, (uint32_t)beg);
+  for (int i = lane; i < nkb; i += 64) b.count[head * bp.Lk + key0 + i] = (int32_t)cur[i];
+  if (hb == bp.BH * L.nb - 1 && lane == 0) b.count[bp.BH * bp.Lk] = end;
+  // each pair into its key's list, in increasing pair order
+  for (int32_t e0 = beg; e0 < end; e0 += 64 * BK_BATCH) {
+    uint64_t vq[BK_BATCH];
+#pragma unroll
+    for (int u = 0; u < BK_BATCH; ++u) {
+      const int32_t e = e0 + u * 64 + lane;
+      vq[u] = e < end ? stage[e] : 0ull;
+    }
+#pragma unroll
+    for (int u = 0; u < BK_BATCH; ++u) {
+      const bool ok = e0 + u * 64 + lane < end;
+      const uint32_t key = (uint32_t)(vq[u] >> 32) & kmask;
+      const uint64_t peers = match_low_bits(key, L.shift, __ballot(ok));
+      const uint32_t prior = ok ? cur[key] : 0u;
+      const uint32_t rank = lanes_below(peers);
+      if (ok) {
+        b.list[prior + rank] = (int32_t)(vq[u] & 0x7FFFFFFFull);
+        if (rank == 0) cur[key] = prior + (uint32_t)__popcll(peers);
+      }
+      wave_sync_lds();
+    }
   }
 }
 
@@ -1981,7 +2154,8 @@ __global__ __launch_bounds__(256) void k_bwd_keys(BwdProblem bp, BwdBufs b) {
     wave_sync_lds();
     accumulate([&](int e) { return lst[wave][e]; });
   };
-  if (n <= 64) sorted(std::integral_constant<int, 1>{});
+  if (b.L.bucketed) accumulate([&](int e) { return b.list[beg + e]; });
+  else if (n <= 64) sorted(std::integral_constant<int, 1>{});
   else if (n <= 128) sorted(std::integral_constant<int, 2>{});
   else if (n <= 256) sorted(std::integral_constant<int, 4>{});
   else if (n <= 512) sorted(std::integral_constant<int, 8>{});
@@ -2002,10 +2176,25 @@ __global__ __launch_bounds__(256) void k_bwd_keys(BwdProblem bp, BwdBufs b) {
   }
 }
 
+// exclusive scan of a[0 .. n) in place; sums holds ceil(n / 1024) entries
+static void scan_in_place(int32_t* a, int64_t n, int32_t* sums, hipStream_t st) {
+  const int64_t nb = (n + 1023) / 1024;
+  k_bwd_scan_local<<<(unsigned)nb, 256, 0, st>>>(a, n, sums);
+  k_bwd_scan_sums<<<1, 256, 0, st>>>(sums, nb);
+  k_bwd_scan_add<<<(unsigned)nb, 256, 0, st>>>(a, n, sums);
+}
+
 hipError_t launch_backward(const BwdProblem& bp, const BwdBufs& b, hipStream_t st) {
   const int64_t nkeys = bp.BH * bp.Lk, rows = bp.BH * bp.Lq, npairs = rows * bp.k;
-  const int64_t nb = (nkeys + 1 + 1023) / 1024;
-  k_bwd_zero<<<1024, 256, 0, st>>>(b.count, nkeys + 1);
+  const BwdLayout& L = b.L;
+  if (L.bucketed) {
+    k_bwd_bucket_count<<<(unsigned)(bp.BH * L.tiles), 64, 0, st>>>(bp, L, b.hist);
+    scan_in_place(b.hist, L.nhist + 1, b.block_sums, st);
+    k_bwd_bucket_scatter<<<(unsigned)(bp.BH * L.tiles), 64, 0, st>>>(bp, L, b.hist, b.stage);
+    k_bwd_bucket_lists<<<(unsigned)(bp.BH * L.nb), 64, sizeof(uint32_t) << L.shift, st>>>(bp, L, b.hist, b.stage, b);
+  } else {
+    k_bwd_zero<<<1024, 256, 0, st>>>(b.count, nkeys + 1);
+  }
   // grids rounded up to a multiple of 8 for the XCD-aware renumbering
   const unsigned grid_rows = (unsigned)(((rows + 3) / 4 + 7) / 8 * 8);
   const unsigned grid_keys = (unsigned)(((nkeys + 3) / 4 + 7) / 8 * 8);
@@ -2018,11 +2207,11 @@ hipError_t launch_backward(const BwdProblem& bp, const BwdBufs& b, hipStream_t s
   else if (bp.dtype == T_F32 && ncl == 4) KERNEL<float, 4><<<GRID, 256, 0, st>>>(bp, b);         \
   else return hipErrorInvalidValue;
   TOPK_BWD(k_bwd_rows, grid_rows)
-  k_bwd_scan_local<<<(unsigned)nb, 256, 0, st>>>(b.count, nkeys + 1, b.block_sums);
-  k_bwd_scan_sums<<<1, 256, 0, st>>>(b.block_sums, nb);
-  k_bwd_scan_add<<<(unsigned)nb, 256, 0, st>>>(b.count, nkeys + 1, b.block_sums);
-  const int64_t gf = (npairs + 255) / 256;
-  k_bwd_fill<<<(unsigned)(gf < 65536 ? gf : 65536), 256, 0, st>>>(bp, b);
+  if (!L.bucketed) {
+    scan_in_place(b.count, nkeys + 1, b.block_sums, st);
+    const int64_t gf = (npairs + 255) / 256;
+    k_bwd_fill<<<(unsigned)(gf < 65536 ? gf : 65536), 256, 0, st>>>(bp, b);
+  }
   TOPK_BWD(k_bwd_keys, grid_keys)
 #undef TOPK_BWD
   return hipGetLastError();

@@ -104,3 +104,28 @@ def test_bench_refuses_more_than_one_gpu():
                        timeout=120)
     assert r.returncode != 0
     assert "one GPU" in r.stderr
+
+
+def test_backward_list_modes():
+    """The list-mode setting is validated; the bucket sort needs more workspace than
+    atomic counters (a stage entry per pair and the tile counts) and refuses heads of
+    more than 2^21 keys, which the automatic mode gives to atomic counters."""
+    L = tk.lib()
+    assert L.topk_set_backward_lists(3) == E_INVAL
+    assert L.topk_set_backward_lists(-1) == E_INVAL
+    shape = (1, 4, 4096, 8192, 64, 64, 1)
+    try:
+        tk.set_backward_lists(tk.TOPK_LISTS_ATOMIC)
+        atomic = L.topk_attn_backward_workspace_bytes(*shape)
+        tk.set_backward_lists(tk.TOPK_LISTS_BUCKET)
+        bucket = L.topk_attn_backward_workspace_bytes(*shape)
+        assert bucket > atomic > 0
+        pairs = 4 * 4096 * 64
+        assert bucket - atomic >= pairs * 4  # 8-byte stage entries instead of 4-byte places
+        big = (1, 1, 16, (1 << 21) + 1, 8, 4, 1)
+        assert L.topk_attn_backward_workspace_bytes(*big) == 0  # bucket sort refuses
+        tk.set_backward_lists(tk.TOPK_LISTS_AUTO)
+        assert L.topk_attn_backward_workspace_bytes(*shape) == bucket
+        assert L.topk_attn_backward_workspace_bytes(*big) > 0
+    finally:
+        tk.set_backward_lists(tk.TOPK_LISTS_AUTO)

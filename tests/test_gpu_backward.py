@@ -117,3 +117,87 @@ def test_backward_is_deterministic():
     torch.cuda.synchronize()
     for a, b in zip(first, second):
         assert torch.equal(a, b)
+
+
+def _with_lists(mode, fn):
+    tk.set_backward_lists(mode)
+    try:
+        return fn()
+    finally:
+        tk.set_backward_lists(tk.TOPK_LISTS_AUTO)
+
+
+LIST_CASES = {
+    "c3_bf16": ("attn", "c3", dict(H=2, Lq=512, Lk=4096, chunk=256)),
+    "c4_bf16_causal": ("attn", "c4", dict(B=1, H=2, Lq=600, Lk=600, chunk=128)),
+    "c5_bf16": ("ffn", "c5", dict(N=300, d_model=256, d_ff=3000, k=128, chunk=64)),
+}
+
+
+def _run_backward(kind, w, x, seed):
+    if kind == "attn":
+        q, k, v = (parity.to_dev(x[n]) for n in ("Q", "K", "V"))
+        _, idx, dots = tk.attn(q, k, v, w.k, w.chunk, w.causal, w.scale, debug=True)
+        g = parity.to_dev(_grad_out((w.B, w.H, w.Lq, w.d), w.dtype, seed))
+        return idx, lambda: tk.attn_backward(q, k, v, idx, dots, g, w.scale)
+    a, b1, b2 = (parity.to_dev(x[n]) for n in ("X", "W1", "W2"))
+    _, idx, dots = tk.ffn(a, b1, b2, w.k, w.chunk, debug=True)
+    g = parity.to_dev(_grad_out((w.N, w.d_model), w.dtype, seed))
+    return idx, lambda: tk.ffn_backward(a, b1, b2, idx, dots, g)
+
+
+@pytest.mark.parametrize("name", sorted(LIST_CASES))
+def test_bucket_and_atomic_lists_agree_bit_for_bit(name):
+    """Both ways of grouping the pairs by key sum every key's pairs in increasing
+    pair order (atomic lists here hold at most 1024 pairs, so they are sorted):
+    the gradients agree bit for bit."""
+    kind, base, kw = LIST_CASES[name]
+    w = wl.WORKLOADS[base].scaled(**kw)
+    _say(name, w)
+    x = wl.make_inputs(w)
+    _, step = _run_backward(kind, w, x, 80)
+    bucket = _with_lists(tk.TOPK_LISTS_BUCKET, step)
+    atomic = _with_lists(tk.TOPK_LISTS_ATOMIC, step)
+    torch.cuda.synchronize()
+    for a, b in zip(bucket, atomic):
+        assert torch.equal(a, b)
+
+
+EDGE_CASES = {
+    # one key per bucket (Lk <= 256), a ragged last tile (Lq * k not a multiple of 4096)
+    "attn_lk100": ("attn", "c1", dict(Lq=333, Lk=100, k=7, chunk=64), tk.TOPK_LISTS_BUCKET),
+    # two keys per bucket, a partial last bucket
+    "attn_lk301_causal": ("attn", "c1", dict(Lq=301, Lk=301, k=16, chunk=64, causal=True), tk.TOPK_LISTS_BUCKET),
+    # lists of about 2000 pairs (beyond the atomic path's sorted lists)
+    "ffn_long_lists": ("ffn", "c5", dict(N=4096, d_model=64, d_ff=64, k=32, chunk=512), tk.TOPK_LISTS_BUCKET),
+    "ffn_long_lists_atomic": ("ffn", "c5", dict(N=4096, d_model=64, d_ff=64, k=32, chunk=512), tk.TOPK_LISTS_ATOMIC),
+    # 2^21 keys: the largest head the bucket sort takes (8192 keys per bucket)
+    "attn_2m_keys_bucket": ("attn", "c3", dict(H=1, Lq=24, Lk=1 << 21, d=8, k=8, chunk=24, planted=0),
+                            tk.TOPK_LISTS_BUCKET),
+    # one key more: the automatic mode takes atomic counters
+    "attn_2m_keys_auto_atomic": ("attn", "c3", dict(H=1, Lq=24, Lk=(1 << 21) + 1, d=8, k=8, chunk=24, planted=0),
+                                 tk.TOPK_LISTS_AUTO),
+}
+
+
+@pytest.mark.parametrize("name", sorted(EDGE_CASES))
+def test_backward_list_edges(name):
+    kind, base, kw, mode = EDGE_CASES[name]
+    w = wl.WORKLOADS[base].scaled(**kw)
+    _say(name, w)
+    x = wl.make_inputs(w)
+    idx, step = _run_backward(kind, w, x, 81)
+    got = _with_lists(mode, step)
+    torch.cuda.synchronize()
+    ix = idx.cpu().numpy()
+    if kind == "attn":
+        g = _grad_out((w.B, w.H, w.Lq, w.d), w.dtype, 81)
+        ref = bo.oracle_attn_backward(x["Q"].values, x["K"].values, x["V"].values, ix, g.values, w.scale,
+                                      chunk=min(w.chunk, 8))
+        names = ("d_Q", "d_K", "d_V")
+    else:
+        g = _grad_out((w.N, w.d_model), w.dtype, 81)
+        ref = bo.oracle_ffn_backward(x["X"].values, x["W1"].values, x["W2"].values, ix, g.values, chunk=w.chunk)
+        names = ("d_X", "d_W1", "d_W2")
+    errs = [_check(n, a, b, w.dtype) for n, a, b in zip(names, got, ref)]
+    _say(name, "ok", dict(zip(names, errs)))
