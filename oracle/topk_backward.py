@@ -133,3 +133,46 @@ def oracle_ffn_backward(X, W1, W2, top_idx, d_out, chunk=None):
         dW1 += g1
         dW2 += g2
     return dX, dW1, dW2
+
+
+def row_terms(Qr, K, V, top_idx_r, d_out_r, activation, scale=1.0):
+    """Steps 1-3 for a set of rows: (top_actv, d_top_dots), each [R, k], from the
+    rows' queries Qr [R, d], index sets top_idx_r [R, k] and output gradients d_out_r."""
+    Qr, d_out_r = _f64(Qr), _f64(d_out_r)
+    valid = top_idx_r >= 0
+    safe = np.where(valid, top_idx_r, 0)
+    top_dots = selected_dots(Qr, K, top_idx_r)
+    d_top_actv = np.where(valid, np.einsum("rt,rmt->rm", d_out_r, _f64(V[safe])), 0.0)
+    return activation_backward(top_dots, d_top_actv, valid, activation, scale)
+
+
+def sampled_backward(Q, K, V, top_idx, d_out, rows, keys, activation, scale=1.0, batch=64):
+    """The gradients of one head at a sample of rows and keys, for checks at sizes
+    where the dense [Lq, Lk] matrices of chunk_backward do not fit: Q [Lq, d],
+    K and V [Lk, d], top_idx [Lq, k], d_out [Lq, d].
+
+    Step 5 restricted to rows: d_Q[r] = sum_m d_top_dots[r, m] K[top_idx[r, m]];
+    steps 4-5 restricted to keys: d_K[j] = sum over the (r, m) with top_idx[r, m] = j
+    of d_top_dots[r, m] Q[r], and d_V[j] the same with top_actv[r, m] d_out[r]. Rows
+    go through steps 1-3 `batch` at a time. Returns fp64 (d_Q [len(rows), d],
+    d_K [len(keys), d], d_V [len(keys), d]), keys taken in increasing order."""
+    rows = np.asarray(rows, dtype=np.int64)
+    keys = np.unique(np.asarray(keys, dtype=np.int64))
+    k, d = top_idx.shape[1], Q.shape[1]
+    dQ = np.zeros((len(rows), d))
+    for b0 in range(0, len(rows), batch):
+        rb = rows[b0:b0 + batch]
+        _, dd = row_terms(Q[rb], K, V, top_idx[rb], d_out[rb], activation, scale)
+        safe = np.where(top_idx[rb] >= 0, top_idx[rb], 0)
+        dQ[b0:b0 + batch] = np.einsum("rm,rmt->rt", dd, _f64(K[safe]))
+    sel_rows = np.unique(np.flatnonzero(np.isin(top_idx.ravel(), keys)) // k)  # rows that chose a sampled key
+    dK = np.zeros((len(keys), d))
+    dV = np.zeros((len(keys), d))
+    for b0 in range(0, len(sel_rows), batch):
+        rb = sel_rows[b0:b0 + batch]
+        actv, dd = row_terms(Q[rb], K, V, top_idx[rb], d_out[rb], activation, scale)
+        a, m = np.nonzero(np.isin(top_idx[rb], keys))
+        n = np.searchsorted(keys, top_idx[rb][a, m])
+        np.add.at(dK, n, dd[a, m, None] * _f64(Q[rb][a]))
+        np.add.at(dV, n, actv[a, m, None] * _f64(d_out[rb][a]))
+    return dQ, dK, dV

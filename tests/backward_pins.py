@@ -178,4 +178,31 @@ def pin_bwd_chunk_invariance_and_padding(bo):
     assert sel_last[:, : L - 1].sum() == 0
 
 
+
+def pin_bwd_sampled_equals_full(bo):
+    """The sampled backward (per-row steps, then sums restricted to chosen rows and
+    keys) equals the full chunked backward at those rows and keys, for the softmax
+    (causal, with padded rows) and for ReLU."""
+    rng = _rng(107)
+    L, d, k = 40, 6, 5
+    Q, K, V, G = (rng.standard_normal((1, 1, L, d)) for _ in range(4))
+    r = fwd.oracle_attn(Q, K, V, k, 8, True, 0.4)
+    full = bo.oracle_attn_backward(Q, K, V, r["idx"], G, 0.4, chunk=8)
+    rows, keys = np.array([0, 3, 17, 39]), np.array([0, 1, 20, 39])
+    got = bo.sampled_backward(Q[0, 0], K[0, 0], V[0, 0], r["idx"][0, 0], G[0, 0], rows, keys, "softmax", 0.4)
+    _close(got[0], full[0][0, 0][rows], 1e-12, "sampled dQ")
+    _close(got[1], full[1][0, 0][keys], 1e-12, "sampled dK")
+    _close(got[2], full[2][0, 0][keys], 1e-12, "sampled dV")
+    N, dff = 30, 50
+    X, Gx = rng.standard_normal((N, d)), rng.standard_normal((N, d))
+    W1, W2 = rng.standard_normal((dff, d)), rng.standard_normal((dff, d))
+    rf = fwd.oracle_ffn(X, W1, W2, 7, 0)
+    fullf = bo.oracle_ffn_backward(X, W1, W2, rf["idx"], Gx, chunk=9)
+    rows, keys = np.array([1, 29]), np.arange(0, dff, 7)
+    got = bo.sampled_backward(X, W1, W2, rf["idx"], Gx, rows, keys, "relu")
+    _close(got[0], fullf[0][rows], 1e-12, "sampled dX")
+    _close(got[1], fullf[1][keys], 1e-12, "sampled dW1")
+    _close(got[2], fullf[2][keys], 1e-12, "sampled dW2")
+
+
 ALL_PINS = [v for kname, v in sorted(globals().items()) if kname.startswith("pin_")]

@@ -120,3 +120,13 @@ def sample_attn_rows(w: wl.Workload, n: int, seed=0):
     rest = n - len(picks)
     rand = np.stack([rng.integers(0, w.B, rest), rng.integers(0, w.H, rest), rng.integers(0, w.Lq, rest)], -1)
     return np.concatenate([np.array(picks, dtype=np.int64).reshape(-1, 3), rand]).astype(np.int64)
+
+
+def grad_out(shape, dtype, seed) -> wl.Tensor:
+    """A seeded standard-normal output gradient in the workload's dtype."""
+    rng = np.random.Generator(np.random.PCG64(seed))
+    g = rng.standard_normal(shape).astype(np.float32)
+    if dtype == wl.BF16:
+        bits = wl.f32_to_bf16_bits(g)
+        return wl.Tensor(wl.bf16_bits_to_f32(bits), bits, wl.BF16)
+    return wl.Tensor(g, None, wl.F32)

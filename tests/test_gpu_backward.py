@@ -34,12 +34,7 @@ def _gpu():
 
 
 def _grad_out(shape, dtype, seed):
-    rng = np.random.Generator(np.random.PCG64(seed))
-    g = rng.standard_normal(shape).astype(np.float32)
-    if dtype == wl.BF16:
-        bits = wl.f32_to_bf16_bits(g)
-        return wl.Tensor(wl.bf16_bits_to_f32(bits), bits, wl.BF16)
-    return wl.Tensor(g, None, wl.F32)
+    return parity.grad_out(shape, dtype, seed)
 
 
 def _check(name, got, ref, dtype):

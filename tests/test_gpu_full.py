@@ -8,6 +8,7 @@ import torch
 
 import paper_2106_06899_amd as tk
 from paper_2106_06899_amd import workloads as wl
+from oracle import topk_backward as bo
 from tests import parity
 
 pytestmark = pytest.mark.gpu
@@ -58,3 +59,86 @@ def test_ffn_full_size():
     g = idx.cpu().numpy()
     assert np.all((g >= 0).sum(-1) == w.k)
     assert torch.isfinite(out.float()).all()
+
+
+# ---------------------------------------------------------------- backward, full size
+BWD_RTOL = {wl.F32: 1e-5, wl.BF16: 2e-2}
+
+
+def _sample_keys(idx_head, Lk, rng, n):
+    """Keys 0 and Lk - 1, the three most selected keys, and n random keys."""
+    counts = np.bincount(idx_head[idx_head >= 0].ravel(), minlength=Lk)
+    hot = np.argsort(-counts, kind="stable")[:3]
+    return np.unique(np.concatenate([[0, Lk - 1], hot, rng.integers(0, Lk, n)]))
+
+
+def _check_sample(name, got, ref, rtol):
+    scale = max(float(np.abs(ref).max()), 1e-30)
+    err = np.abs(got.astype(np.float64) - ref).max(axis=1) / scale
+    assert np.all(err <= rtol), f"{name}: error {err.max():.3e} > {rtol} at sample {int(np.argmax(err))}"
+    return float(err.max())
+
+
+def _unselected_are_zero(idx, dk, dv, Lk):
+    """Every key that no row selected gets exactly zero gradients (any size)."""
+    counts = np.bincount(idx[idx >= 0].ravel(), minlength=Lk)
+    cold = np.flatnonzero(counts == 0)
+    assert not np.any(dk[cold]) and not np.any(dv[cold])
+    return len(cold)
+
+
+@pytest.mark.parametrize("name", ["c3", "c4"])
+def test_attn_backward_full_size(name):
+    """The backward call bench.py --backward times, at the full workload: d_Q at
+    sampled rows and d_K, d_V at sampled keys of three heads against the oracle's
+    sampled backward (computed from the same cached index sets)."""
+    w = wl.WORKLOADS[name]
+    _say(name, "backward", w.note)
+    x = wl.make_inputs(w)
+    q, k, v = (parity.to_dev(x[n]) for n in ("Q", "K", "V"))
+    _, idx, dots = tk.attn(q, k, v, w.k, w.chunk, w.causal, w.scale, debug=True)
+    g = parity.grad_out((w.B, w.H, w.Lq, w.d), w.dtype, 5)
+    dq, dk, dv = tk.attn_backward(q, k, v, idx, dots, parity.to_dev(g), w.scale)
+    torch.cuda.synchronize()
+    ix = idx.cpu().numpy()
+    dq, dk, dv = (t.float().cpu().numpy() for t in (dq, dk, dv))
+    assert np.isfinite(dq).all() and np.isfinite(dk).all() and np.isfinite(dv).all()
+    rng = np.random.Generator(np.random.PCG64(w.seed + 1))
+    heads = sorted({(0, 0), (w.B - 1, w.H - 1), (int(rng.integers(w.B)), int(rng.integers(w.H)))})
+    C = w.chunk or w.Lq
+    rtol = BWD_RTOL[w.dtype]
+    for b, h in heads:
+        rows = np.unique(np.concatenate([[0, 1, C - 1, C, min(w.k - 1, w.Lq - 1), w.Lq - 1],
+                                         rng.integers(0, w.Lq, 40)]))
+        keys = _sample_keys(ix[b, h], w.Lk, rng, 24)
+        rq, rk, rv = bo.sampled_backward(x["Q"].values[b, h], x["K"].values[b, h], x["V"].values[b, h], ix[b, h],
+                                         g.values[b, h], rows, keys, "softmax", w.scale)
+        errs = (_check_sample("d_Q", dq[b, h][rows], rq, rtol), _check_sample("d_K", dk[b, h][keys], rk, rtol),
+                _check_sample("d_V", dv[b, h][keys], rv, rtol))
+        cold = _unselected_are_zero(ix[b, h], dk[b, h], dv[b, h], w.Lk)
+        _say(name, f"head ({b},{h}) rows {len(rows)} keys {len(keys)} unselected keys {cold} errors", errs)
+
+
+def test_ffn_backward_full_size():
+    """The feed-forward backward at the full c5 workload: d_X at sampled rows and
+    d_W1, d_W2 at sampled keys (hidden units) against the oracle's sampled backward."""
+    w = wl.WORKLOADS["c5"]
+    _say("c5", "backward", w.note)
+    x = wl.make_inputs(w)
+    a, b1, b2 = (parity.to_dev(x[n]) for n in ("X", "W1", "W2"))
+    _, idx, dots = tk.ffn(a, b1, b2, w.k, w.chunk, debug=True)
+    g = parity.grad_out((w.N, w.d_model), w.dtype, 5)
+    dx, dw1, dw2 = tk.ffn_backward(a, b1, b2, idx, dots, parity.to_dev(g))
+    torch.cuda.synchronize()
+    ix = idx.cpu().numpy()
+    dx, dw1, dw2 = (t.float().cpu().numpy() for t in (dx, dw1, dw2))
+    assert np.isfinite(dx).all() and np.isfinite(dw1).all() and np.isfinite(dw2).all()
+    rng = np.random.Generator(np.random.PCG64(w.seed + 1))
+    rows = np.unique(np.concatenate([[0, 1, w.chunk - 1, w.chunk, w.N - 1], rng.integers(0, w.N, 40)]))
+    keys = _sample_keys(ix, w.d_ff, rng, 16)
+    rx, r1, r2 = bo.sampled_backward(x["X"].values, x["W1"].values, x["W2"].values, ix, g.values, rows, keys, "relu")
+    rtol = BWD_RTOL[w.dtype]
+    errs = (_check_sample("d_X", dx[rows], rx, rtol), _check_sample("d_W1", dw1[keys], r1, rtol),
+            _check_sample("d_W2", dw2[keys], r2, rtol))
+    cold = _unselected_are_zero(ix, dw1, dw2, w.d_ff)
+    _say("c5", f"rows {len(rows)} keys {len(keys)} unselected keys {cold} errors", errs)
