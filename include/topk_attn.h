@@ -196,7 +196,7 @@ int topk_ffn_backward(const void* X, const void* W1, const void* W2, const int32
 
 /*
  * How the backward calls group the selected (row, key) pairs by key, process-wide:
- * TOPK_LISTS_AUTO (default) takes the bucket sort for heads of up to 2^21 keys
+ * TOPK_LISTS_AUTO (default) takes the bucket sort for heads of up to 2^19 keys
  * and atomic counters beyond; TOPK_LISTS_BUCKET asks for the bucket sort (a
  * backward call on a larger head then fails with TOPK_E_UNSUPPORTED);
  * TOPK_LISTS_ATOMIC asks for the atomic counters. The bucket sort (a two-level

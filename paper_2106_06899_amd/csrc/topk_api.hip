@@ -375,7 +375,7 @@ int bwd_problem(BwdProblem* bp, const void* Q, const void* K, const void* V, con
   if (BH * Lq > (int64_t(1) << 31) / k || BH * Lk >= (int64_t(1) << 31) - 1)
     return fail(TOPK_E_UNSUPPORTED, "the backward pass needs rows * k and heads * keys below 2^31");
   if (g_list_mode == TOPK_LISTS_BUCKET && !bwd_layout(BH, Lq, Lk, k, g_list_mode).bucketed)
-    return fail(TOPK_E_UNSUPPORTED, "bucket-sorted backward lists need at most 2^21 keys per head (got %lld)",
+    return fail(TOPK_E_UNSUPPORTED, "bucket-sorted backward lists need at most 2^19 keys per head (got %lld)",
                 (long long)Lk);
   if (check_ptrs) {
     if ((rc = check_ptr(Q, "queries")) || (rc = check_ptr(K, "keys")) || (rc = check_ptr(V, "values")) ||

@@ -91,17 +91,19 @@ struct BwdProblem {
   int act;
 };
 
-// How the backward pass groups the selected pairs by key. Heads of up to 2^21 keys
+// How the backward pass groups the selected pairs by key. Heads of up to 2^19 keys
 // take a two-level stable bucket sort in LDS (keys in buckets of 1 << shift, at most
 // BK_MAXB buckets per head, the pairs of a head in tiles of BK_TILE); the lists come
 // out in increasing pair order. Larger heads count pairs with atomics on global
 // counters and sort each list before summing.
 constexpr int BK_TILE = 4096;
 constexpr int BK_MAXB = 256;
-constexpr int BK_MAXSHIFT = 13;  // at most 8192 keys per bucket
+constexpr int BK_MAXSHIFT = 11;         // at most 2048 keys per bucket
+constexpr int BK_LIST_LDS = 40 * 1024;  // LDS of a list workgroup: 4 waves' counters + staged lists
 struct BwdLayout {
   bool bucketed;
   int shift;        // keys per bucket = 1 << shift
+  int lcap;         // list entries a bucket may stage in LDS (larger buckets write directly)
   int64_t nb;       // buckets per head
   int64_t tiles;    // tiles per head
   int64_t nhist;    // BH * nb * tiles tile counts
@@ -113,6 +115,7 @@ inline BwdLayout bwd_layout(int64_t BH, int64_t Lq, int64_t Lk, int64_t k, int l
   while (((Lk + (int64_t(1) << s) - 1) >> s) > BK_MAXB) ++s;
   L.bucketed = list_mode != 2 && s <= BK_MAXSHIFT;
   L.shift = s;
+  L.lcap = (BK_LIST_LDS - 4 * 4 * (1 << (s < BK_MAXSHIFT ? s : BK_MAXSHIFT))) / 4;
   L.nb = (Lk + (int64_t(1) << s) - 1) >> s;
   L.tiles = (Lq * k + BK_TILE - 1) / BK_TILE;
   L.nhist = L.bucketed ? BH * L.nb * L.tiles : 0;

@@ -1572,7 +1572,7 @@ hipError_t launch_mfma_probe(int32_t* rows, int32_t* cols, hipStream_t st) {
 // survivors, backpropagates through it, and forms the three gradients by gathers,
 // never an Lq x Lk matrix:
 //  0. the pairs grouped by key into per-key lists (see the bucket kernels below;
-//     heads of more than 2^21 keys use per-key atomic counters, steps 2-3);
+//     heads of more than 2^19 keys use per-key atomic counters, steps 2-3);
 //  1. k_bwd_rows (one wave per query row): d_top_actv[m] = d_out . V[j_m] for the
 //     k selected keys; the activation (softmax with temperature, or ReLU)
 //     recomputed from the cached scores and backpropagated to d_top_dots;
@@ -1907,7 +1907,7 @@ __global__ __launch_bounds__(256) void k_bwd_fill(BwdProblem bp, BwdBufs b) {
   }
 }
 
-// ---- per-key lists by a two-level stable bucket sort (heads of up to 2^21 keys)
+// ---- per-key lists by a two-level stable bucket sort (heads of up to 2^19 keys)
 // Level 1 groups each head's pairs by bucket (key >> shift): k_bwd_bucket_count
 // counts every tile's pairs per bucket, a scan over (head, bucket, tile) gives each
 // tile's run of every bucket, k_bwd_bucket_scatter places the tile's pairs in LDS
@@ -1956,51 +1956,87 @@ __device__ __forceinline__ uint32_t wave_excl_scan_lds(uint32_t* a, int n, uint3
   return carry;
 }
 
-constexpr int BK_PER_LANE = BK_TILE / 64;  // a tile's pair ids per lane, loaded up front
-constexpr int BK_BATCH = 8;                  // chunks of 64 stage entries loaded together
+constexpr int BK_WAVES = 4;                             // waves per bucket-pass workgroup
+constexpr int BK_PER_LANE = BK_TILE / (64 * BK_WAVES);  // a wave's quarter of a tile, per lane
+constexpr int BK_BATCH = 8;                             // chunks of 64 stage entries loaded together
 
-__global__ __launch_bounds__(64) void k_bwd_bucket_count(BwdProblem bp, BwdLayout L, int32_t* hist) {
+__global__ __launch_bounds__(256) void k_bwd_bucket_count(BwdProblem bp, BwdLayout L, int32_t* hist) {
   __shared__ uint32_t cnt[BK_MAXB];
-  const int lane = threadIdx.x;
+  const int tid = threadIdx.x;
   const int64_t head = blockIdx.x / L.tiles, t = blockIdx.x - head * L.tiles;
   const int64_t per_head = bp.Lq * bp.k, e_beg = t * BK_TILE;
   const int n = (int)(per_head - e_beg < BK_TILE ? per_head - e_beg : BK_TILE);
   const int32_t* idx = bp.idx + head * per_head + e_beg;
-  for (int i = lane; i < L.nb; i += 64) cnt[i] = 0;
   int32_t jj[BK_PER_LANE];
 #pragma unroll
-  for (int u = 0; u < BK_PER_LANE; ++u) jj[u] = u * 64 + lane < n ? idx[u * 64 + lane] : -1;
-  wave_sync_lds();
+  for (int u = 0; u < BK_PER_LANE; ++u) jj[u] = u * 256 + tid < n ? idx[u * 256 + tid] : -1;
+  for (int i = tid; i < L.nb; i += 256) cnt[i] = 0;
+  __syncthreads();
 #pragma unroll
   for (int u = 0; u < BK_PER_LANE; ++u)
     if (jj[u] >= 0 && (int64_t)jj[u] < bp.Lk) atomicAdd(&cnt[jj[u] >> L.shift], 1u);
-  wave_sync_lds();
-  for (int i = lane; i < L.nb; i += 64) hist[(head * L.nb + i) * L.tiles + t] = (int32_t)cnt[i];
-  if (blockIdx.x == 0 && lane == 0) hist[L.nhist] = 0;
+  __syncthreads();
+  for (int i = tid; i < L.nb; i += 256) hist[(head * L.nb + i) * L.tiles + t] = (int32_t)cnt[i];
+  if (blockIdx.x == 0 && tid == 0) hist[L.nhist] = 0;
 }
 
-// stage entry: bits 0..30 pair id, 32..44 key within its bucket, 48..55 bucket
-__global__ __launch_bounds__(64) void k_bwd_bucket_scatter(BwdProblem bp, BwdLayout L, const int32_t* off,
-                                                           uint64_t* stage) {
-  __shared__ uint32_t start[BK_MAXB], cur[BK_MAXB];
+// stage entry: bits 0..30 pair id, 32..42 key within its bucket, 48..55 bucket.
+// Wave w places the w-th quarter of the tile; its cursor in a bucket's run starts
+// after the lower waves' pairs of that bucket, so the runs stay in pair order.
+__global__ __launch_bounds__(256) void k_bwd_bucket_scatter(BwdProblem bp, BwdLayout L, const int32_t* off,
+                                                            uint64_t* stage) {
+  __shared__ uint32_t cur[BK_WAVES][BK_MAXB];  // per-wave counts, then per-wave cursors
+  __shared__ uint32_t start[BK_MAXB];
   __shared__ int32_t gpos[BK_MAXB];
+  __shared__ uint32_t tmp[4], nvalid_s;
   __shared__ uint64_t buf[BK_TILE];
-  const int lane = threadIdx.x;
+  const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
   const int64_t head = blockIdx.x / L.tiles, t = blockIdx.x - head * L.tiles;
   const int64_t per_head = bp.Lq * bp.k, e_beg = t * BK_TILE, p_beg = head * per_head + e_beg;
   const int n = (int)(per_head - e_beg < BK_TILE ? per_head - e_beg : BK_TILE);
+  const int e_w = wave * (BK_TILE / BK_WAVES);
   int32_t jj[BK_PER_LANE];
 #pragma unroll
-  for (int u = 0; u < BK_PER_LANE; ++u) jj[u] = u * 64 + lane < n ? bp.idx[p_beg + u * 64 + lane] : -1;
-  for (int i = lane; i < L.nb; i += 64) {
-    const int64_t h = (head * L.nb + i) * L.tiles + t;
-    gpos[i] = off[h];
-    start[i] = (uint32_t)(off[h + 1] - off[h]);  // this tile's count, scanned below
+  for (int u = 0; u < BK_PER_LANE; ++u) {
+    const int e = e_w + u * 64 + lane;
+    jj[u] = e < n ? bp.idx[p_beg + e] : -1;
   }
-  wave_sync_lds();
-  const uint32_t nvalid = wave_excl_scan_lds(start, (int)L.nb, 0u);
-  for (int i = lane; i < L.nb; i += 64) cur[i] = start[i];
-  wave_sync_lds();
+  for (int i = tid; i < BK_WAVES * BK_MAXB; i += 256) (&cur[0][0])[i] = 0;
+  __syncthreads();
+#pragma unroll
+  for (int u = 0; u < BK_PER_LANE; ++u)
+    if (jj[u] >= 0 && (int64_t)jj[u] < bp.Lk) atomicAdd(&cur[wave][jj[u] >> L.shift], 1u);
+  __syncthreads();
+  // tile-local run starts (thread tid takes buckets BPT * tid ...) and each wave's
+  // cursor in its run
+  constexpr int BPT = BK_MAXB / 256;
+  uint32_t tot[BPT], all = 0;
+#pragma unroll
+  for (int q = 0; q < BPT; ++q) {
+    const int bk = tid * BPT + q;
+    tot[q] = 0;
+    if (bk < L.nb)
+      for (int w = 0; w < BK_WAVES; ++w) tot[q] += cur[w][bk];
+    all += tot[q];
+  }
+  uint32_t st = team_excl_scan<256>(all, tmp);
+#pragma unroll
+  for (int q = 0; q < BPT; ++q) {
+    const int bk = tid * BPT + q;
+    if (bk < L.nb) {
+      start[bk] = st;
+      gpos[bk] = off[(head * L.nb + bk) * L.tiles + t];
+      uint32_t c = st;
+      for (int w = 0; w < BK_WAVES; ++w) {
+        const uint32_t x = cur[w][bk];
+        cur[w][bk] = c;
+        c += x;
+      }
+    }
+    st += tot[q];
+  }
+  if (tid == 255) nvalid_s = st;
+  __syncthreads();
   const int bbits = digit_bits(L.nb);
   const uint32_t kmask = (1u << L.shift) - 1u;
 #pragma unroll
@@ -2009,72 +2045,107 @@ __global__ __launch_bounds__(64) void k_bwd_bucket_scatter(BwdProblem bp, BwdLay
     const bool ok = j >= 0 && (int64_t)j < bp.Lk;
     const uint32_t bk = ok ? (uint32_t)j >> L.shift : 0u;
     const uint64_t peers = match_low_bits(bk, bbits, __ballot(ok));
-    const uint32_t prior = ok ? cur[bk] : 0u;
+    const uint32_t prior = ok ? cur[wave][bk] : 0u;
     const uint32_t rank = lanes_below(peers);
     if (ok) {
       buf[prior + rank] = ((uint64_t)bk << 48) | ((uint64_t)((uint32_t)j & kmask) << 32) |
-                          (uint64_t)(p_beg + u * 64 + lane);
-      if (rank == 0) cur[bk] = prior + (uint32_t)__popcll(peers);
+                          (uint64_t)(p_beg + e_w + u * 64 + lane);
+      if (rank == 0) cur[wave][bk] = prior + (uint32_t)__popcll(peers);
     }
     wave_sync_lds();
   }
-  // write the runs: consecutive lanes write consecutive entries of a run
-  for (uint32_t i = lane; i < nvalid; i += 64) {
+  __syncthreads();
+  // write the runs: consecutive threads write consecutive entries of a run
+  const uint32_t nvalid = nvalid_s;
+  for (uint32_t i = tid; i < nvalid; i += 256) {
     const uint64_t v = buf[i];
     const uint32_t bk = (uint32_t)(v >> 48);
     stage[gpos[bk] + (i - start[bk])] = v;
   }
 }
 
-__global__ __launch_bounds__(64) void k_bwd_bucket_lists(BwdProblem bp, BwdLayout L, const int32_t* off,
-                                                         const uint64_t* stage, BwdBufs b) {
-  extern __shared__ uint32_t cur[];  // [1 << shift]: per-key counts, then list cursors
-  const int lane = threadIdx.x;
+// One workgroup per bucket; wave w takes the w-th quarter of the bucket's pairs
+// (cursors after the lower waves' pairs of each key, as in the scatter).
+__global__ __launch_bounds__(256) void k_bwd_bucket_lists(BwdProblem bp, BwdLayout L, const int32_t* off,
+                                                          const uint64_t* stage, BwdBufs b) {
+  // [BK_WAVES][1 << shift] per-wave counts, then cursors; then up to lcap list entries
+  extern __shared__ uint32_t cur[];
+  __shared__ uint32_t tmp[4];
+  const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
   const int64_t head = blockIdx.x / L.nb, bk = blockIdx.x - head * L.nb, hb = head * L.nb + bk;
   const int32_t beg = off[hb * L.tiles], end = off[(hb + 1) * L.tiles];
   const int KB = 1 << L.shift;
   const int64_t key0 = bk * KB;
   const int nkb = (int)(bp.Lk - key0 < KB ? bp.Lk - key0 : KB);
   const uint32_t kmask = (uint32_t)KB - 1u;
-  for (int i = lane; i < KB; i += 64) cur[i] = 0;
-  wave_sync_lds();
-  // pairs per key; BK_BATCH chunks of loads in flight
-  for (int32_t e0 = beg; e0 < end; e0 += 64 * BK_BATCH) {
+  // a bucket whose lists fit in LDS is placed there and written out contiguously
+  const bool staged = end - beg <= L.lcap;
+  int32_t* lds_list = (int32_t*)(cur + (BK_WAVES << L.shift));
+  const int32_t share = ((end - beg + BK_WAVES - 1) / BK_WAVES + 63) / 64 * 64;
+  const int32_t wb = beg + wave * share, we = wb + share < end ? wb + share : end;
+  uint32_t* wc = cur + wave * KB;
+  for (int i = tid; i < BK_WAVES * KB; i += 256) cur[i] = 0;
+  __syncthreads();
+  // this wave's pairs per key; BK_BATCH chunks of loads in flight
+  for (int32_t e0 = wb; e0 < we; e0 += 64 * BK_BATCH) {
     uint32_t kq[BK_BATCH];
 #pragma unroll
     for (int u = 0; u < BK_BATCH; ++u) {
       const int32_t e = e0 + u * 64 + lane;
-      kq[u] = e < end ? (uint32_t)(stage[e] >> 32) & kmask : 0xFFFFFFFFu;
+      kq[u] = e < we ? (uint32_t)(stage[e] >> 32) & kmask : 0xFFFFFFFFu;
     }
 #pragma unroll
     for (int u = 0; u < BK_BATCH; ++u)
-      if (kq[u] != 0xFFFFFFFFu) atomicAdd(&cur[kq[u]], 1u);
+      if (kq[u] != 0xFFFFFFFFu) atomicAdd(&wc[kq[u]], 1u);
   }
-  wave_sync_lds();
-  wave_excl_scan_lds(cur, KB, (uint32_t)beg);
-  for (int i = lane; i < nkb; i += 64) b.count[head * bp.Lk + key0 + i] = (int32_t)cur[i];
-  if (hb == bp.BH * L.nb - 1 && lane == 0) b.count[bp.BH * bp.Lk] = end;
-  // each pair into its key's list, in increasing pair order
-  for (int32_t e0 = beg; e0 < end; e0 += 64 * BK_BATCH) {
+  __syncthreads();
+  // list starts (keys in order) and each wave's cursor; thread tid takes `per` keys
+  const int per = (KB + 255) / 256, kq0 = tid * per;
+  uint32_t tot = 0;
+  for (int i = 0; i < per; ++i)
+    if (kq0 + i < KB)
+      for (int w = 0; w < BK_WAVES; ++w) tot += cur[w * KB + kq0 + i];
+  uint32_t c = (uint32_t)beg + team_excl_scan<256>(tot, tmp);
+  for (int i = 0; i < per; ++i) {
+    const int key = kq0 + i;
+    if (key < KB) {
+      if (key < nkb) b.count[head * bp.Lk + key0 + key] = (int32_t)c;
+      for (int w = 0; w < BK_WAVES; ++w) {
+        const uint32_t x = cur[w * KB + key];
+        cur[w * KB + key] = c;
+        c += x;
+      }
+    }
+  }
+  if (hb == bp.BH * L.nb - 1 && tid == 0) b.count[bp.BH * bp.Lk] = end;
+  __syncthreads();
+  // each of this wave's pairs into its key's list, in increasing pair order
+  for (int32_t e0 = wb; e0 < we; e0 += 64 * BK_BATCH) {
     uint64_t vq[BK_BATCH];
 #pragma unroll
     for (int u = 0; u < BK_BATCH; ++u) {
       const int32_t e = e0 + u * 64 + lane;
-      vq[u] = e < end ? stage[e] : 0ull;
+      vq[u] = e < we ? stage[e] : 0ull;
     }
 #pragma unroll
     for (int u = 0; u < BK_BATCH; ++u) {
-      const bool ok = e0 + u * 64 + lane < end;
+      const bool ok = e0 + u * 64 + lane < we;
       const uint32_t key = (uint32_t)(vq[u] >> 32) & kmask;
       const uint64_t peers = match_low_bits(key, L.shift, __ballot(ok));
-      const uint32_t prior = ok ? cur[key] : 0u;
+      const uint32_t prior = ok ? wc[key] : 0u;
       const uint32_t rank = lanes_below(peers);
       if (ok) {
-        b.list[prior + rank] = (int32_t)(vq[u] & 0x7FFFFFFFull);
-        if (rank == 0) cur[key] = prior + (uint32_t)__popcll(peers);
+        const int32_t p = (int32_t)(vq[u] & 0x7FFFFFFFull);
+        if (staged) lds_list[prior + rank - (uint32_t)beg] = p;
+        else b.list[prior + rank] = p;
+        if (rank == 0) wc[key] = prior + (uint32_t)__popcll(peers);
       }
       wave_sync_lds();
     }
+  }
+  if (staged) {
+    __syncthreads();
+    for (int32_t i = tid; i < end - beg; i += 256) b.list[beg + i] = lds_list[i];
   }
 }
 
@@ -2188,10 +2259,10 @@ hipError_t launch_backward(const BwdProblem& bp, const BwdBufs& b, hipStream_t s
   const int64_t nkeys = bp.BH * bp.Lk, rows = bp.BH * bp.Lq, npairs = rows * bp.k;
   const BwdLayout& L = b.L;
   if (L.bucketed) {
-    k_bwd_bucket_count<<<(unsigned)(bp.BH * L.tiles), 64, 0, st>>>(bp, L, b.hist);
+    k_bwd_bucket_count<<<(unsigned)(bp.BH * L.tiles), 256, 0, st>>>(bp, L, b.hist);
     scan_in_place(b.hist, L.nhist + 1, b.block_sums, st);
-    k_bwd_bucket_scatter<<<(unsigned)(bp.BH * L.tiles), 64, 0, st>>>(bp, L, b.hist, b.stage);
-    k_bwd_bucket_lists<<<(unsigned)(bp.BH * L.nb), 64, sizeof(uint32_t) << L.shift, st>>>(bp, L, b.hist, b.stage, b);
+    k_bwd_bucket_scatter<<<(unsigned)(bp.BH * L.tiles), 256, 0, st>>>(bp, L, b.hist, b.stage);
+    k_bwd_bucket_lists<<<(unsigned)(bp.BH * L.nb), 256, BK_LIST_LDS, st>>>(bp, L, b.hist, b.stage, b);
   } else {
     k_bwd_zero<<<1024, 256, 0, st>>>(b.count, nkeys + 1);
   }

@@ -109,7 +109,7 @@ def test_bench_refuses_more_than_one_gpu():
 def test_backward_list_modes():
     """The list-mode setting is validated; the bucket sort needs more workspace than
     atomic counters (a stage entry per pair and the tile counts) and refuses heads of
-    more than 2^21 keys, which the automatic mode gives to atomic counters."""
+    more than 2^19 keys, which the automatic mode gives to atomic counters."""
     L = tk.lib()
     assert L.topk_set_backward_lists(3) == E_INVAL
     assert L.topk_set_backward_lists(-1) == E_INVAL
@@ -122,7 +122,7 @@ def test_backward_list_modes():
         assert bucket > atomic > 0
         pairs = 4 * 4096 * 64
         assert bucket - atomic >= pairs * 4  # 8-byte stage entries instead of 4-byte places
-        big = (1, 1, 16, (1 << 21) + 1, 8, 4, 1)
+        big = (1, 1, 16, (1 << 19) + 1, 8, 4, 1)
         assert L.topk_attn_backward_workspace_bytes(*big) == 0  # bucket sort refuses
         tk.set_backward_lists(tk.TOPK_LISTS_AUTO)
         assert L.topk_attn_backward_workspace_bytes(*shape) == bucket

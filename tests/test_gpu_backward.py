@@ -166,12 +166,14 @@ EDGE_CASES = {
     # lists of about 2000 pairs (beyond the atomic path's sorted lists)
     "ffn_long_lists": ("ffn", "c5", dict(N=4096, d_model=64, d_ff=64, k=32, chunk=512), tk.TOPK_LISTS_BUCKET),
     "ffn_long_lists_atomic": ("ffn", "c5", dict(N=4096, d_model=64, d_ff=64, k=32, chunk=512), tk.TOPK_LISTS_ATOMIC),
-    # 2^21 keys: the largest head the bucket sort takes (8192 keys per bucket)
-    "attn_2m_keys_bucket": ("attn", "c3", dict(H=1, Lq=24, Lk=1 << 21, d=8, k=8, chunk=24, planted=0),
-                            tk.TOPK_LISTS_BUCKET),
+    # about 12288 pairs per key: buckets too large to stage their lists in LDS
+    "ffn_lists_beyond_lds": ("ffn", "c5", dict(N=16384, d_model=64, d_ff=64, k=48, chunk=1024), tk.TOPK_LISTS_BUCKET),
+    # 2^19 keys: the largest head the bucket sort takes (2048 keys per bucket, 256 buckets)
+    "attn_512k_keys_bucket": ("attn", "c3", dict(H=1, Lq=96, Lk=1 << 19, d=8, k=8, chunk=48, planted=0),
+                              tk.TOPK_LISTS_BUCKET),
     # one key more: the automatic mode takes atomic counters
-    "attn_2m_keys_auto_atomic": ("attn", "c3", dict(H=1, Lq=24, Lk=(1 << 21) + 1, d=8, k=8, chunk=24, planted=0),
-                                 tk.TOPK_LISTS_AUTO),
+    "attn_512k_keys_auto_atomic": ("attn", "c3", dict(H=1, Lq=96, Lk=(1 << 19) + 1, d=8, k=8, chunk=48,
+                                                      planted=0), tk.TOPK_LISTS_AUTO),
 }
 
 
