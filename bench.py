@@ -156,7 +156,7 @@ def bench_backward(args, w, x, dev_tensor):
         "warmup": args.warmup, "ms_per_step": ms_step, "higher_is_better": True, "scaling": "weak",
         "vs_baseline": None, "dtype": "bf16" if w.dtype == wl.BF16 else "f32", "data": "synthetic",
         "config": {"workload": f"{w.name}: {w.note}", "selected_pairs": pairs},
-        "roofline": {"kernel": "backward call (rows, scan, fill, keys)", "bound": "hbm", "achieved": achieved,
+        "roofline": {"kernel": "backward call (list build, row and key gathers)", "bound": "hbm", "achieved": achieved,
                      "peak": PEAK_HBM_GBS, "unit": "GB/s", "frac": achieved / PEAK_HBM_GBS, "traffic": None,
                      "algorithmic_bytes_per_launch": algo_bytes, "avg_launch_ms": bwd_ms},
     }
