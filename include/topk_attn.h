@@ -108,6 +108,24 @@ int topk_ffn_debug(const void* X, const void* W1, const void* W2, void* out,
                    int32_t* idx_out, float* score_out);
 
 /*
+ * Forward pass for training with input checkpointing (Section 2.2, "Input
+ * checkpointing"): the same computation as topk_attn / topk_ffn, also writing the
+ * cache the backward calls take: top_idx int32 [rows, k] and top_dots fp32
+ * [rows, k], laid out as idx_out / score_out above (both required, 4-byte aligned,
+ * caller-owned device memory). Unlike the debug variants these calls do not read
+ * anything back: they only enqueue on hip_stream. Errors as topk_attn, and
+ * TOPK_E_NULL when top_idx or top_dots is NULL.
+ */
+int topk_attn_with_cache(const void* Q, const void* K, const void* V, void* out,
+                         int64_t B, int64_t H, int64_t Lq, int64_t Lk, int64_t d,
+                         int64_t k, int64_t chunk, int causal, float scale,
+                         int dtype, void* hip_stream, int32_t* top_idx, float* top_dots);
+int topk_ffn_with_cache(const void* X, const void* W1, const void* W2, void* out,
+                        int64_t N, int64_t d_model, int64_t d_ff, int64_t k,
+                        int64_t chunk, int dtype, void* hip_stream,
+                        int32_t* top_idx, float* top_dots);
+
+/*
  * Workspace (bytes) a call with these arguments uses under the default memory
  * budget; 0 when the arguments are invalid. Register at least this much with
  * topk_set_workspace() to run without library allocations. The budget caps the

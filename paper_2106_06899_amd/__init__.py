@@ -56,6 +56,8 @@ def lib() -> ctypes.CDLL:
         "topk_attn_debug": (attn_args + [vp, vp], i32),
         "topk_ffn": (ffn_args, i32),
         "topk_ffn_debug": (ffn_args + [vp, vp], i32),
+        "topk_attn_with_cache": (attn_args + [vp, vp], i32),
+        "topk_ffn_with_cache": (ffn_args + [vp, vp], i32),
         "topk_attn_workspace_bytes": ([i64] * 7 + [i32, i32], ctypes.c_size_t),
         "topk_ffn_workspace_bytes": ([i64] * 5 + [i32], ctypes.c_size_t),
         "topk_set_workspace": ([vp, ctypes.c_size_t], i32),
@@ -142,12 +144,15 @@ def ffn_path(N, d_model, d_ff, k, chunk=0, dtype=TOPK_BF16) -> int:
 
 
 def attn(q, k, v, topk: int, chunk: int = 0, causal: bool = False, scale: float | None = None,
-         debug: bool = False):
-    """Top-k attention over [B, H, L, d] tensors; returns out (and idx, scores if debug).
+         debug: bool = False, cache: bool = False):
+    """Top-k attention over [B, H, L, d] tensors; returns out (and idx, scores if debug
+    or cache).
 
     ``scale`` is the softmax temperature 1/lambda of Eq. 1 (default 1/sqrt(d)).
     ``debug`` also returns the selected indices (int32 [B, H, Lq, topk], -1 pads) and
-    their raw fp32 scores (-inf pads), ordered by (score desc, index asc).
+    their raw fp32 scores (-inf pads), ordered by (score desc, index asc), and records
+    the fallback row count (the call waits for the stream). ``cache`` returns the same
+    two tensors, the backward pass's input-checkpointing cache, without waiting.
     """
     import torch
     device = q.device
@@ -162,23 +167,25 @@ def attn(q, k, v, topk: int, chunk: int = 0, causal: bool = False, scale: float 
     if scale is None:
         scale = 1.0 / math.sqrt(d)
     out = torch.empty_like(q)
-    idx = torch.empty((B, H, Lq, topk), dtype=torch.int32, device=device) if debug else None
-    sc = torch.empty((B, H, Lq, topk), dtype=torch.float32, device=device) if debug else None
+    idx = torch.empty((B, H, Lq, topk), dtype=torch.int32, device=device) if debug or cache else None
+    sc = torch.empty((B, H, Lq, topk), dtype=torch.float32, device=device) if debug or cache else None
     L = lib()
     nbytes = L.topk_attn_workspace_bytes(B, H, Lq, Lk, d, topk, chunk, int(causal), dt)
     if nbytes == 0:  # invalid arguments: let the call report why
         _raise(L.topk_attn(None, None, None, None, B, H, Lq, Lk, d, topk, chunk, int(causal), scale, dt, None))
     args = (q.data_ptr(), k.data_ptr(), v.data_ptr(), out.data_ptr(), B, H, Lq, Lk, d, topk, chunk, int(causal),
             float(scale), dt, _stream_ptr(device))
-    if debug:
-        _with_workspace(nbytes, device, lambda: L.topk_attn_debug(*args, idx.data_ptr(), sc.data_ptr()))
+    if debug or cache:
+        fn = L.topk_attn_debug if debug else L.topk_attn_with_cache
+        _with_workspace(nbytes, device, lambda: fn(*args, idx.data_ptr(), sc.data_ptr()))
         return out, idx, sc
     _with_workspace(nbytes, device, lambda: L.topk_attn(*args))
     return out
 
 
-def ffn(x, w1, w2, topk: int, chunk: int = 0, debug: bool = False):
-    """Top-k feed-forward layer: x [N, d_model], w1/w2 [d_ff, d_model] (row j = key/value j)."""
+def ffn(x, w1, w2, topk: int, chunk: int = 0, debug: bool = False, cache: bool = False):
+    """Top-k feed-forward layer: x [N, d_model], w1/w2 [d_ff, d_model] (row j = key/value j).
+    ``debug`` / ``cache`` as for ``attn``."""
     import torch
     device = x.device
     _check(x, "x", 2, x.dtype, device)
@@ -190,16 +197,17 @@ def ffn(x, w1, w2, topk: int, chunk: int = 0, debug: bool = False):
         raise ValueError(f"shape mismatch x {tuple(x.shape)} w1 {tuple(w1.shape)} w2 {tuple(w2.shape)}")
     dt = _dtype_code(x)
     out = torch.empty_like(x)
-    idx = torch.empty((N, topk), dtype=torch.int32, device=device) if debug else None
-    sc = torch.empty((N, topk), dtype=torch.float32, device=device) if debug else None
+    idx = torch.empty((N, topk), dtype=torch.int32, device=device) if debug or cache else None
+    sc = torch.empty((N, topk), dtype=torch.float32, device=device) if debug or cache else None
     L = lib()
     nbytes = L.topk_ffn_workspace_bytes(N, dm, dff, topk, chunk, dt)
     if nbytes == 0:
         _raise(L.topk_ffn(None, None, None, None, N, dm, dff, topk, chunk, dt, None))
     args = (x.data_ptr(), w1.data_ptr(), w2.data_ptr(), out.data_ptr(), N, dm, dff, topk, chunk, dt,
             _stream_ptr(device))
-    if debug:
-        _with_workspace(nbytes, device, lambda: L.topk_ffn_debug(*args, idx.data_ptr(), sc.data_ptr()))
+    if debug or cache:
+        fn = L.topk_ffn_debug if debug else L.topk_ffn_with_cache
+        _with_workspace(nbytes, device, lambda: fn(*args, idx.data_ptr(), sc.data_ptr()))
         return out, idx, sc
     _with_workspace(nbytes, device, lambda: L.topk_ffn(*args))
     return out

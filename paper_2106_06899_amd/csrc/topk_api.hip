@@ -188,7 +188,8 @@ PassBufs carve(const Problem& pb, const Plan& pl, char* ws) {
 }
 
 // ---------------------------------------------------------------- execution
-int run(Problem pb, hipStream_t st) {
+// report: read back the rows a fallback selected (waits for the stream; debug calls)
+int run(Problem pb, hipStream_t st, bool report) {
   Plan pl;
   choose_path(pb, &pl);
   size_t budget = g_ws ? g_ws_bytes : DEFAULT_BUDGET;
@@ -207,7 +208,7 @@ int run(Problem pb, hipStream_t st) {
   }
   hipError_t e = hipSuccess;
   int64_t fallback = 0;
-  if (pb.idx_out) g_fallback_rows = -1;
+  if (report) g_fallback_rows = -1;
   for (int64_t c0 = 0; c0 < pl.total_chunks && e == hipSuccess; c0 += pl.per_pass) {
     Pass ps;
     ps.c0 = c0;
@@ -243,14 +244,14 @@ int run(Problem pb, hipStream_t st) {
       StageTimer t(st, ST_FINAL);
       e = launch_finalize(pb, ps, b, st);
     }
-    if (e == hipSuccess && pb.idx_out) {  // debug calls report the fallback rows (synchronously)
+    if (e == hipSuccess && report) {  // debug calls report the fallback rows (synchronously)
       int32_t h = 0;
       e = hipMemcpyAsync(&h, b.redo_count, sizeof(h), hipMemcpyDeviceToHost, st);
       if (e == hipSuccess) e = hipStreamSynchronize(st);
       fallback += h;
     }
   }
-  if (pb.idx_out) g_fallback_rows = e == hipSuccess ? fallback : -1;
+  if (report) g_fallback_rows = e == hipSuccess ? fallback : -1;
   if (own) hipFreeAsync(ws, st);
   if (e != hipSuccess) return fail(TOPK_E_HIP, "kernel launch failed: %s", hipGetErrorString(e));
   return TOPK_OK;
@@ -444,7 +445,7 @@ int topk_attn_debug(const void* Q, const void* K, const void* V, void* out, int6
   int rc = attn_problem(&pb, Q, K, V, out, B, H, Lq, Lk, d, k, chunk, causal, scale, dtype, idx_out, score_out, true);
   if (rc) return rc;
   if ((rc = debug_ptrs(idx_out, score_out))) return rc;
-  return run(pb, (hipStream_t)hip_stream);
+  return run(pb, (hipStream_t)hip_stream, idx_out != nullptr || score_out != nullptr);
 }
 
 int topk_attn(const void* Q, const void* K, const void* V, void* out, int64_t B, int64_t H, int64_t Lq, int64_t Lk,
@@ -460,7 +461,31 @@ int topk_ffn_debug(const void* X, const void* W1, const void* W2, void* out, int
   int rc = ffn_problem(&pb, X, W1, W2, out, N, d_model, d_ff, k, chunk, dtype, idx_out, score_out, true);
   if (rc) return rc;
   if ((rc = debug_ptrs(idx_out, score_out))) return rc;
-  return run(pb, (hipStream_t)hip_stream);
+  return run(pb, (hipStream_t)hip_stream, idx_out != nullptr || score_out != nullptr);
+}
+
+int topk_attn_with_cache(const void* Q, const void* K, const void* V, void* out, int64_t B, int64_t H, int64_t Lq,
+                         int64_t Lk, int64_t d, int64_t k, int64_t chunk, int causal, float scale, int dtype,
+                         void* hip_stream, int32_t* top_idx, float* top_dots) {
+  g_err.clear();
+  if (!top_idx || !top_dots) return fail(TOPK_E_NULL, "top_idx and top_dots are required");
+  Problem pb;
+  int rc = attn_problem(&pb, Q, K, V, out, B, H, Lq, Lk, d, k, chunk, causal, scale, dtype, top_idx, top_dots, true);
+  if (rc) return rc;
+  if ((rc = debug_ptrs(top_idx, top_dots))) return rc;
+  return run(pb, (hipStream_t)hip_stream, false);
+}
+
+int topk_ffn_with_cache(const void* X, const void* W1, const void* W2, void* out, int64_t N, int64_t d_model,
+                        int64_t d_ff, int64_t k, int64_t chunk, int dtype, void* hip_stream, int32_t* top_idx,
+                        float* top_dots) {
+  g_err.clear();
+  if (!top_idx || !top_dots) return fail(TOPK_E_NULL, "top_idx and top_dots are required");
+  Problem pb;
+  int rc = ffn_problem(&pb, X, W1, W2, out, N, d_model, d_ff, k, chunk, dtype, top_idx, top_dots, true);
+  if (rc) return rc;
+  if ((rc = debug_ptrs(top_idx, top_dots))) return rc;
+  return run(pb, (hipStream_t)hip_stream, false);
 }
 
 int topk_ffn(const void* X, const void* W1, const void* W2, void* out, int64_t N, int64_t d_model, int64_t d_ff,
