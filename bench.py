@@ -163,6 +163,156 @@ def bench_backward(args, w, x, dev_tensor):
     print(json.dumps(rec), flush=True)
 
 
+def _timed(step, steps, warmup):
+    """Average ms of `steps` calls of step() after `warmup` untimed ones (synchronised)."""
+    import torch
+    for _ in range(warmup):
+        step()
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(steps):
+        step()
+    torch.cuda.synchronize()
+    return 1e3 * (time.perf_counter() - t0) / steps
+
+
+def bench_layer(args):
+    """The multi-head attention layer at BERT-base shape (d_model 768, 12 heads of 64),
+    causal, k = 128, chunk 1024 (the paper's single-layer benchmark setting), one JSON
+    line per sequence length: forward and forward + backward time per step, tokens/s,
+    the peak of PyTorch's allocator, and the library's per-stage times."""
+    import torch
+    import paper_2106_06899_amd as tk
+    from paper_2106_06899_amd import layers
+    dev = torch.device("cuda:0")
+    for L in (int(t) for t in args.lengths.split(",")):
+        torch.manual_seed(11)
+        layer = layers.TopkMultiheadAttention(768, 12, 128, 1024, causal=True, device=dev, dtype=torch.bfloat16)
+        x = torch.randn(1, L, 768, device=dev, dtype=torch.bfloat16).requires_grad_()
+        g = torch.randn(1, L, 768, device=dev, dtype=torch.bfloat16)
+
+        def fwd():
+            with torch.no_grad():
+                layer(x)
+
+        def train():
+            layer(x).backward(g)
+
+        torch.cuda.synchronize()
+        torch.cuda.reset_peak_memory_stats(dev)
+        ms_fwd = _timed(fwd, args.steps, args.warmup)
+        peak_fwd = torch.cuda.max_memory_allocated(dev)
+        torch.cuda.reset_peak_memory_stats(dev)
+        tk.profile_begin()
+        ms_train = _timed(train, args.steps, args.warmup)
+        st = tk.profile_end()
+        peak_train = torch.cuda.max_memory_allocated(dev)
+        n = args.steps + args.warmup
+        stages = {k_: round(v[0] / n, 4) for k_, v in st.items() if v[1]}
+        print(json.dumps({
+            "metric": "top-k multi-head attention layer tokens/s, forward + backward (BERT-base, causal, k=128, C=1024)",
+            "value": L / (ms_train / 1e3), "unit": "tokens/s", "n_gpus": 1, "steps": args.steps,
+            "warmup": args.warmup, "ms_per_step": ms_train, "ms_forward": ms_fwd, "higher_is_better": True,
+            "dtype": "bf16", "data": "synthetic (N(0,1) tokens, default-initialised projections)",
+            "config": {"workload": f"attention layer d_model 768, 12 heads x 64, causal, k 128, chunk 1024, L {L}",
+                       "batch": 1, "seq_len": L},
+            "peak_gib_forward": peak_fwd / 2**30, "peak_gib_train": peak_train / 2**30,
+            "library_stage_ms_per_step": stages}), flush=True)
+        del layer, x, g
+
+
+def bench_paper_ff(args):
+    """The feed-forward layer at the paper's benchmark shape: 2^18 tokens (batch 512 x
+    length 512), d_model 768, k = 512, query chunk 2^14, one JSON line per d_ff."""
+    import torch
+    import paper_2106_06899_amd as tk
+    from paper_2106_06899_amd import layers
+    dev = torch.device("cuda:0")
+    N, dm, k, C = 1 << 18, 768, 512, 1 << 14
+    gen = torch.Generator(device=dev).manual_seed(12)
+    x = torch.randn(N, dm, device=dev, dtype=torch.bfloat16, generator=gen).requires_grad_()
+    g = torch.randn(N, dm, device=dev, dtype=torch.bfloat16, generator=gen)
+    for dff in (int(t) for t in args.d_ff.split(",")):
+        w1 = (0.02 * torch.randn(dff, dm, device=dev, generator=gen)).to(torch.bfloat16).requires_grad_()
+        w2 = (0.02 * torch.randn(dff, dm, device=dev, generator=gen)).to(torch.bfloat16).requires_grad_()
+
+        def fwd():
+            with torch.no_grad():
+                tk.ffn(x, w1, w2, k, C)
+
+        def train():
+            layers.topk_feed_forward(x, w1, w2, k, C).backward(g)
+
+        torch.cuda.synchronize()
+        torch.cuda.reset_peak_memory_stats(dev)
+        tk.profile_begin()
+        ms_fwd = _timed(fwd, args.steps, args.warmup)
+        st_f = tk.profile_end()
+        peak_fwd = torch.cuda.max_memory_allocated(dev)
+        torch.cuda.reset_peak_memory_stats(dev)
+        tk.profile_begin()
+        ms_train = _timed(train, args.steps, args.warmup)
+        st = tk.profile_end()
+        peak_train = torch.cuda.max_memory_allocated(dev)
+        n = args.steps + args.warmup
+        score_ms = st_f["score"][0] / n
+        print(json.dumps({
+            "metric": "top-k feed-forward layer tokens/s, forward + backward (2^18 tokens, d_model 768, k=512, C=2^14)",
+            "value": N / (ms_train / 1e3), "unit": "tokens/s", "n_gpus": 1, "steps": args.steps,
+            "warmup": args.warmup, "ms_per_step": ms_train, "ms_forward": ms_fwd, "higher_is_better": True,
+            "dtype": "bf16", "data": "synthetic (X ~ N(0,1), W1, W2 ~ N(0, 0.02^2))",
+            "config": {"workload": f"feed-forward layer N 2^18, d_model 768, d_ff {dff}, k 512, chunk 2^14",
+                       "d_ff": dff},
+            "score_tflops": 2.0 * N * dff * dm / (score_ms / 1e3) / 1e12,
+            "forward_workspace_gib": tk.ffn_workspace_bytes(N, dm, dff, k, C) / 2**30,
+            "peak_gib_forward": peak_fwd / 2**30, "peak_gib_train": peak_train / 2**30,
+            "library_stage_ms_per_step": {k_: round(v[0] / n, 4) for k_, v in st.items() if v[1]}}), flush=True)
+        del w1, w2
+        x.grad = None
+
+
+def bench_chunk_sweep(args):
+    """Forward pass of one BERT-base multi-head self-attention layer (d_model 768, 12
+    heads of 64, bidirectional, k = 128) at L = 65536 for each query chunk size: time,
+    the peak of PyTorch's allocator (inputs, projections, outputs and the library's
+    workspace, which is a PyTorch tensor) and the workspace the library asks for."""
+    import torch
+    import paper_2106_06899_amd as tk
+    from paper_2106_06899_amd import layers
+    dev = torch.device("cuda:0")
+    L = args.sweep_length
+    torch.manual_seed(13)
+    x = torch.randn(1, L, 768, device=dev, dtype=torch.bfloat16)
+    for C, budget in ((int(t), b) for t in args.chunks.split(",") for b in (0, 1)):
+        torch.manual_seed(14)
+        layer = layers.TopkMultiheadAttention(768, 12, 128, C, causal=False, device=dev, dtype=torch.bfloat16)
+
+        def fwd():
+            with torch.no_grad():
+                layer(x)
+
+        tk.set_memory_budget(budget)  # 0: default budget; 1: one chunk in flight (sequential chunks)
+        torch.cuda.synchronize()
+        torch.cuda.reset_peak_memory_stats(dev)
+        tk.profile_begin()
+        ms = _timed(fwd, args.steps, args.warmup)
+        st = tk.profile_end()
+        ws = tk.attn_workspace_bytes(1, 12, L, L, 64, 128, C, False)
+        tk.set_memory_budget(0)
+        n = args.steps + args.warmup
+        print(json.dumps({
+            "metric": "top-k multi-head attention layer forward ms vs query chunk size (BERT-base, L 65536, k 128)",
+            "value": ms, "unit": "ms", "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
+            "ms_per_step": ms, "higher_is_better": False, "dtype": "bf16", "data": "synthetic",
+            "config": {"workload": f"attention layer d_model 768, 12 heads x 64, bidirectional, k 128, L {L}, chunk {C}",
+                       "chunk": C, "seq_len": L, "chunks_in_flight": "one (sequential)" if budget else "default budget",
+                       "path": tk.attn_path(1, 12, L, L, 64, 128, C, False, tk.TOPK_BF16)},
+            "peak_gib": torch.cuda.max_memory_allocated(dev) / 2**30,
+            "workspace_gib": ws / 2**30,
+            "library_stage_ms_per_step": {k_: round(v[0] / n, 4) for k_, v in st.items() if v[1]}}), flush=True)
+        del layer
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -177,6 +327,16 @@ def main():
                     help="write the scan's HBM bytes per launch from four rocprofv3 counter_collection.csv files")
     ap.add_argument("--copy-bytes", type=int, default=1 << 30)
     ap.add_argument("--traffic-command", default="")
+    ap.add_argument("--layer", action="store_true",
+                    help="time the multi-head attention layer (BERT-base shape, causal, k 128, chunk 1024)")
+    ap.add_argument("--lengths", default="4096,16384,65536", help="sequence lengths for --layer")
+    ap.add_argument("--chunk-sweep", action="store_true",
+                    help="forward of one BERT-base attention layer at L 65536, k 128, for each query chunk size")
+    ap.add_argument("--chunks", default="64,128,256,512,1024,2048,4096", help="chunk sizes for --chunk-sweep")
+    ap.add_argument("--sweep-length", type=int, default=65536)
+    ap.add_argument("--paper-ff", action="store_true",
+                    help="time the feed-forward layer at the paper's shape (2^18 tokens, d_model 768, k 512)")
+    ap.add_argument("--d-ff", default="2048,4096,8192,16384,32768,65536", help="d_ff values for --paper-ff")
     ap.add_argument("--backward", action="store_true",
                     help="time the backward pass (input checkpointing) instead of the forward")
     args = ap.parse_args()
@@ -196,6 +356,16 @@ def main():
         print(f"bench.py measures one GPU only (asked for {args.gpus}); there is no multi-GPU path.",
               file=sys.stderr)
         sys.exit(2)
+
+    if args.layer:
+        bench_layer(args)
+        return
+    if args.paper_ff:
+        bench_paper_ff(args)
+        return
+    if args.chunk_sweep:
+        bench_chunk_sweep(args)
+        return
 
     import torch
     import paper_2106_06899_amd as tk

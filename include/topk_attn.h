@@ -126,11 +126,12 @@ int topk_ffn_with_cache(const void* X, const void* W1, const void* W2, void* out
                         int32_t* top_idx, float* top_dots);
 
 /*
- * Workspace (bytes) a call with these arguments uses under the default memory
- * budget; 0 when the arguments are invalid. Register at least this much with
+ * Workspace (bytes) a call with these arguments uses under the memory budget;
+ * 0 when the arguments are invalid. Register at least this much with
  * topk_set_workspace() to run without library allocations. The budget caps the
  * number of query chunks in flight, so the figure is O(chunk) per chunk and
- * never exceeds the budget plus a fixed remainder.
+ * never exceeds the budget plus a fixed remainder (at least one chunk runs per
+ * pass whatever the budget).
  */
 size_t topk_attn_workspace_bytes(int64_t B, int64_t H, int64_t Lq, int64_t Lk, int64_t d,
                                  int64_t k, int64_t chunk, int causal, int dtype);
@@ -147,6 +148,15 @@ size_t topk_ffn_workspace_bytes(int64_t N, int64_t d_model, int64_t d_ff, int64_
  * 256-byte aligned.
  */
 int topk_set_workspace(void* dev_ptr, size_t bytes);
+
+/*
+ * The forward calls' memory budget, process-wide: the most workspace a call sizes
+ * for itself (the chunks of a call run in passes of as many chunks as fit; a
+ * budget below one chunk's needs runs one chunk per pass, the paper's sequential
+ * query chunking of Section 2.2). 0 restores the default of 8 GiB. A registered
+ * workspace (topk_set_workspace) takes the place of the budget. Returns TOPK_OK.
+ */
+int topk_set_memory_budget(size_t bytes);
 
 /* Message describing the calling thread's last non-OK return ("" if none). */
 const char* topk_last_error(void);

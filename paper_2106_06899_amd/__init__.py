@@ -20,7 +20,7 @@ import os
 
 __all__ = ["attn", "ffn", "attn_workspace_bytes", "ffn_workspace_bytes", "attn_path", "ffn_path",
            "mfma_layout", "lib", "TopkError", "LIB_PATH", "profile_begin", "profile_end", "STAGES",
-           "attn_backward", "ffn_backward", "set_backward_lists", "last_fallback_rows"]
+           "attn_backward", "ffn_backward", "set_backward_lists", "set_memory_budget", "last_fallback_rows"]
 
 LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libtopk.so")
 
@@ -64,6 +64,7 @@ def lib() -> ctypes.CDLL:
         "topk_last_error": ([], ctypes.c_char_p),
         "topk_last_fallback_rows": ([], i64),
         "topk_set_backward_lists": ([i32], i32),
+        "topk_set_memory_budget": ([ctypes.c_size_t], i32),
         "topk_attn_backward": ([vp] * 9 + [i64] * 6 + [ctypes.c_float, i32, vp], i32),
         "topk_ffn_backward": ([vp] * 9 + [i64] * 4 + [i32, vp], i32),
         "topk_attn_backward_workspace_bytes": ([i64] * 6 + [i32], ctypes.c_size_t),
@@ -286,6 +287,12 @@ def profile_end():
     n = (ctypes.c_int64 * len(STAGES))()
     _raise(lib().topk_profile_end(ms, n, len(STAGES)))
     return {s: (ms[i], n[i]) for i, s in enumerate(STAGES)}
+
+
+def set_memory_budget(nbytes: int) -> None:
+    """Most workspace a forward call sizes for itself (process-wide; 0 = 8 GiB). A small
+    budget runs the query chunks in more passes (one chunk per pass at the limit)."""
+    _raise(lib().topk_set_memory_budget(int(nbytes)))
 
 
 def set_backward_lists(mode: int) -> None:

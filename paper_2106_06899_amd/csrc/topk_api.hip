@@ -53,6 +53,7 @@ struct StageTimer {
 
 constexpr size_t ALIGN = 256;
 constexpr size_t DEFAULT_BUDGET = size_t(8) << 30;  // workspace cap when the library allocates
+size_t g_budget = DEFAULT_BUDGET;                    // process-wide, set by topk_set_memory_budget
 constexpr int64_t DEFAULT_CHUNK = 1024;
 constexpr int64_t FUSED_CAPH = 512;                   // candidates kept per (query, half-wave)
 
@@ -192,7 +193,7 @@ PassBufs carve(const Problem& pb, const Plan& pl, char* ws) {
 int run(Problem pb, hipStream_t st, bool report) {
   Plan pl;
   choose_path(pb, &pl);
-  size_t budget = g_ws ? g_ws_bytes : DEFAULT_BUDGET;
+  size_t budget = g_ws ? g_ws_bytes : g_budget;
   plan_sizes(pb, &pl, budget);
   const size_t need = plan_total(pl, pb);
   char* ws = (char*)g_ws;
@@ -327,7 +328,7 @@ int debug_ptrs(int32_t* idx_out, float* score_out) {
 size_t workspace_for(const Problem& pb) {
   Plan pl;
   choose_path(pb, &pl);
-  plan_sizes(pb, &pl, DEFAULT_BUDGET);
+  plan_sizes(pb, &pl, g_budget);
   return plan_total(pl, pb);
 }
 
@@ -557,6 +558,12 @@ size_t topk_ffn_backward_workspace_bytes(int64_t N, int64_t d_model, int64_t d_f
                   d_model, k, 0, 1.f, dtype, ACT_RELU, false))
     return 0;
   return bwd_bytes(bp);
+}
+
+int topk_set_memory_budget(size_t bytes) {
+  g_err.clear();
+  g_budget = bytes ? bytes : DEFAULT_BUDGET;
+  return TOPK_OK;
 }
 
 int topk_set_backward_lists(int mode) {

@@ -129,3 +129,21 @@ def test_backward_list_modes():
         assert L.topk_attn_backward_workspace_bytes(*big) > 0
     finally:
         tk.set_backward_lists(tk.TOPK_LISTS_AUTO)
+
+
+def test_memory_budget_bounds_the_workspace():
+    """The budget caps the workspace a call sizes for itself; at a budget below one
+    chunk's needs one chunk runs per pass, and 0 restores the default."""
+    L = tk.lib()
+    shape = (1, 4, 8192, 8192, 64, 64, 512, 0, 1)
+    default = L.topk_attn_workspace_bytes(*shape)
+    try:
+        tk.set_memory_budget(1)
+        one = L.topk_attn_workspace_bytes(*shape)
+        tk.set_memory_budget(64 << 20)
+        mid = L.topk_attn_workspace_bytes(*shape)
+        assert 0 < one < mid <= default
+        assert mid <= (64 << 20) + one  # the budget plus at most the fixed part
+    finally:
+        tk.set_memory_budget(0)
+    assert L.topk_attn_workspace_bytes(*shape) == default
