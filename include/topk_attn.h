@@ -164,8 +164,11 @@ const char* topk_last_error(void);
 /*
  * Which implementation the arguments select: 1 = fused score+filter path
  * (bf16 MFMA score tiles, candidates filtered on chip), 2 = chunk-tile path
- * (the chunk's score tile in workspace, then a row-wise select), or a negative
- * status for invalid arguments. For tests and reports.
+ * (the chunk's score tile in workspace, then a row-wise select), 3 = both, by rows
+ * (causal masks on the fused path: the first 1024 R rows of every head, whose few
+ * valid keys give the fused threshold sample too few blocks, run on the chunk-tile
+ * path; R = 3, 6, 12 for k <= 32, 64, 128), or a negative status for invalid
+ * arguments. For tests and reports.
  */
 int topk_attn_path(int64_t B, int64_t H, int64_t Lq, int64_t Lk, int64_t d,
                    int64_t k, int64_t chunk, int causal, int dtype);

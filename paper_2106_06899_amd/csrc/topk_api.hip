@@ -108,11 +108,15 @@ int order_stat_for(int64_t k) { return k <= 32 ? 3 : (k <= 64 ? 6 : 12); }
 void choose_path(const Problem& pb, Plan* pl) {
   pl->path = PATH_TILE;
   pl->scan = {MODE_ALL, 16, 8, 2};
+  if (pb.tile_only) return;
   // 64 queries per wave: measured faster than 128 once the filter runs (the LDS
   // staging, not the K operand reads, bounds the scan)
   const int groups = 2;
-  const bool shape_ok = pb.dtype == T_BF16 && !pb.causal && (pb.d == 64 || pb.d == 128) && pb.k <= 128 &&
-                        pb.Lk < (int64_t(1) << 25);
+  // Causal rows (Eq. 2) take the fused path only when the keys are long against k:
+  // short rows have so few keys per selected one that most score blocks would
+  // beat the threshold and the on-chip filter would stage nearly all of them.
+  const bool shape_ok = pb.dtype == T_BF16 && (pb.d == 64 || pb.d == 128) && pb.k <= 128 &&
+                        pb.Lk < (int64_t(1) << 25) && (!pb.causal || pb.Lk >= 256 * pb.k);
   if (!shape_ok) return;
   if (pb.Lk <= 2 * FUSED_CAPH) {  // every key fits the candidate buffers
     pl->path = PATH_FUSED;
@@ -141,7 +145,7 @@ size_t row_bytes(const Problem& pb, const Plan& pl) {
 }
 
 void plan_sizes(const Problem& pb, Plan* pl, size_t budget) {
-  pl->nchunk = (pb.Lq + pb.C - 1) / pb.C;
+  pl->nchunk = (pb.q1 - pb.q0 + pb.C - 1) / pb.C;
   pl->total_chunks = pb.BH * pl->nchunk;
   pl->per_chunk = row_bytes(pb, *pl) * (size_t)pb.C + 6 * ALIGN;
   pl->fixed = 2 * ALIGN + (pl->path == PATH_FUSED ? up((size_t)(REDO_CAP + REDO_BLOCKS) * pb.Lk * 4) : 0);
@@ -188,14 +192,38 @@ PassBufs carve(const Problem& pb, const Plan& pl, char* ws) {
   return b;
 }
 
-// ---------------------------------------------------------------- execution
-// report: read back the rows a fallback selected (waits for the stream; debug calls)
-int run(Problem pb, hipStream_t st, bool report) {
+// Causal rows on the fused path: a row needs at least 2R valid sampled blocks per
+// half-wave for its 1-in-16 threshold sample, i.e. i + 1 >= 1024 R valid keys. The
+// first 1024 R rows of every head therefore run on the chunk-tile path, the rest
+// fused. Each row's path, and so its result, does not depend on the chunk size.
+int split_rows(const Problem& pb, Problem* parts) {
+  parts[0] = pb;
   Plan pl;
   choose_path(pb, &pl);
-  size_t budget = g_ws ? g_ws_bytes : g_budget;
-  plan_sizes(pb, &pl, budget);
-  const size_t need = plan_total(pl, pb);
+  if (!pb.causal || pl.path != PATH_FUSED || pl.scan.mode != MODE_SAMPLE) return 1;
+  const int64_t T = 1024 * (int64_t)pl.scan.R;
+  if (T <= pb.q0) return 1;
+  parts[0].q1 = pb.q1 < T ? pb.q1 : T;
+  parts[0].tile_only = 1;
+  if (T >= pb.q1) return 1;
+  parts[1] = pb;
+  parts[1].q0 = T;
+  return 2;
+}
+
+// ---------------------------------------------------------------- execution
+// report: read back the rows a fallback selected (waits for the stream; debug calls)
+int run(Problem whole, hipStream_t st, bool report) {
+  Problem parts[2];
+  Plan plans[2];
+  const int np = split_rows(whole, parts);
+  size_t budget = g_ws ? g_ws_bytes : g_budget, need = 0;
+  for (int q = 0; q < np; ++q) {
+    choose_path(parts[q], &plans[q]);
+    plan_sizes(parts[q], &plans[q], budget);
+    const size_t n = plan_total(plans[q], parts[q]);
+    need = n > need ? n : need;
+  }
   char* ws = (char*)g_ws;
   bool own = false;
   if (g_ws) {
@@ -210,7 +238,10 @@ int run(Problem pb, hipStream_t st, bool report) {
   hipError_t e = hipSuccess;
   int64_t fallback = 0;
   if (report) g_fallback_rows = -1;
-  for (int64_t c0 = 0; c0 < pl.total_chunks && e == hipSuccess; c0 += pl.per_pass) {
+  for (int q = 0; q < np; ++q)
+  for (int64_t c0 = 0; c0 < plans[q].total_chunks && e == hipSuccess; c0 += plans[q].per_pass) {
+    const Problem& pb = parts[q];
+    const Plan& pl = plans[q];
     Pass ps;
     ps.c0 = c0;
     ps.nc = pl.total_chunks - c0 < pl.per_pass ? pl.total_chunks - c0 : pl.per_pass;
@@ -275,6 +306,9 @@ int attn_problem(Problem* pb, const void* Q, const void* K, const void* V, void*
   pb->out = out;
   pb->BH = B * H;
   pb->Lq = Lq;
+  pb->q0 = 0;
+  pb->q1 = Lq;
+  pb->tile_only = 0;
   pb->Lk = Lk;
   pb->d = d;
   pb->k = k;
@@ -305,6 +339,9 @@ int ffn_problem(Problem* pb, const void* X, const void* W1, const void* W2, void
   pb->out = out;
   pb->BH = 1;
   pb->Lq = N;
+  pb->q0 = 0;
+  pb->q1 = N;
+  pb->tile_only = 0;
   pb->Lk = d_ff;
   pb->d = d_model;
   pb->k = k;
@@ -325,11 +362,18 @@ int debug_ptrs(int32_t* idx_out, float* score_out) {
   return TOPK_OK;
 }
 
-size_t workspace_for(const Problem& pb) {
-  Plan pl;
-  choose_path(pb, &pl);
-  plan_sizes(pb, &pl, g_budget);
-  return plan_total(pl, pb);
+size_t workspace_for(const Problem& whole) {
+  Problem parts[2];
+  const int np = split_rows(whole, parts);
+  size_t need = 0;
+  for (int q = 0; q < np; ++q) {
+    Plan pl;
+    choose_path(parts[q], &pl);
+    plan_sizes(parts[q], &pl, g_budget);
+    const size_t n = plan_total(pl, parts[q]);
+    need = n > need ? n : need;
+  }
+  return need;
 }
 
 // ---------------------------------------------------------------- backward
@@ -584,8 +628,10 @@ int topk_attn_path(int64_t B, int64_t H, int64_t Lq, int64_t Lk, int64_t d, int6
   int rc = attn_problem(&pb, nullptr, nullptr, nullptr, nullptr, B, H, Lq, Lk, d, k, chunk, causal, 1.f, dtype,
                         nullptr, nullptr, false);
   if (rc) return rc;
+  Problem parts[2];
+  if (split_rows(pb, parts) == 2) return 3;
   Plan pl;
-  choose_path(pb, &pl);
+  choose_path(parts[0], &pl);
   return pl.path;
 }
 

@@ -28,7 +28,9 @@ struct Problem {
   const void* K;
   const void* V;
   void* out;
-  int64_t BH, Lq, Lk, d, k, C;   // C = query chunk size
+  int64_t BH, Lq, Lk, d, k, C;   // C = query chunk size; Lq = query rows per head in memory
+  int64_t q0, q1;                // the rows this problem processes: [q0, q1) of every head
+  int tile_only;                 // run on the chunk-tile path whatever the shape
   int64_t kv_head_stride;
   int causal;
   float scale;
@@ -39,7 +41,7 @@ struct Problem {
 };
 
 // A pass covers chunk ids [c0, c0 + nc); chunk id = bh * nchunk + c covers query
-// rows [c*C, min((c+1)*C, Lq)) of head bh. Pass-local row p = (id - c0) * C + r.
+// rows [q0 + c*C, min(q0 + (c+1)*C, q1)) of head bh. Pass-local row p = (id - c0) * C + r.
 struct Pass {
   int64_t c0, nc, nchunk;
 };

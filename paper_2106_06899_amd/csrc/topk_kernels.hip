@@ -75,8 +75,8 @@ __device__ __forceinline__ RowRef row_of(const Problem& pb, const Pass& ps, int6
   int64_t id = ps.c0 + chunk_local;
   RowRef rr;
   rr.bh = id / ps.nchunk;
-  rr.i = (id - rr.bh * ps.nchunk) * pb.C + r;
-  rr.ok = chunk_local < ps.nc && rr.i < pb.Lq;
+  rr.i = pb.q0 + (id - rr.bh * ps.nchunk) * pb.C + r;
+  rr.ok = chunk_local < ps.nc && rr.i < pb.q1;
   return rr;
 }
 __device__ __forceinline__ int64_t valid_keys(const Problem& pb, int64_t i) {
@@ -214,8 +214,8 @@ __global__ __launch_bounds__(256) void k_tile_scores(Problem pb, Pass ps, float*
   __shared__ float ks[16][65];
   const int tid = threadIdx.x, tx = tid & 15, ty = tid >> 4;
   const int64_t key0 = (int64_t)blockIdx.x * 64, r0 = (int64_t)blockIdx.y * 64, cl = blockIdx.z;
-  const int64_t id = ps.c0 + cl, bh = id / ps.nchunk, c = id - bh * ps.nchunk, i0 = c * pb.C;
-  if (r0 >= pb.C || i0 + r0 >= pb.Lq) return;
+  const int64_t id = ps.c0 + cl, bh = id / ps.nchunk, c = id - bh * ps.nchunk, i0 = pb.q0 + c * pb.C;
+  if (r0 >= pb.C || i0 + r0 >= pb.q1) return;
   if (pb.causal) {
     int64_t last = r0 + 63 < pb.C ? r0 + 63 : pb.C - 1;
     if (key0 > i0 + last) return;  // tile entirely above the diagonal: never read
@@ -228,7 +228,7 @@ __global__ __launch_bounds__(256) void k_tile_scores(Problem pb, Pass ps, float*
     for (int m = 0; m < 4; ++m) {
       const int e = tid + 256 * m, rr = e >> 4, cc = e & 15;
       const int64_t lr = r0 + rr, i = i0 + lr, key = key0 + rr, f = d0 + cc;
-      qs[cc][rr] = (lr < pb.C && i < pb.Lq && f < d) ? load_elem<T>(pb.Q, (bh * pb.Lq + i) * d + f) : 0.f;
+      qs[cc][rr] = (lr < pb.C && i < pb.q1 && f < d) ? load_elem<T>(pb.Q, (bh * pb.Lq + i) * d + f) : 0.f;
       ks[cc][rr] = (key < pb.Lk && f < d) ? load_elem<T>(Kh, key * d + f) : 0.f;
     }
     __syncthreads();
@@ -250,7 +250,7 @@ __global__ __launch_bounds__(256) void k_tile_scores(Problem pb, Pass ps, float*
 #pragma unroll
   for (int a = 0; a < 4; ++a) {
     const int64_t lr = r0 + ty * 4 + a, i = i0 + lr;
-    if (lr >= pb.C || i >= pb.Lq) continue;
+    if (lr >= pb.C || i >= pb.q1) continue;
     const int64_t nv = valid_keys(pb, i);
 #pragma unroll
     for (int b = 0; b < 4; ++b) {
@@ -290,8 +290,8 @@ __global__ __launch_bounds__(256, 2) void k_tile_scores_mfma(Problem pb, Pass ps
   const int64_t nq = (pb.C + TQ - 1) / TQ, nk = (pb.Lk + TK - 1) / TK;
   const int64_t qt = wg % nq, kt = (wg / nq) % nk, cl = wg / (nq * nk);
   const int64_t key0 = kt * TK, r0 = qt * TQ;
-  const int64_t id = ps.c0 + cl, bh = id / ps.nchunk, c = id - bh * ps.nchunk, i0 = c * pb.C;
-  if (r0 >= pb.C || i0 + r0 >= pb.Lq) return;
+  const int64_t id = ps.c0 + cl, bh = id / ps.nchunk, c = id - bh * ps.nchunk, i0 = pb.q0 + c * pb.C;
+  if (r0 >= pb.C || i0 + r0 >= pb.q1) return;
   if (pb.causal) {
     const int64_t last = r0 + TQ - 1 < pb.C ? r0 + TQ - 1 : pb.C - 1;
     if (key0 > i0 + last) return;
@@ -306,7 +306,7 @@ __global__ __launch_bounds__(256, 2) void k_tile_scores_mfma(Problem pb, Pass ps
     for (int j = 0; j < QLPW; ++j) {
       const int cidx = (wave * QLPW + j) * 64 + lane, r = cidx >> 2, p = (cidx & 3) ^ ((r >> 1) & 3);
       const int64_t lr = r0 + r, i = i0 + lr;
-      const int64_t qi = (lr < pb.C && i < pb.Lq) ? i : i0 + r0;
+      const int64_t qi = (lr < pb.C && i < pb.q1) ? i : i0 + r0;
       __builtin_amdgcn_global_load_lds((const void*)(Qb + (bh * pb.Lq + qi) * d + f0 + p * 8),
                                        (__attribute__((address_space(3))) void*)&sm[buf][(wave * QLPW + j) * 1024],
                                        16, 0, 0);
@@ -358,7 +358,7 @@ __global__ __launch_bounds__(256, 2) void k_tile_scores_mfma(Problem pb, Pass ps
 #pragma unroll
   for (int a = 0; a < 2; ++a) {
     const int64_t lr = r0 + wq + a * 32 + n, i = i0 + lr;
-    if (lr >= pb.C || i >= pb.Lq) continue;
+    if (lr >= pb.C || i >= pb.q1) continue;
     const int64_t nv = valid_keys(pb, i);
     float* srow = S + (cl * pb.C + lr) * pb.Lk;
 #pragma unroll
@@ -554,12 +554,13 @@ __global__ __launch_bounds__(256) void k_tile_select(Problem pb, Pass ps, const 
 struct ScanArgs {
   const uint16_t* Q;
   const uint16_t* K;
-  int64_t Lq, Lk, C, kv_head_stride;
+  int64_t Lq, Lk, C, kv_head_stride;  // Lq: query rows per head in memory
+  int64_t q0, q1;                     // rows processed: [q0, q1) of every head
   int64_t c0, nchunk, wgs_per_chunk;
   uint64_t* cand;
   int32_t* cnt;
   int64_t caph;
-  int mode, stride;
+  int mode, stride, causal;
 };
 
 constexpr int SCAN_KT = 64;  // keys per K tile
@@ -609,9 +610,16 @@ __global__ __launch_bounds__(256, ScanShape<G>::OCC) void k_fused_scan(ScanArgs 
   const int64_t cl = wg / a.wgs_per_chunk, blk = wg - cl * a.wgs_per_chunk;
   const int64_t id = a.c0 + cl, bh = id / a.nchunk, c = id - bh * a.nchunk;
   const uint16_t* Kh = a.K + bh * a.kv_head_stride;
-  const int64_t ntiles = (a.Lk + KT - 1) / KT;
-  const bool tail = ntiles * KT != a.Lk;
+  // the workgroup's first and last query (index in the head); under the causal mask
+  // (Eq. 2) its key tiles end at the one holding its last query
+  const int64_t q_first = a.q0 + c * a.C + blk * QB;
+  int64_t q_last = a.q0 + c * a.C + (blk * QB + QB < a.C ? blk * QB + QB : a.C) - 1;
+  q_last = q_last < a.q1 - 1 ? q_last : a.q1 - 1;
+  const int64_t ntiles_all = (a.Lk + KT - 1) / KT;
+  const int64_t ntiles = a.causal && q_last / KT + 1 < ntiles_all ? q_last / KT + 1 : ntiles_all;
+  const bool tail = ntiles * KT > a.Lk;
   const int64_t wave_row0 = cl * a.C + blk * QB + wave * 32 * G;  // pass-local row of the wave's query 0
+  const int64_t wave_q0 = q_first + wave * 32 * G;                 // the wave's first query
 
   bool ok[G];
   bf16x8 b[G][NS];
@@ -619,8 +627,8 @@ __global__ __launch_bounds__(256, ScanShape<G>::OCC) void k_fused_scan(ScanArgs 
     const bf16x8 zero8 = {};
 #pragma unroll
     for (int g = 0; g < G; ++g) {
-      const int64_t local = blk * QB + wave * 32 * G + g * 32 + n, i = c * a.C + local;
-      ok[g] = local < a.C && i < a.Lq;
+      const int64_t local = blk * QB + wave * 32 * G + g * 32 + n, i = a.q0 + c * a.C + local;
+      ok[g] = local < a.C && i < a.q1;
       const uint16_t* q = a.Q + (bh * a.Lq + (ok[g] ? i : 0)) * D + (D / 2) * half;
 #pragma unroll
       for (int s = 0; s < NS; ++s) b[g][s] = ok[g] ? *(const bf16x8*)(q + 8 * s) : zero8;
@@ -681,6 +689,19 @@ __global__ __launch_bounds__(256, ScanShape<G>::OCC) void k_fused_scan(ScanArgs 
     for (int v = 0; v < 16; ++v)
       if (jb + 8 * (v >> 2) + (v & 3) >= a.Lk) acc[v] = -INFINITY;
   };
+  // causal mask: keys j > i of this lane's queries -> -inf (jb: the lane's first key
+  // of the block); only blocks reaching past the wave's first query need it
+  auto mask_future = [&](f32x16 (&acc)[G], int64_t t, int rb) {
+    if (!a.causal || t * KT + rb * 32 + 31 <= wave_q0) return;
+    const int64_t jb = t * KT + rb * 32 + 4 * half;
+#pragma unroll
+    for (int g = 0; g < G; ++g) {
+      const int64_t i = wave_q0 + g * 32 + n;
+#pragma unroll
+      for (int v = 0; v < 16; ++v)
+        if (jb + 8 * (v >> 2) + (v & 3) > i) acc[g][v] = -INFINITY;
+    }
+  };
   auto block_max = [&](const f32x16& acc) {
     float m = acc[0];
 #pragma unroll
@@ -691,6 +712,9 @@ __global__ __launch_bounds__(256, ScanShape<G>::OCC) void k_fused_scan(ScanArgs 
   float tau[G];
 #pragma unroll
   for (int g = 0; g < G; ++g) tau[g] = -INFINITY;
+  // Causal rows sample the same 1-in-stride tiles; the masked (future) keys of a
+  // sampled tile give -inf block maxima, so a row's threshold depends on the row
+  // alone. The host sends only rows with enough valid sampled blocks this way.
   if (a.mode == MODE_SAMPLE) {
     float top[G][R];
 #pragma unroll
@@ -716,6 +740,7 @@ __global__ __launch_bounds__(256, ScanShape<G>::OCC) void k_fused_scan(ScanArgs 
 #pragma unroll
           for (int g = 0; g < G; ++g) mask_keys(acc[g], jb);
         }
+        mask_future(acc, t, rb);
 #pragma unroll
         for (int g = 0; g < G; ++g) insert(top[g], block_max(acc[g]));
       }
@@ -849,6 +874,7 @@ __global__ __launch_bounds__(256, ScanShape<G>::OCC) void k_fused_scan(ScanArgs 
 #pragma unroll
         for (int g = 0; g < G; ++g) mask_keys(acc[g], jb);
       }
+      mask_future(acc, t, rb);
     };
     for (int i = 0; i < SCAN_NB - 1 && i < ntiles; ++i) issue(i, i);
     open_tile(0);
@@ -1505,6 +1531,8 @@ hipError_t launch_fused_scan(const Problem& pb, const Pass& ps, const PassBufs& 
   a.Q = (const uint16_t*)pb.Q;
   a.K = (const uint16_t*)pb.K;
   a.Lq = pb.Lq;
+  a.q0 = pb.q0;
+  a.q1 = pb.q1;
   a.Lk = pb.Lk;
   a.C = pb.C;
   a.kv_head_stride = pb.kv_head_stride;
@@ -1515,6 +1543,7 @@ hipError_t launch_fused_scan(const Problem& pb, const Pass& ps, const PassBufs& 
   a.caph = b.caph;
   a.mode = cfg.mode;
   a.stride = cfg.stride;
+  a.causal = pb.causal ? 1 : 0;
   const int G = cfg.groups;
   a.wgs_per_chunk = (pb.C + 128 * G - 1) / (128 * G);
   const unsigned grid = (unsigned)(ps.nc * a.wgs_per_chunk);

@@ -147,3 +147,14 @@ def test_memory_budget_bounds_the_workspace():
     finally:
         tk.set_memory_budget(0)
     assert L.topk_attn_workspace_bytes(*shape) == default
+
+
+def test_causal_split_path():
+    """Causal masks with long keys take the fused path for rows from 1024 R on and the
+    chunk-tile path below (reported as 3); short keys stay on the chunk-tile path."""
+    assert tk.attn_path(1, 12, 65536, 65536, 64, 128, 1024, True, tk.TOPK_BF16) == 3
+    assert tk.attn_path(1, 1, 4500, 4500, 64, 16, 512, True, tk.TOPK_BF16) == 3
+    assert tk.attn_path(1, 1, 3000, 4500, 64, 16, 512, True, tk.TOPK_BF16) == 2  # every row below 1024 R
+    assert tk.attn_path(4, 16, 8192, 8192, 128, 128, 1024, True, tk.TOPK_BF16) == 2  # Lk < 256 k
+    assert tk.attn_path(1, 1, 4500, 4500, 64, 16, 512, True, tk.TOPK_F32) == 2
+    assert tk.attn_workspace_bytes(1, 12, 65536, 65536, 64, 128, 1024, True) > 0

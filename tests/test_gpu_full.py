@@ -46,6 +46,26 @@ def test_attn_full_size(name):
         assert kept > 0.8
 
 
+def test_attn_causal_layer_shape_full_size():
+    """The causal attention of the layer benchmark at its longest length: 12 heads of
+    64, L 65536, k 128, chunk 1024 (rows below 12288 on the chunk-tile path, the rest
+    fused), sampled rows of both parts against the oracle."""
+    w = wl.WORKLOADS["c4"].scaled(B=1, H=12, Lq=65536, Lk=65536, d=64, k=128, chunk=1024,
+                                  scale=float(np.float32(0.125)))
+    assert tk.attn_path(w.B, w.H, w.Lq, w.Lk, w.d, w.k, w.chunk, True, tk.TOPK_BF16) == 3
+    _say("causal 12x65536", w)
+    x = wl.make_inputs(w)
+    out, idx, sc = parity.run_attn(w, x)
+    rows = parity.sample_attn_rows(w, 120, seed=7)
+    rep = {"fallback_rows": tk.last_fallback_rows()}
+    parity.check_attn(w, x, out, idx, rows=rows, report=rep)
+    _say("causal 12x65536 sampled rows ok", rep)
+    g = idx.cpu().numpy()
+    k_eff = np.minimum(w.k, np.arange(w.Lq) + 1)
+    assert np.array_equal((g >= 0).sum(-1), np.broadcast_to(k_eff, g.shape[:-1]))
+    assert np.all(g <= np.arange(w.Lq)[:, None]), "a causal row selected a future key"
+
+
 def test_ffn_full_size():
     w = wl.WORKLOADS["c5"]
     _say("c5", w.note)

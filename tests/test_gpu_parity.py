@@ -64,6 +64,12 @@ ATTN_CASES = {
     # case whose rows cross 1024 keys
     "tile_long_rows": ("c2", dict(B=1, H=1, Lq=40, Lk=9500, d=96, k=300, chunk=40)),
     "c4_causal_long": ("c4", dict(B=1, H=1, Lq=2100, Lk=2100, chunk=1024)),
+    # causal masks with Lk >= 256 k: rows below 1024 R on the chunk-tile path, the
+    # rest on the fused path (path 3)
+    "c3_causal_fused_k16": ("c3", dict(H=2, Lq=4500, Lk=4500, k=16, chunk=512, causal=True)),
+    "c4_d128_causal_fused": ("c4", dict(B=1, H=1, Lq=8300, Lk=8300, k=32, chunk=1024)),
+    "causal_fused_lq_below_lk": ("c3", dict(H=1, Lq=4000, Lk=8000, k=16, chunk=256, causal=True)),
+    "causal_fused_lq_above_lk": ("c3", dict(H=1, Lq=6000, Lk=4200, k=16, chunk=1000, causal=True)),
 }
 
 
@@ -153,6 +159,7 @@ def test_k_equals_Lk_is_vanilla_attention(base, kw):
     ("c3", dict(H=1, Lq=300, Lk=9000)),
     ("c4", dict(B=1, H=1, Lq=300, Lk=300)),
     ("c1", dict(Lq=200, Lk=300)),
+    ("c3", dict(H=1, Lq=4200, Lk=4200, k=16, causal=True)),
 ])
 def test_chunking_does_not_change_the_result(base, kw):
     """Query chunking is result-neutral: bit-identical outputs and indices for every C."""
