@@ -581,7 +581,7 @@ template <int G>
 constexpr int scan_queries_per_wg() { return 4 * 32 * G; }
 
 
-template <int D, int R, int G>
+template <int D, int R, int G, bool CAUSAL>
 __global__ __launch_bounds__(256, ScanShape<G>::OCC) void k_fused_scan(ScanArgs a) {
   static_assert(ScanShape<G>::CAP >= 128, "a ring holds one block's 64 lanes, both halves");
   constexpr int SCAN_NB = ScanShape<G>::NB;
@@ -616,7 +616,7 @@ __global__ __launch_bounds__(256, ScanShape<G>::OCC) void k_fused_scan(ScanArgs 
   int64_t q_last = a.q0 + c * a.C + (blk * QB + QB < a.C ? blk * QB + QB : a.C) - 1;
   q_last = q_last < a.q1 - 1 ? q_last : a.q1 - 1;
   const int64_t ntiles_all = (a.Lk + KT - 1) / KT;
-  const int64_t ntiles = a.causal && q_last / KT + 1 < ntiles_all ? q_last / KT + 1 : ntiles_all;
+  const int64_t ntiles = CAUSAL && q_last / KT + 1 < ntiles_all ? q_last / KT + 1 : ntiles_all;
   const bool tail = ntiles * KT > a.Lk;
   const int64_t wave_row0 = cl * a.C + blk * QB + wave * 32 * G;  // pass-local row of the wave's query 0
   const int64_t wave_q0 = q_first + wave * 32 * G;                 // the wave's first query
@@ -689,17 +689,19 @@ __global__ __launch_bounds__(256, ScanShape<G>::OCC) void k_fused_scan(ScanArgs 
     for (int v = 0; v < 16; ++v)
       if (jb + 8 * (v >> 2) + (v & 3) >= a.Lk) acc[v] = -INFINITY;
   };
-  // causal mask: keys j > i of this lane's queries -> -inf (jb: the lane's first key
-  // of the block); only blocks reaching past the wave's first query need it
+  // causal mask: keys j > i of this lane's queries -> -inf; only blocks reaching past
+  // the wave's first query need it (offsets within 32-bit range: the block starts
+  // at most 63 keys past that query)
   auto mask_future = [&](f32x16 (&acc)[G], int64_t t, int rb) {
-    if (!a.causal || t * KT + rb * 32 + 31 <= wave_q0) return;
-    const int64_t jb = t * KT + rb * 32 + 4 * half;
+    if (!CAUSAL) return;
+    const int64_t j0 = t * KT + rb * 32;
+    if (j0 + 31 <= wave_q0) return;
 #pragma unroll
     for (int g = 0; g < G; ++g) {
-      const int64_t i = wave_q0 + g * 32 + n;
+      const int room = (int)(wave_q0 - j0) + g * 32 + n - 4 * half;  // i - (lane's first key)
 #pragma unroll
       for (int v = 0; v < 16; ++v)
-        if (jb + 8 * (v >> 2) + (v & 3) > i) acc[g][v] = -INFINITY;
+        if (8 * (v >> 2) + (v & 3) > room) acc[g][v] = -INFINITY;
     }
   };
   auto block_max = [&](const f32x16& acc) {
@@ -1545,17 +1547,20 @@ hipError_t launch_fused_scan(const Problem& pb, const Pass& ps, const PassBufs& 
   a.stride = cfg.stride;
   a.causal = pb.causal ? 1 : 0;
   const int G = cfg.groups;
+  const bool causal = pb.causal != 0;
   a.wgs_per_chunk = (pb.C + 128 * G - 1) / (128 * G);
   const unsigned grid = (unsigned)(ps.nc * a.wgs_per_chunk);
-#define TOPK_SCAN(D_, G_)                                                 \
-  do {                                                                    \
-    if (cfg.R == 3) k_fused_scan<D_, 3, G_><<<grid, 256, 0, st>>>(a);     \
-    else if (cfg.R == 6) k_fused_scan<D_, 6, G_><<<grid, 256, 0, st>>>(a); \
-    else k_fused_scan<D_, 12, G_><<<grid, 256, 0, st>>>(a);               \
+#define TOPK_SCAN(D_, G_, C_)                                                 \
+  do {                                                                        \
+    if (cfg.R == 3) k_fused_scan<D_, 3, G_, C_><<<grid, 256, 0, st>>>(a);     \
+    else if (cfg.R == 6) k_fused_scan<D_, 6, G_, C_><<<grid, 256, 0, st>>>(a); \
+    else k_fused_scan<D_, 12, G_, C_><<<grid, 256, 0, st>>>(a);               \
   } while (0)
   if (G != 2) return hipErrorInvalidValue;
-  if (pb.d == 64) TOPK_SCAN(64, 2);
-  else TOPK_SCAN(128, 2);
+  if (pb.d == 64 && !causal) TOPK_SCAN(64, 2, false);
+  else if (pb.d == 64) TOPK_SCAN(64, 2, true);
+  else if (!causal) TOPK_SCAN(128, 2, false);
+  else TOPK_SCAN(128, 2, true);
 #undef TOPK_SCAN
   return hipGetLastError();
 }
