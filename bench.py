@@ -440,9 +440,9 @@ def main():
         "data": "synthetic",
         "config": {"workload": f"{w.name}: {w.note}", "B": w.B, "H": w.H, "Lq": w.Lq, "Lk": w.Lk, "d": w.d,
                    "k": w.k, "chunk": w.chunk, "causal": w.causal, "scale": w.scale,
-                   "path": {1: "fused", 2: "chunk-tile", 3: "chunk-tile rows below 1024 R, fused above"}.get(path, path)} if w.kind == "attn" else
+                   "path": {1: "fused", 2: "chunk-tile", 3: "chunk-tile rows below 1024 R, fused above", 4: "filtered chunk-tile"}.get(path, path)} if w.kind == "attn" else
                   {"workload": f"{w.name}: {w.note}", "N": w.N, "d_model": w.d_model, "d_ff": w.d_ff, "k": w.k,
-                   "chunk": w.chunk, "path": {1: "fused", 2: "chunk-tile", 3: "chunk-tile rows below 1024 R, fused above"}.get(path, path)},
+                   "chunk": w.chunk, "path": {1: "fused", 2: "chunk-tile", 3: "chunk-tile rows below 1024 R, fused above", 4: "filtered chunk-tile"}.get(path, path)},
         "score_tflops_whole_call": score_tflops_call,
         "score_frac_of_bf16_peak_whole_call": score_tflops_call / PEAK_BF16_TFLOPS,
         "stage_ms_per_step": {s: stages[s][0] / args.steps for s in stages},

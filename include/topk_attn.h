@@ -167,7 +167,10 @@ const char* topk_last_error(void);
  * (the chunk's score tile in workspace, then a row-wise select), 3 = both, by rows
  * (causal masks on the fused path: the first 1024 R rows of every head, whose few
  * valid keys give the fused threshold sample too few blocks, run on the chunk-tile
- * path; R = 3, 6, 12 for k <= 32, 64, 128), or a negative status for invalid
+ * path; R = 3, 6, 12 for k <= 32, 64, 128), 4 = filtered chunk-tile path (bf16,
+ * d % 32 == 0, k <= 256, 2048 < Lk <= 16384: every 16th key is scored first, each
+ * row's threshold comes from those samples, and the tile GEMM keeps only the scores
+ * at or above it; the rest as the fused path), or a negative status for invalid
  * arguments. For tests and reports.
  */
 int topk_attn_path(int64_t B, int64_t H, int64_t Lq, int64_t Lk, int64_t d,

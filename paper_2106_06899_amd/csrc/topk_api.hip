@@ -69,7 +69,7 @@ int fail(int code, const char* fmt, ...) {
 
 size_t up(size_t x) { return (x + ALIGN - 1) / ALIGN * ALIGN; }
 
-enum Path { PATH_FUSED = 1, PATH_TILE = 2 };
+enum Path { PATH_FUSED = 1, PATH_TILE = 2, PATH_FILTER = 4 };
 
 struct Plan {
   int path;
@@ -105,10 +105,21 @@ int validate_shape(int64_t BH_a, int64_t BH_b, int64_t Lq, int64_t Lk, int64_t d
 // ---------------------------------------------------------------- planning
 int order_stat_for(int64_t k) { return k <= 32 ? 3 : (k <= 64 ? 6 : 12); }
 
+// Filtered chunk-tile path: bf16 MFMA tiles (d % 32 == 0) whose rows are long
+// enough for a sampled threshold and short enough for 1024 samples, k <= 256 (its
+// candidates, about 16 R per row, stay within the 1024 the select holds).
+bool filter_ok(const Problem& pb) {
+  return pb.dtype == T_BF16 && pb.d % 32 == 0 && pb.d <= 1024 && pb.k <= 256 && pb.Lk > 2048 &&
+         pb.Lk <= FILTER_MAX_LK;
+}
+
 void choose_path(const Problem& pb, Plan* pl) {
   pl->path = PATH_TILE;
   pl->scan = {MODE_ALL, 16, 8, 2};
-  if (pb.tile_only) return;
+  if (pb.tile_only) {
+    if (filter_ok(pb)) pl->path = PATH_FILTER;
+    return;
+  }
   // 64 queries per wave: measured faster than 128 once the filter runs (the LDS
   // staging, not the K operand reads, bounds the scan)
   const int groups = 2;
@@ -117,7 +128,10 @@ void choose_path(const Problem& pb, Plan* pl) {
   // beat the threshold and the on-chip filter would stage nearly all of them.
   const bool shape_ok = pb.dtype == T_BF16 && (pb.d == 64 || pb.d == 128) && pb.k <= 128 &&
                         pb.Lk < (int64_t(1) << 25) && (!pb.causal || pb.Lk >= 256 * pb.k);
-  if (!shape_ok) return;
+  if (!shape_ok) {
+    if (filter_ok(pb)) pl->path = PATH_FILTER;
+    return;
+  }
   if (pb.Lk <= 2 * FUSED_CAPH) {  // every key fits the candidate buffers
     pl->path = PATH_FUSED;
     pl->scan = {MODE_ALL, 16, order_stat_for(pb.k), groups};
@@ -132,6 +146,8 @@ void choose_path(const Problem& pb, Plan* pl) {
   if (sampled_tiles * (kt / 32) >= 2 * R) {
     pl->path = PATH_FUSED;
     pl->scan = {MODE_SAMPLE, 16, R, groups};
+  } else if (filter_ok(pb)) {
+    pl->path = PATH_FILTER;
   }
 }
 
@@ -141,6 +157,7 @@ size_t row_bytes(const Problem& pb, const Plan& pl) {
     b += (size_t)pb.Lk * 4;
   else
     b += 2 * FUSED_CAPH * 8 + 8;
+  if (pl.path == PATH_FILTER) b += (size_t)((pb.Lk + FILTER_KSTRIDE - 1) / FILTER_KSTRIDE) * 4 + 4;
   return b;
 }
 
@@ -148,7 +165,7 @@ void plan_sizes(const Problem& pb, Plan* pl, size_t budget) {
   pl->nchunk = (pb.q1 - pb.q0 + pb.C - 1) / pb.C;
   pl->total_chunks = pb.BH * pl->nchunk;
   pl->per_chunk = row_bytes(pb, *pl) * (size_t)pb.C + 6 * ALIGN;
-  pl->fixed = 2 * ALIGN + (pl->path == PATH_FUSED ? up((size_t)(REDO_CAP + REDO_BLOCKS) * pb.Lk * 4) : 0);
+  pl->fixed = 2 * ALIGN + (pl->path != PATH_TILE ? up((size_t)(REDO_CAP + REDO_BLOCKS) * pb.Lk * 4) : 0);
   int64_t n = 1;
   if (budget > pl->fixed + pl->per_chunk) n = (int64_t)((budget - pl->fixed) / pl->per_chunk);
   if (n > pl->total_chunks) n = pl->total_chunks;
@@ -188,6 +205,13 @@ PassBufs carve(const Problem& pb, const Plan& pl, char* ws) {
     off += up(rows * 8);
     b.scores = (float*)(ws + off);
     off += up((size_t)(REDO_CAP + REDO_BLOCKS) * pb.Lk * 4);
+    if (pl.path == PATH_FILTER) {
+      b.cand_single = 1;
+      b.samp = (float*)(ws + off);
+      off += up(rows * (size_t)((pb.Lk + FILTER_KSTRIDE - 1) / FILTER_KSTRIDE) * 4);
+      b.thr = (float*)(ws + off);
+      off += up(rows * 4);
+    }
   }
   return b;
 }
@@ -247,7 +271,24 @@ int run(Problem whole, hipStream_t st, bool report) {
     ps.nc = pl.total_chunks - c0 < pl.per_pass ? pl.total_chunks - c0 : pl.per_pass;
     ps.nchunk = pl.nchunk;
     PassBufs b = carve(pb, pl, ws);
-    if (pl.path == PATH_TILE) {
+    if (pl.path == PATH_FILTER) {
+      if (e == hipSuccess) e = launch_init(b, st);
+      if (e == hipSuccess) e = launch_filter(pb, ps, b, 0, st);
+      if (e == hipSuccess) {
+        StageTimer t(st, ST_SCORE);
+        e = launch_filter(pb, ps, b, 1, st);
+        if (e == hipSuccess) e = launch_filter(pb, ps, b, 2, st);
+        if (e == hipSuccess) e = launch_filter(pb, ps, b, 3, st);
+      }
+      if (e == hipSuccess) {
+        StageTimer t(st, ST_SELECT);
+        e = launch_cand_select(pb, ps, b, st);
+      }
+      if (e == hipSuccess) {
+        StageTimer t(st, ST_REDO);
+        e = launch_redo(pb, ps, b, st);
+      }
+    } else if (pl.path == PATH_TILE) {
       if (e == hipSuccess) e = launch_init(b, st);
       if (e == hipSuccess) {
         StageTimer t(st, ST_SCORE);

@@ -46,15 +46,24 @@ struct Pass {
   int64_t c0, nc, nchunk;
 };
 
+// Filtered chunk-tile path: every FILTER_KSTRIDE-th key is scored first; the R-th
+// largest of a row's valid samples is its threshold, and the tile GEMM keeps only
+// scores at or above it.
+constexpr int FILTER_KSTRIDE = 16;
+constexpr int64_t FILTER_MAX_LK = 16384;  // at most 1024 samples per row
+
 // Workspace pointers of one pass.
 struct PassBufs {
   uint64_t* sel;      // [rows, k] selected keys, (score desc, index asc); 0 pads
   int32_t* redo_list; // [rows]
   int32_t* redo_count;
   float* scores;      // chunk-tile path: [rows, Lk]; fused path: redo rows [REDO_CAP + REDO_BLOCKS, Lk]
-  uint64_t* cand;     // fused path: [rows, 2, caph]
-  int32_t* cnt;       // fused path: [rows, 2]
+  uint64_t* cand;     // fused and filtered paths: [rows, 2, caph]
+  int32_t* cnt;       // fused and filtered paths: [rows, 2]
   int64_t caph;
+  int cand_single;    // filtered path: one list of up to 2 caph per row, its length in cnt[2p]
+  float* samp;        // filtered path: [rows, ceil(Lk / FILTER_KSTRIDE)] sampled scores
+  float* thr;         // filtered path: [rows] thresholds
 };
 
 struct ScanCfg {
@@ -136,5 +145,6 @@ struct BwdBufs {
 };
 
 hipError_t launch_backward(const BwdProblem& bp, const BwdBufs& b, hipStream_t st);
+hipError_t launch_filter(const Problem& pb, const Pass& ps, const PassBufs& b, int stage, hipStream_t st);
 
 }  // namespace topk

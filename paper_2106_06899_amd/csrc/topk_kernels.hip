@@ -272,10 +272,15 @@ __global__ __launch_bounds__(256) void k_tile_scores(Problem pb, Pass ps, float*
 // and lane l holds keys 8*(v/4) + 4*(l/32) + v%4 of a block for query l % 32,
 // four consecutive keys of one score row per 16-byte store. Tiles entirely above
 // the causal diagonal are skipped (never read by the select).
+// MODE 0 writes the tile; MODE 1 scores every FILTER_KSTRIDE-th key only (the
+// filtered path's sample, "keys" of the grid are sample slots); MODE 2 appends the
+// scores at or above each row's threshold to the row's candidate list instead of
+// writing the tile.
 constexpr int TSM_TQ = 128, TSM_TK = 256;
 
-template <int DUMMY>
-__global__ __launch_bounds__(256, 2) void k_tile_scores_mfma(Problem pb, Pass ps, float* S) {
+template <int MODE>
+__global__ __launch_bounds__(256, 2) void k_tile_scores_mfma(Problem pb, Pass ps, PassBufs bufs) {
+  constexpr int64_t KSTEP = MODE == 1 ? FILTER_KSTRIDE : 1;  // key index of grid key slot s: s * KSTEP
   constexpr int TQ = TSM_TQ, TK = TSM_TK, KS = 32;  // tile rows, tile keys, features per slice
   constexpr int QBYTES = TQ * KS * 2, KBYTES = TK * KS * 2;
   constexpr int QLPW = QBYTES / 1024 / 4, KLPW = KBYTES / 1024 / 4;  // 1 KB loads per wave
@@ -287,14 +292,15 @@ __global__ __launch_bounds__(256, 2) void k_tile_scores_mfma(Problem pb, Pass ps
   // Q stays in L2 while K streams past once per chunk.
   const int64_t NG = gridDim.x, bid = blockIdx.x;
   const int64_t wg = (NG % 8 == 0) ? (bid % 8) * (NG / 8) + bid / 8 : bid;
-  const int64_t nq = (pb.C + TQ - 1) / TQ, nk = (pb.Lk + TK - 1) / TK;
+  const int64_t Lslots = (pb.Lk + KSTEP - 1) / KSTEP;  // key slots of the grid
+  const int64_t nq = (pb.C + TQ - 1) / TQ, nk = (Lslots + TK - 1) / TK;
   const int64_t qt = wg % nq, kt = (wg / nq) % nk, cl = wg / (nq * nk);
   const int64_t key0 = kt * TK, r0 = qt * TQ;
   const int64_t id = ps.c0 + cl, bh = id / ps.nchunk, c = id - bh * ps.nchunk, i0 = pb.q0 + c * pb.C;
   if (r0 >= pb.C || i0 + r0 >= pb.q1) return;
   if (pb.causal) {
     const int64_t last = r0 + TQ - 1 < pb.C ? r0 + TQ - 1 : pb.C - 1;
-    if (key0 > i0 + last) return;
+    if (key0 * KSTEP > i0 + last) return;
   }
   const int64_t d = pb.d;
   const uint16_t* Qb = (const uint16_t*)pb.Q;
@@ -314,7 +320,7 @@ __global__ __launch_bounds__(256, 2) void k_tile_scores_mfma(Problem pb, Pass ps
 #pragma unroll
     for (int j = 0; j < KLPW; ++j) {
       const int cidx = (wave * KLPW + j) * 64 + lane, r = cidx >> 2, p = (cidx & 3) ^ ((r >> 1) & 3);
-      int64_t key = key0 + r;
+      int64_t key = (key0 + r) * KSTEP;
       key = key < pb.Lk ? key : pb.Lk - 1;
       __builtin_amdgcn_global_load_lds(
           (const void*)(Kh + key * d + f0 + p * 8),
@@ -354,13 +360,84 @@ __global__ __launch_bounds__(256, 2) void k_tile_scores_mfma(Problem pb, Pass ps
     }
   }
   // D[m][n]: m = key 8*(v/4) + 4*half + v%4 of block b, n = query lane%32 of block a
-  const bool vec = (pb.Lk & 3) == 0;  // rows start 16-byte aligned
+  if (MODE == 2) {
+    // candidates: count this lane's passing scores per row, reserve room per row in
+    // LDS, then once per row and workgroup in the row's global list
+    uint32_t* rc = (uint32_t*)&sm[0][0];
+    __syncthreads();  // every wave is done with the operand buffers
+    if (tid < TQ) rc[tid] = 0;
+    __syncthreads();
+    uint32_t off[2];
+    uint32_t pass[2][4];  // bit v: score v of block (a, b) is a candidate
+    // keys of this wave's sub-tile all valid for every row of the tile (no causal
+    // diagonal, no tail): the per-key test can go
+    const int64_t kend = key0 + wk + 128;
+    const bool all_valid = kend <= pb.Lk && (!pb.causal || kend <= i0 + r0 + 1);
+#pragma unroll
+    for (int a = 0; a < 2; ++a) {
+      const int64_t lr = r0 + wq + a * 32 + n, i = i0 + lr;
+      const bool okr = lr < pb.C && i < pb.q1;
+      const int64_t nv = okr ? valid_keys(pb, i) : 0;
+      const float ts = okr ? bufs.thr[cl * pb.C + lr] : INFINITY;
+      uint32_t c = 0;
+#pragma unroll
+      for (int b = 0; b < 4; ++b) {
+        uint32_t m = 0;
+        if (all_valid) {
+#pragma unroll
+          for (int v = 0; v < 16; ++v) m |= (acc[a][b][v] >= ts ? 1u : 0u) << v;
+        } else {
+          const int64_t kb = key0 + wk + b * 32 + 4 * half;
+#pragma unroll
+          for (int v = 0; v < 16; ++v)
+            m |= (kb + 8 * (v >> 2) + (v & 3) < nv && acc[a][b][v] >= ts ? 1u : 0u) << v;
+        }
+        pass[a][b] = m;
+        c += (uint32_t)__builtin_popcount(m);
+      }
+      off[a] = c ? atomicAdd(&rc[wq + a * 32 + n], c) : 0u;
+    }
+    __syncthreads();
+    if (tid < TQ) {
+      const int64_t lr = r0 + tid, i = i0 + lr;
+      const uint32_t total = rc[tid];
+      rc[tid] = (total && lr < pb.C && i < pb.q1)
+                    ? (uint32_t)atomicAdd(&bufs.cnt[2 * (cl * pb.C + lr)], (int32_t)total) : 0u;
+    }
+    __syncthreads();
+    const uint32_t cap = 2u * (uint32_t)bufs.caph;
+#pragma unroll
+    for (int a = 0; a < 2; ++a) {
+      const int64_t lr = r0 + wq + a * 32 + n;
+      uint32_t pos = rc[wq + a * 32 + n] + off[a];
+      uint64_t* dst = bufs.cand + 2 * (cl * pb.C + lr) * bufs.caph;
+#pragma unroll
+      for (int b = 0; b < 4; ++b) {
+        const uint32_t kb = (uint32_t)(key0 + wk + b * 32 + 4 * half);
+        // scores of this block as a list of set bits: the wave loops as often as its
+        // busiest lane (the score is picked by a select over the 16 registers)
+        for (uint32_t m = pass[a][b]; m; m &= m - 1) {
+          const uint32_t v = (uint32_t)__builtin_ctz(m);
+          float x = acc[a][b][0];
+#pragma unroll
+          for (int u = 1; u < 16; ++u) x = v == (uint32_t)u ? acc[a][b][u] : x;
+          if (pos < cap)
+            dst[pos] = ((uint64_t)__float_as_uint(x) << 32) | (uint64_t)(0xFFFFFFFFu - (kb + 8 * (v >> 2) + (v & 3)));
+          ++pos;
+        }
+      }
+    }
+    return;
+  }
+  float* S = MODE == 1 ? bufs.samp : bufs.scores;
+  const int64_t rowlen = MODE == 1 ? Lslots : pb.Lk;
+  const bool vec = (rowlen & 3) == 0;  // rows start 16-byte aligned
 #pragma unroll
   for (int a = 0; a < 2; ++a) {
     const int64_t lr = r0 + wq + a * 32 + n, i = i0 + lr;
     if (lr >= pb.C || i >= pb.q1) continue;
-    const int64_t nv = valid_keys(pb, i);
-    float* srow = S + (cl * pb.C + lr) * pb.Lk;
+    const int64_t nv = (valid_keys(pb, i) + KSTEP - 1) / KSTEP;  // valid key slots
+    float* srow = S + (cl * pb.C + lr) * rowlen;
 #pragma unroll
     for (int b = 0; b < 4; ++b) {
 #pragma unroll
@@ -1083,7 +1160,11 @@ __device__ __forceinline__ void cand_select_row(const Problem& pb, const Pass& p
   if (!rr.ok) return;
   const int64_t nv = valid_keys(pb, rr.i);
   const uint32_t k_eff = (uint32_t)(pb.k < nv ? pb.k : nv);
-  const int64_t c0 = bufs.cnt[2 * p], c1 = bufs.cnt[2 * p + 1];
+  int64_t c0 = bufs.cnt[2 * p], c1 = bufs.cnt[2 * p + 1];
+  if (bufs.cand_single) {  // one list of c0 entries running on into the second half
+    c1 = c0 > bufs.caph ? c0 - bufs.caph : 0;
+    c0 = c0 > bufs.caph ? bufs.caph : c0;
+  }
   if (c0 > bufs.caph || c1 > bufs.caph || c0 + c1 < (int64_t)k_eff || k_eff > 256 ||
       c0 + c1 > 64 * CAND_REGS) {
     if ((threadIdx.x & 63) == 0) bufs.redo_list[atomicAdd(bufs.redo_count, 1)] = (int32_t)p;
@@ -1102,6 +1183,75 @@ __global__ __launch_bounds__(64) void k_cand_select(Problem pb, Pass ps, PassBuf
   __shared__ uint64_t sbuf[256];
   __shared__ uint32_t hist[256];
   cand_select_row(pb, ps, bufs, blockIdx.x, sbuf, hist);
+}
+
+// ------------------------------------------------------------------ filtered chunk-tile path
+// Per row, the threshold is the R-th largest of its valid sampled scores (every
+// FILTER_KSTRIDE-th key), R a few standard deviations above the sample's expected
+// share mu of the top k_eff. About R * FILTER_KSTRIDE scores of the row are then at
+// or above it; a row with fewer than R valid samples keeps every valid key. The
+// candidate select proves each row's set complete (at least k_eff entries, no
+// overflow) or sends the row to the exact fallback.
+__global__ __launch_bounds__(64) void k_filter_threshold(Problem pb, Pass ps, PassBufs bufs) {
+  __shared__ uint32_t hist[256];
+  const int64_t p = blockIdx.x;
+  const RowRef rr = row_of(pb, ps, p);
+  if (!rr.ok) return;
+  const int lane = threadIdx.x & 63;
+  const int64_t nv = valid_keys(pb, rr.i);
+  const int64_t ns = (nv + FILTER_KSTRIDE - 1) / FILTER_KSTRIDE;  // valid samples (<= 64 * CAND_REGS)
+  const uint32_t k_eff = (uint32_t)(pb.k < nv ? pb.k : nv);
+  const float mu = (float)k_eff * (float)ns / (float)nv;
+  const int R = (int)ceilf(mu + 4.0f * sqrtf(mu) + 4.0f);
+  float ts = -INFINITY;
+  if (R < ns) {
+    const float* row = bufs.samp + p * ((pb.Lk + FILTER_KSTRIDE - 1) / FILTER_KSTRIDE);
+    auto rth = [&](auto tag) {  // the R-th largest of the row's ns samples
+      constexpr int E = decltype(tag)::value;
+      uint64_t key[E];
+#pragma unroll
+      for (int e = 0; e < E; ++e) {
+        const int64_t s = lane + 64 * e;
+        key[e] = s < ns ? make_key(row[s], (uint32_t)s) : 0ull;
+      }
+      int shift;
+      uint64_t prefix;
+      wave_radix_select<E>(key, (int)ns, (uint32_t)R, hist, &shift, &prefix);
+      uint32_t m = 0xFFFFFFFFu;
+#pragma unroll
+      for (int e = 0; e < E; ++e)
+        if (lane + 64 * e < ns && (key[e] >> shift) >= (prefix >> shift)) m = min(m, (uint32_t)(key[e] >> 32));
+      for (int off = 32; off > 0; off >>= 1) m = min(m, (uint32_t)__shfl_xor(m, off, 64));
+      return ord_to_f32(m);
+    };
+    if (ns <= 128) ts = rth(std::integral_constant<int, 2>{});
+    else if (ns <= 256) ts = rth(std::integral_constant<int, 4>{});
+    else if (ns <= 512) ts = rth(std::integral_constant<int, 8>{});
+    else ts = rth(std::integral_constant<int, CAND_REGS>{});
+  }
+  if (lane == 0) bufs.thr[p] = ts;
+}
+
+__global__ void k_zero_counts(int32_t* p, int64_t n) {
+  for (int64_t e = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; e < n; e += (int64_t)gridDim.x * blockDim.x)
+    p[e] = 0;
+}
+
+// stage 0: zero the candidate counts; 1: sampled scores; 2: thresholds; 3: filtered tile
+hipError_t launch_filter(const Problem& pb, const Pass& ps, const PassBufs& b, int stage, hipStream_t st) {
+  const int64_t rows = ps.nc * pb.C;
+  if (stage == 0) {
+    k_zero_counts<<<1024, 256, 0, st>>>(b.cnt, 2 * rows);
+  } else if (stage == 1 || stage == 3) {
+    const int64_t slots = stage == 1 ? (pb.Lk + FILTER_KSTRIDE - 1) / FILTER_KSTRIDE : pb.Lk;
+    const int64_t g = ((slots + TSM_TK - 1) / TSM_TK) * ((pb.C + TSM_TQ - 1) / TSM_TQ) * ps.nc;
+    if (g > 0x7FFFFFFF || pb.dtype != T_BF16 || pb.d % 32 != 0 || pb.Lk > FILTER_MAX_LK) return hipErrorInvalidValue;
+    if (stage == 1) k_tile_scores_mfma<1><<<(unsigned)g, 256, 0, st>>>(pb, ps, b);
+    else k_tile_scores_mfma<2><<<(unsigned)g, 256, 0, st>>>(pb, ps, b);
+  } else {
+    k_filter_threshold<<<(unsigned)rows, 64, 0, st>>>(pb, ps, b);
+  }
+  return hipGetLastError();
 }
 
 // ------------------------------------------------------------------ chunk-tile path: short-row select
@@ -1504,7 +1654,7 @@ hipError_t launch_tile_scores(const Problem& pb, const Pass& ps, const PassBufs&
   if (pb.dtype == T_BF16 && pb.d % 32 == 0) {
     const int64_t g = ((pb.Lk + TSM_TK - 1) / TSM_TK) * ((pb.C + TSM_TQ - 1) / TSM_TQ) * ps.nc;
     if (g > 0x7FFFFFFF) return hipErrorInvalidValue;
-    k_tile_scores_mfma<0><<<(unsigned)g, 256, 0, st>>>(pb, ps, b.scores);
+    k_tile_scores_mfma<0><<<(unsigned)g, 256, 0, st>>>(pb, ps, b);
     return hipGetLastError();
   }
   dim3 grid((unsigned)((pb.Lk + 63) / 64), (unsigned)((pb.C + 63) / 64), (unsigned)ps.nc);

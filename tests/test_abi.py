@@ -71,11 +71,11 @@ def test_set_workspace_validation():
 
 def test_path_choice_for_the_five_workloads():
     # c1 fp32 -> chunk-tile; c2 short rows -> fused (every key a candidate);
-    # c3 long rows -> fused (sampled threshold); c4 causal -> chunk-tile; c5 FFN d_model 1024 -> chunk-tile
+    # c3 long rows -> fused (sampled threshold); c4 causal -> filtered chunk-tile; c5 FFN k 512 -> chunk-tile
     assert tk.attn_path(1, 1, 1024, 1024, 64, 32, 256, False, tk.TOPK_F32) == 2
     assert tk.attn_path(8, 12, 512, 512, 64, 64, 512, False, tk.TOPK_BF16) == 1
     assert tk.attn_path(1, 16, 32768, 32768, 64, 64, 1024, False, tk.TOPK_BF16) == 1
-    assert tk.attn_path(4, 16, 8192, 8192, 128, 128, 1024, True, tk.TOPK_BF16) == 2
+    assert tk.attn_path(4, 16, 8192, 8192, 128, 128, 1024, True, tk.TOPK_BF16) == 4
     assert tk.ffn_path(16384, 1024, 65536, 512, 1024, tk.TOPK_BF16) == 2
     assert tk.attn_path(1, 1, 10, 10, 64, 0) == E_INVAL
 
@@ -154,7 +154,7 @@ def test_causal_split_path():
     chunk-tile path below (reported as 3); short keys stay on the chunk-tile path."""
     assert tk.attn_path(1, 12, 65536, 65536, 64, 128, 1024, True, tk.TOPK_BF16) == 3
     assert tk.attn_path(1, 1, 4500, 4500, 64, 16, 512, True, tk.TOPK_BF16) == 3
-    assert tk.attn_path(1, 1, 3000, 4500, 64, 16, 512, True, tk.TOPK_BF16) == 2  # every row below 1024 R
-    assert tk.attn_path(4, 16, 8192, 8192, 128, 128, 1024, True, tk.TOPK_BF16) == 2  # Lk < 256 k
+    assert tk.attn_path(1, 1, 3000, 4500, 64, 16, 512, True, tk.TOPK_BF16) == 4  # every row below 1024 R: filtered tiles
+    assert tk.attn_path(4, 16, 8192, 8192, 128, 128, 1024, True, tk.TOPK_BF16) == 4  # Lk < 256 k: filtered tiles
     assert tk.attn_path(1, 1, 4500, 4500, 64, 16, 512, True, tk.TOPK_F32) == 2
     assert tk.attn_workspace_bytes(1, 12, 65536, 65536, 64, 128, 1024, True) > 0

@@ -59,7 +59,7 @@ ATTN_CASES = {
     # chunk-tile short-row select past 1024 keys: exact sampled rank (R > 96) and
     # the per-lane top-two threshold (R <= 96)
     "tile_sampled_exact_rank": ("c2", dict(B=1, H=1, Lq=90, Lk=1500, d=96, k=128, chunk=64)),
-    "tile_sampled_top_two": ("c2", dict(B=1, H=1, Lq=90, Lk=6000, d=96, k=64, chunk=64)),
+    "tile_sampled_top_two": ("c2", dict(B=1, H=1, Lq=90, Lk=6000, d=96, k=64, chunk=64, dtype=wl.F32)),
     # chunk-tile long-row select (workgroup per row, sampled blocks) and a causal
     # case whose rows cross 1024 keys
     "tile_long_rows": ("c2", dict(B=1, H=1, Lq=40, Lk=9500, d=96, k=300, chunk=40)),
@@ -70,6 +70,11 @@ ATTN_CASES = {
     "c4_d128_causal_fused": ("c4", dict(B=1, H=1, Lq=8300, Lk=8300, k=32, chunk=1024)),
     "causal_fused_lq_below_lk": ("c3", dict(H=1, Lq=4000, Lk=8000, k=16, chunk=256, causal=True)),
     "causal_fused_lq_above_lk": ("c3", dict(H=1, Lq=6000, Lk=4200, k=16, chunk=1000, causal=True)),
+    # filtered chunk-tile path (path 4): sampled thresholds, the tile GEMM keeps only
+    # scores at or above them
+    "filter_causal_d128_k128": ("c4", dict(B=1, H=2, Lq=3000, Lk=3000, chunk=512)),
+    "filter_d96_k200": ("c2", dict(B=1, H=1, Lq=300, Lk=12000, d=96, k=200, chunk=128)),
+    "filter_d32_k7_ragged": ("c2", dict(B=2, H=1, Lq=333, Lk=2601, d=32, k=7, chunk=100)),
 }
 
 
@@ -160,6 +165,7 @@ def test_k_equals_Lk_is_vanilla_attention(base, kw):
     ("c4", dict(B=1, H=1, Lq=300, Lk=300)),
     ("c1", dict(Lq=200, Lk=300)),
     ("c3", dict(H=1, Lq=4200, Lk=4200, k=16, causal=True)),
+    ("c4", dict(B=1, H=1, Lq=2500, Lk=2500)),
 ])
 def test_chunking_does_not_change_the_result(base, kw):
     """Query chunking is result-neutral: bit-identical outputs and indices for every C."""
@@ -282,7 +288,7 @@ def test_tile_short_row_fallback():
     """Only 100 of the 1024 sampled keys score high (the rest of the sample lowest),
     so the per-lane top-two threshold keeps about 76 < k keys: every row goes to the
     short-row select's fallback list."""
-    w = wl.WORKLOADS["c2"].scaled(B=1, H=1, Lq=120, Lk=4000, d=96, k=128, chunk=64)
+    w = wl.WORKLOADS["c2"].scaled(B=1, H=1, Lq=120, Lk=2000, d=96, k=128, chunk=64)
     assert tk.attn_path(w.B, w.H, w.Lq, w.Lk, w.d, w.k, w.chunk, w.causal, tk.TOPK_BF16) == 2
     alpha = np.full(w.Lk, 3.0)
     pos = (np.arange(1024) * w.Lk) // 1024
@@ -295,11 +301,26 @@ def test_tile_short_row_fallback():
     parity.check_attn(w, x, out, idx)
 
 
+def test_filter_fallback_for_every_row():
+    """Filtered chunk-tile path: every 16th key (the sampled ones) scores high, the rest
+    lower, so each row's threshold keeps only about R < k keys: every row is
+    recomputed by the fallback kernels, more rows than the first fallback kernel
+    takes (1024)."""
+    w = wl.WORKLOADS["c4"].scaled(B=1, H=1, Lq=1200, Lk=4000, causal=False, chunk=512)
+    assert tk.attn_path(w.B, w.H, w.Lq, w.Lk, w.d, w.k, w.chunk, w.causal, tk.TOPK_BF16) == 4
+    alpha = np.where(np.arange(w.Lk) % 16 == 0, 10.0, 3.0)
+    _say("filter fallback", w)
+    x = _planted(w, alpha, 10)
+    out, idx, _ = parity.run_attn(w, x)
+    assert tk.last_fallback_rows() == w.Lq
+    parity.check_attn(w, x, out, idx)
+
+
 def test_tile_long_row_fallback():
     """Rows over 8192 keys: 30 of the 1024 sampled keys score high, the rest of the
     sample lowest; the threshold (24th sampled key) keeps 24 < k keys, and the row is
     selected by the multi-pass radix select from the tile row."""
-    w = wl.WORKLOADS["c2"].scaled(B=1, H=1, Lq=60, Lk=9000, d=96, k=32, chunk=64)
+    w = wl.WORKLOADS["c2"].scaled(B=1, H=1, Lq=60, Lk=17000, d=96, k=32, chunk=64)
     assert tk.attn_path(w.B, w.H, w.Lq, w.Lk, w.d, w.k, w.chunk, w.causal, tk.TOPK_BF16) == 2
     alpha = np.full(w.Lk, 3.0)
     s = np.arange(1024)
