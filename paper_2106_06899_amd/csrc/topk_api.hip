@@ -106,12 +106,15 @@ int validate_shape(int64_t BH_a, int64_t BH_b, int64_t Lq, int64_t Lk, int64_t d
 int order_stat_for(int64_t k) { return k <= 32 ? 3 : (k <= 64 ? 6 : 12); }
 
 // Filtered chunk-tile path: bf16 MFMA tiles (d % 32 == 0) whose rows are long
-// enough for a sampled threshold and short enough for 1024 samples, k <= 256 (its
-// candidates, about 16 R per row, stay within the 1024 the select holds).
+// enough for a sampled threshold and at most 4096 samples, k <= 512 (its
+// candidates, about 16 R per row, stay within the 1024 the select holds for
+// k <= 256, within 2048 for larger k).
 bool filter_ok(const Problem& pb) {
-  return pb.dtype == T_BF16 && pb.d % 32 == 0 && pb.d <= 1024 && pb.k <= 256 && pb.Lk > 2048 &&
+  return pb.dtype == T_BF16 && pb.d % 32 == 0 && pb.d <= 1024 && pb.k <= 512 && pb.Lk > 2048 &&
          pb.Lk <= FILTER_MAX_LK;
 }
+// candidates kept per (row, half) of the list buffers
+int64_t caph_for(const Problem& pb, int path) { return path == PATH_FILTER && pb.k > 256 ? 2 * FUSED_CAPH : FUSED_CAPH; }
 
 void choose_path(const Problem& pb, Plan* pl) {
   pl->path = PATH_TILE;
@@ -156,7 +159,7 @@ size_t row_bytes(const Problem& pb, const Plan& pl) {
   if (pl.path == PATH_TILE)
     b += (size_t)pb.Lk * 4;
   else
-    b += 2 * FUSED_CAPH * 8 + 8;
+    b += 2 * (size_t)caph_for(pb, pl.path) * 8 + 8;
   if (pl.path == PATH_FILTER) b += (size_t)((pb.Lk + FILTER_KSTRIDE - 1) / FILTER_KSTRIDE) * 4 + 4;
   return b;
 }
@@ -198,9 +201,9 @@ PassBufs carve(const Problem& pb, const Plan& pl, char* ws) {
     b.scores = (float*)(ws + off);
     off += up(rows * (size_t)pb.Lk * 4);
   } else {
-    b.caph = FUSED_CAPH;
+    b.caph = caph_for(pb, pl.path);
     b.cand = (uint64_t*)(ws + off);
-    off += up(rows * 2 * FUSED_CAPH * 8);
+    off += up(rows * 2 * (size_t)b.caph * 8);
     b.cnt = (int32_t*)(ws + off);
     off += up(rows * 8);
     b.scores = (float*)(ws + off);

@@ -50,7 +50,7 @@ struct Pass {
 // largest of a row's valid samples is its threshold, and the tile GEMM keeps only
 // scores at or above it.
 constexpr int FILTER_KSTRIDE = 16;
-constexpr int64_t FILTER_MAX_LK = 16384;  // at most 1024 samples per row
+constexpr int64_t FILTER_MAX_LK = 65536;  // at most 4096 samples per row
 
 // Workspace pointers of one pass.
 struct PassBufs {

@@ -1110,9 +1110,9 @@ __device__ __forceinline__ void wave_radix_select(const uint64_t (&key)[E], int 
   *prefix_out = prefix;
 }
 
-// The k_eff (<= 256) largest of n <= E * 64 register keys, sorted descending,
-// written as k words to out (0 pads). sbuf: 256 keys of LDS.
-template <int E>
+// The k_eff (<= KCAP: 256 or 512) largest of n <= E * 64 register keys, sorted
+// descending, written as k words to out (0 pads). sbuf: KCAP keys of LDS.
+template <int E, int KCAP = 256>
 __device__ __forceinline__ void wave_select_store(const uint64_t (&key)[E], int n, uint32_t k_eff, int64_t k,
                                                   uint64_t* sbuf, uint32_t* hist, uint64_t* out) {
   const int lane = threadIdx.x & 63;
@@ -1127,19 +1127,21 @@ __device__ __forceinline__ void wave_select_store(const uint64_t (&key)[E], int 
     const bool take = lane + 64 * e < n && (key[e] >> shift) >= lim;
     const uint64_t m = __ballot(take);
     const int pos = base + (int)__builtin_amdgcn_mbcnt_hi((uint32_t)(m >> 32), __builtin_amdgcn_mbcnt_lo((uint32_t)m, 0u));
-    if (take && pos < 256) sbuf[pos] = key[e];
+    if (take && pos < KCAP) sbuf[pos] = key[e];
     base += __popcll(m);
   }
   __syncthreads();
-  if (k_eff <= 64) wave_sort_store<1>(sbuf, k_eff, k, out);
-  else if (k_eff <= 128) wave_sort_store<2>(sbuf, k_eff, k, out);
-  else wave_sort_store<4>(sbuf, k_eff, k, out);
-  for (int64_t t = lane + 64 * (k_eff <= 64 ? 1 : k_eff <= 128 ? 2 : 4); t < k; t += 64) out[t] = 0ull;
+  int sorted;
+  if (k_eff <= 64) wave_sort_store<1>(sbuf, k_eff, k, out), sorted = 64;
+  else if (k_eff <= 128) wave_sort_store<2>(sbuf, k_eff, k, out), sorted = 128;
+  else if (KCAP <= 256 || k_eff <= 256) wave_sort_store<4>(sbuf, k_eff, k, out), sorted = 256;
+  else wave_sort_store<(KCAP > 256 ? 8 : 4)>(sbuf, k_eff, k, out), sorted = 512;
+  for (int64_t t = lane + sorted; t < k; t += 64) out[t] = 0ull;
 }
 
 // Reads a row's n candidate words (c0 from b0, the rest from b1) into E registers
 // per lane as order-preserving keys, then selects and stores.
-template <int E>
+template <int E, int KCAP = 256>
 __device__ __forceinline__ void cand_select_regs(const uint64_t* b0, const uint64_t* b1, int c0, int n, uint32_t k_eff,
                                                  int64_t k, uint64_t* sbuf, uint32_t* hist, uint64_t* out) {
   const int lane = threadIdx.x & 63;
@@ -1151,11 +1153,14 @@ __device__ __forceinline__ void cand_select_regs(const uint64_t* b0, const uint6
     if (i < n) wd = i < c0 ? b0[i] : b1[i - c0];
     key[e] = ((uint64_t)ord_u32(__uint_as_float((uint32_t)(wd >> 32))) << 32) | (wd & 0xFFFFFFFFull);
   }
-  wave_select_store<E>(key, n, k_eff, k, sbuf, hist, out);
+  wave_select_store<E, KCAP>(key, n, k_eff, k, sbuf, hist, out);
 }
 
+// BIG: rows of up to 2048 candidates and k <= 512 (the filtered path's larger lists)
+template <bool BIG>
 __device__ __forceinline__ void cand_select_row(const Problem& pb, const Pass& ps, const PassBufs& bufs, int64_t p,
                                                 uint64_t* sbuf, uint32_t* hist) {
+  constexpr int KCAP = BIG ? 512 : 256, NMAX = BIG ? 128 * CAND_REGS : 64 * CAND_REGS;
   const RowRef rr = row_of(pb, ps, p);
   if (!rr.ok) return;
   const int64_t nv = valid_keys(pb, rr.i);
@@ -1165,24 +1170,30 @@ __device__ __forceinline__ void cand_select_row(const Problem& pb, const Pass& p
     c1 = c0 > bufs.caph ? c0 - bufs.caph : 0;
     c0 = c0 > bufs.caph ? bufs.caph : c0;
   }
-  if (c0 > bufs.caph || c1 > bufs.caph || c0 + c1 < (int64_t)k_eff || k_eff > 256 ||
-      c0 + c1 > 64 * CAND_REGS) {
+  if (c0 > bufs.caph || c1 > bufs.caph || c0 + c1 < (int64_t)k_eff || k_eff > KCAP || c0 + c1 > NMAX) {
     if ((threadIdx.x & 63) == 0) bufs.redo_list[atomicAdd(bufs.redo_count, 1)] = (int32_t)p;
     return;
   }
   const int n = (int)(c0 + c1);
   const uint64_t* b0 = bufs.cand + (2 * p) * bufs.caph;
   uint64_t* out = bufs.sel + p * pb.k;
-  if (n <= 128) cand_select_regs<2>(b0, b0 + bufs.caph, (int)c0, n, k_eff, pb.k, sbuf, hist, out);
-  else if (n <= 256) cand_select_regs<4>(b0, b0 + bufs.caph, (int)c0, n, k_eff, pb.k, sbuf, hist, out);
-  else if (n <= 512) cand_select_regs<8>(b0, b0 + bufs.caph, (int)c0, n, k_eff, pb.k, sbuf, hist, out);
-  else cand_select_regs<CAND_REGS>(b0, b0 + bufs.caph, (int)c0, n, k_eff, pb.k, sbuf, hist, out);
+  if (!BIG) {
+    if (n <= 128) cand_select_regs<2>(b0, b0 + bufs.caph, (int)c0, n, k_eff, pb.k, sbuf, hist, out);
+    else if (n <= 256) cand_select_regs<4>(b0, b0 + bufs.caph, (int)c0, n, k_eff, pb.k, sbuf, hist, out);
+    else if (n <= 512) cand_select_regs<8>(b0, b0 + bufs.caph, (int)c0, n, k_eff, pb.k, sbuf, hist, out);
+    else cand_select_regs<CAND_REGS>(b0, b0 + bufs.caph, (int)c0, n, k_eff, pb.k, sbuf, hist, out);
+  } else {
+    if (n <= 512) cand_select_regs<8, KCAP>(b0, b0 + bufs.caph, (int)c0, n, k_eff, pb.k, sbuf, hist, out);
+    else if (n <= 1024) cand_select_regs<CAND_REGS, KCAP>(b0, b0 + bufs.caph, (int)c0, n, k_eff, pb.k, sbuf, hist, out);
+    else cand_select_regs<2 * CAND_REGS, KCAP>(b0, b0 + bufs.caph, (int)c0, n, k_eff, pb.k, sbuf, hist, out);
+  }
 }
 
+template <bool BIG>
 __global__ __launch_bounds__(64) void k_cand_select(Problem pb, Pass ps, PassBufs bufs) {
-  __shared__ uint64_t sbuf[256];
+  __shared__ uint64_t sbuf[BIG ? 512 : 256];
   __shared__ uint32_t hist[256];
-  cand_select_row(pb, ps, bufs, blockIdx.x, sbuf, hist);
+  cand_select_row<BIG>(pb, ps, bufs, blockIdx.x, sbuf, hist);
 }
 
 // ------------------------------------------------------------------ filtered chunk-tile path
@@ -1232,6 +1243,40 @@ __global__ __launch_bounds__(64) void k_filter_threshold(Problem pb, Pass ps, Pa
   if (lane == 0) bufs.thr[p] = ts;
 }
 
+// the same threshold with one workgroup per row, for rows of up to 4096 samples
+__global__ __launch_bounds__(256) void k_filter_threshold_wg(Problem pb, Pass ps, PassBufs bufs) {
+  __shared__ uint32_t hist[256];
+  __shared__ uint32_t misc[8];
+  __shared__ uint32_t lowest;
+  const int64_t p = blockIdx.x;
+  const RowRef rr = row_of(pb, ps, p);
+  if (!rr.ok) return;  // whole workgroup
+  const int64_t nv = valid_keys(pb, rr.i);
+  const int64_t ns = (nv + FILTER_KSTRIDE - 1) / FILTER_KSTRIDE;
+  const uint32_t k_eff = (uint32_t)(pb.k < nv ? pb.k : nv);
+  const float mu = (float)k_eff * (float)ns / (float)nv;
+  const int R = (int)ceilf(mu + 4.0f * sqrtf(mu) + 4.0f);
+  float ts = -INFINITY;
+  if (R < ns) {
+    const float* row = bufs.samp + p * ((pb.Lk + FILTER_KSTRIDE - 1) / FILTER_KSTRIDE);
+    auto getkey = [&](int64_t e) { return make_key(row[e], (uint32_t)e); };
+    int shift;
+    uint64_t prefix;
+    team_radix_select<256>(getkey, ns, (uint32_t)R, hist, misc, &shift, &prefix);
+    if (threadIdx.x == 0) lowest = 0xFFFFFFFFu;
+    __syncthreads();
+    uint32_t m = 0xFFFFFFFFu;  // the smallest selected score: the R-th largest sample
+    for (int64_t e = threadIdx.x; e < ns; e += 256) {
+      const uint64_t key = getkey(e);
+      if ((key >> shift) >= (prefix >> shift)) m = min(m, (uint32_t)(key >> 32));
+    }
+    atomicMin(&lowest, m);
+    __syncthreads();
+    ts = ord_to_f32(lowest);
+  }
+  if (threadIdx.x == 0) bufs.thr[p] = ts;
+}
+
 __global__ void k_zero_counts(int32_t* p, int64_t n) {
   for (int64_t e = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; e < n; e += (int64_t)gridDim.x * blockDim.x)
     p[e] = 0;
@@ -1248,8 +1293,10 @@ hipError_t launch_filter(const Problem& pb, const Pass& ps, const PassBufs& b, i
     if (g > 0x7FFFFFFF || pb.dtype != T_BF16 || pb.d % 32 != 0 || pb.Lk > FILTER_MAX_LK) return hipErrorInvalidValue;
     if (stage == 1) k_tile_scores_mfma<1><<<(unsigned)g, 256, 0, st>>>(pb, ps, b);
     else k_tile_scores_mfma<2><<<(unsigned)g, 256, 0, st>>>(pb, ps, b);
-  } else {
+  } else if ((pb.Lk + FILTER_KSTRIDE - 1) / FILTER_KSTRIDE <= 64 * CAND_REGS) {
     k_filter_threshold<<<(unsigned)rows, 64, 0, st>>>(pb, ps, b);
+  } else {
+    k_filter_threshold_wg<<<(unsigned)rows, 256, 0, st>>>(pb, ps, b);
   }
   return hipGetLastError();
 }
@@ -1716,7 +1763,8 @@ hipError_t launch_fused_scan(const Problem& pb, const Pass& ps, const PassBufs& 
 }
 
 hipError_t launch_cand_select(const Problem& pb, const Pass& ps, const PassBufs& b, hipStream_t st) {
-  k_cand_select<<<(unsigned)pass_rows(pb, ps), 64, 0, st>>>(pb, ps, b);
+  if (b.caph > 512) k_cand_select<true><<<(unsigned)pass_rows(pb, ps), 64, 0, st>>>(pb, ps, b);
+  else k_cand_select<false><<<(unsigned)pass_rows(pb, ps), 64, 0, st>>>(pb, ps, b);
   return hipGetLastError();
 }
 

@@ -76,7 +76,7 @@ def test_path_choice_for_the_five_workloads():
     assert tk.attn_path(8, 12, 512, 512, 64, 64, 512, False, tk.TOPK_BF16) == 1
     assert tk.attn_path(1, 16, 32768, 32768, 64, 64, 1024, False, tk.TOPK_BF16) == 1
     assert tk.attn_path(4, 16, 8192, 8192, 128, 128, 1024, True, tk.TOPK_BF16) == 4
-    assert tk.ffn_path(16384, 1024, 65536, 512, 1024, tk.TOPK_BF16) == 2
+    assert tk.ffn_path(16384, 1024, 65536, 512, 1024, tk.TOPK_BF16) == 4
     assert tk.attn_path(1, 1, 10, 10, 64, 0) == E_INVAL
 
 

@@ -99,6 +99,9 @@ FFN_CASES = {
     "c5_tile": dict(N=300, d_model=256, d_ff=4096, k=512, chunk=128),
     "c5_tile_small_k": dict(N=100, d_model=64, d_ff=2000, k=7, chunk=33),
     "ffn_fused_all": dict(N=260, d_model=64, d_ff=1000, k=64, chunk=100),
+    # filtered chunk-tile path with k > 256 (2048-entry lists) and a workgroup threshold
+    # over more than 1024 samples
+    "ffn_filter_k300_wg_threshold": dict(N=200, d_model=128, d_ff=20000, k=300, chunk=64),
     "ffn_fused_sample": dict(N=130, d_model=128, d_ff=20000, k=100, chunk=0),
 }
 
@@ -254,7 +257,7 @@ def test_worked_examples_on_gpu(ex, dtype):
 
 def _planted(w: wl.Workload, alpha: np.ndarray, seed: int) -> dict:
     """Q = e0 + noise, K[j] = alpha[j] e0 + noise, V ~ N(0,1): score(i, j) is about
-    alpha[j], so the test decides which keys win (bf16 storage)."""
+    alpha[j], so the test decides which keys win (stored in the workload's dtype)."""
     rng = np.random.Generator(np.random.PCG64(seed))
     q = 0.3 * rng.standard_normal((w.B, w.H, w.Lq, w.d)).astype(np.float32)
     q[..., 0] = 1.0
@@ -263,6 +266,8 @@ def _planted(w: wl.Workload, alpha: np.ndarray, seed: int) -> dict:
     v = rng.standard_normal((w.B, w.H, w.Lk, w.d)).astype(np.float32)
 
     def t(a):
+        if w.dtype == wl.F32:
+            return wl.Tensor(a, None, wl.F32)
         bits = wl.f32_to_bf16_bits(a)
         return wl.Tensor(wl.bf16_bits_to_f32(bits), bits, wl.BF16)
 
@@ -320,8 +325,8 @@ def test_tile_long_row_fallback():
     """Rows over 8192 keys: 30 of the 1024 sampled keys score high, the rest of the
     sample lowest; the threshold (24th sampled key) keeps 24 < k keys, and the row is
     selected by the multi-pass radix select from the tile row."""
-    w = wl.WORKLOADS["c2"].scaled(B=1, H=1, Lq=60, Lk=17000, d=96, k=32, chunk=64)
-    assert tk.attn_path(w.B, w.H, w.Lq, w.Lk, w.d, w.k, w.chunk, w.causal, tk.TOPK_BF16) == 2
+    w = wl.WORKLOADS["c2"].scaled(B=1, H=1, Lq=60, Lk=17000, d=96, k=32, chunk=64, dtype=wl.F32)
+    assert tk.attn_path(w.B, w.H, w.Lq, w.Lk, w.d, w.k, w.chunk, w.causal, tk.TOPK_F32) == 2
     alpha = np.full(w.Lk, 3.0)
     s = np.arange(1024)
     pos = 32 * ((s >> 5) * w.Lk // 1024) + (s & 31)
