@@ -32,15 +32,13 @@ SCAN_END = "// -----------------------------------------------------------------
 
 
 def scan_source_digest() -> str:
-    """Digest of the scan kernel's own source (its section of topk_kernels.hip plus
-    the shared internal header): counter readings stay valid while it is unchanged."""
+    """Digest of the scan kernel's own source (its section of topk_kernels.hip: the
+    argument block, launch shape and kernel): counter readings stay valid while it
+    is unchanged."""
     with open(os.path.join(CSRC, "topk_kernels.hip")) as f:
         text = f.read()
     a, b = text.index(SCAN_BEGIN), text.index(SCAN_END)
-    h = hashlib.sha256(text[a:b].encode())
-    with open(os.path.join(CSRC, "topk_internal.h"), "rb") as f:
-        h.update(f.read())
-    return h.hexdigest()[:16]
+    return hashlib.sha256(text[a:b].encode()).hexdigest()[:16]
 
 
 def traffic_for_current_kernel(workload: str, path: int):
