@@ -992,13 +992,32 @@ __device__ __forceinline__ uint64_t shfl_xor_u64(uint64_t x, int m) {
   const uint32_t lo = __shfl_xor((uint32_t)x, m, 64), hi = __shfl_xor((uint32_t)(x >> 32), m, 64);
   return ((uint64_t)hi << 32) | lo;
 }
+// The value of lane (lane ^ m), m a power of two known at compile time once the
+// caller is unrolled: m = 1, 2 by a DPP quad permutation (no LDS traffic), m = 4..16
+// by a bit-mode ds_swizzle (xor within 32 lanes), m = 32 by ds_bpermute.
+__device__ __forceinline__ uint32_t xor_lane_u32(uint32_t x, int m) {
+  switch (m) {
+    case 1: return (uint32_t)__builtin_amdgcn_mov_dpp((int)x, 0xB1, 0xF, 0xF, false);  // quad [1,0,3,2]
+    case 2: return (uint32_t)__builtin_amdgcn_mov_dpp((int)x, 0x4E, 0xF, 0xF, false);  // quad [2,3,0,1]
+    case 4: return (uint32_t)__builtin_amdgcn_ds_swizzle((int)x, 0x1F | (4 << 10));
+    case 8: return (uint32_t)__builtin_amdgcn_ds_swizzle((int)x, 0x1F | (8 << 10));
+    case 16: return (uint32_t)__builtin_amdgcn_ds_swizzle((int)x, 0x1F | (16 << 10));
+    default: return (uint32_t)__shfl_xor((int)x, m, 64);
+  }
+}
+__device__ __forceinline__ uint64_t xor_lane_u64(uint64_t x, int m) {
+  return ((uint64_t)xor_lane_u32((uint32_t)(x >> 32), m) << 32) | xor_lane_u32((uint32_t)x, m);
+}
 
 // Bitonic sort, descending, of 64*E keys held as r[e] = element (e*64 + lane).
 template <int E>
 __device__ __forceinline__ void wave_sort_desc(uint64_t (&r)[E]) {
   const int lane = threadIdx.x & 63;
   constexpr int P = 64 * E;
+  // fully unrolled: every shuffle distance is a compile-time constant
+#pragma unroll
   for (int size = 2; size <= P; size <<= 1) {
+#pragma unroll
     for (int stride = size >> 1; stride > 0; stride >>= 1) {
       if (stride >= 64) {  // partners in the same lane, other register
         const int rs = stride / 64;
@@ -1018,7 +1037,7 @@ __device__ __forceinline__ void wave_sort_desc(uint64_t (&r)[E]) {
 #pragma unroll
         for (int e = 0; e < E; ++e) {
           const int i = e * 64 + lane;
-          const uint64_t y = shfl_xor_u64(r[e], stride);
+          const uint64_t y = xor_lane_u64(r[e], stride);
           const bool desc = (i & size) == 0;
           const bool lower = (lane & stride) == 0;
           // the lower element of a pair keeps the larger key when descending
