@@ -1008,6 +1008,19 @@ __device__ __forceinline__ uint32_t xor_lane_u32(uint32_t x, int m) {
 __device__ __forceinline__ uint64_t xor_lane_u64(uint64_t x, int m) {
   return ((uint64_t)xor_lane_u32((uint32_t)(x >> 32), m) << 32) | xor_lane_u32((uint32_t)x, m);
 }
+// Inclusive prefix sum over the 64 lanes of a wave whose lanes are all active, by
+// DPP: row shifts 1, 2, 4, 8 scan each row of 16 lanes, then the broadcasts of lane
+// 15 (into rows 1 and 3) and lane 31 (into rows 2 and 3) carry the row totals.
+// Lanes without a source add the `old` operand, 0.
+__device__ __forceinline__ uint32_t wave_incl_scan_full(uint32_t x) {
+  x += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)x, 0x111, 0xF, 0xF, false);  // row_shr:1
+  x += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)x, 0x112, 0xF, 0xF, false);  // row_shr:2
+  x += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)x, 0x114, 0xF, 0xF, false);  // row_shr:4
+  x += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)x, 0x118, 0xF, 0xF, false);  // row_shr:8
+  x += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)x, 0x142, 0xA, 0xF, false);  // row_bcast:15
+  x += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)x, 0x143, 0xC, 0xF, false);  // row_bcast:31
+  return x;
+}
 
 // Bitonic sort, descending, of 64*E keys held as r[e] = element (e*64 + lane).
 template <int E>
@@ -1079,7 +1092,7 @@ __device__ __forceinline__ void wave_radix_select(const uint64_t (&key)[E], int 
   }
 #pragma unroll
   for (int off = 32; off > 0; off >>= 1) {
-    const uint64_t a0 = shfl_xor_u64(kmin, off), a1 = shfl_xor_u64(kmax, off);
+    const uint64_t a0 = xor_lane_u64(kmin, off), a1 = xor_lane_u64(kmax, off);
     kmin = a0 < kmin ? a0 : kmin;
     kmax = a1 > kmax ? a1 : kmax;
   }
@@ -1102,7 +1115,7 @@ __device__ __forceinline__ void wave_radix_select(const uint64_t (&key)[E], int 
     const uint4 h4 = reinterpret_cast<const uint4*>(hist)[63 - lane];  // bins 255-4l .. 252-4l
     const uint32_t c4[4] = {h4.w, h4.z, h4.y, h4.x};                   // descending digit order
     const uint32_t local = c4[0] + c4[1] + c4[2] + c4[3];
-    uint32_t run = team_excl_scan<64>(local, nullptr);
+    uint32_t run = wave_incl_scan_full(local) - local;
     uint32_t digit = 0, above = 0, cnt = 0;
     bool here = false;
 #pragma unroll
@@ -1116,10 +1129,10 @@ __device__ __forceinline__ void wave_radix_select(const uint64_t (&key)[E], int 
       run += c4[e];
     }
     const uint64_t who = __ballot(here);
-    const int src = __builtin_ctzll(who);
-    digit = __shfl(digit, src, 64);
-    above = __shfl(above, src, 64);
-    cnt = __shfl(cnt, src, 64);
+    const int src = __builtin_ctzll(who);  // wave-uniform
+    digit = (uint32_t)__builtin_amdgcn_readlane((int)digit, src);
+    above = (uint32_t)__builtin_amdgcn_readlane((int)above, src);
+    cnt = (uint32_t)__builtin_amdgcn_readlane((int)cnt, src);
     __syncthreads();  // hist is cleared again by the next pass
     prefix |= (uint64_t)digit << shift;
     kr -= above;
