@@ -337,3 +337,33 @@ def test_tile_long_row_fallback():
     out, idx, _ = parity.run_attn(w, x)
     assert tk.last_fallback_rows() == w.Lq
     parity.check_attn(w, x, out, idx)
+
+
+@pytest.mark.parametrize("base,kw,path", [
+    ("c3", dict(H=2, Lq=700, Lk=9000, chunk=128), 1),                                  # fused
+    ("c2", dict(B=1, H=2, Lq=300, Lk=1500, d=96, k=40, chunk=64), 2),                # chunk-tile
+    ("c4", dict(B=1, H=2, Lq=2500, Lk=2500, chunk=256), 4),                          # filtered chunk-tile
+    ("c3", dict(H=2, Lq=4200, Lk=4200, k=16, chunk=512, causal=True), 3),            # split by rows
+])
+def test_one_chunk_per_pass_is_bit_identical(base, kw, path):
+    """A memory budget below one chunk runs every chunk in a pass of its own (the
+    paper's sequential query chunking); the result is the default budget's, bit for bit."""
+    w = wl.WORKLOADS[base].scaled(**kw)
+    dt = tk.TOPK_BF16 if w.dtype == wl.BF16 else tk.TOPK_F32
+    assert tk.attn_path(w.B, w.H, w.Lq, w.Lk, w.d, w.k, w.chunk, w.causal, dt) == path
+    _say("one chunk per pass", path, w)
+    x = wl.make_inputs(w)
+    ref = parity.run_attn(w, x)
+    tk.set_memory_budget(1)
+    try:
+        got = parity.run_attn(w, x)
+    finally:
+        tk.set_memory_budget(0)
+    def bits(t):  # compare floating-point outputs bit for bit (NaN-safe)
+        t = t.cpu()
+        return t.view(torch.int32) if t.dtype == torch.float32 else t.view(torch.int16) \
+            if t.dtype == torch.bfloat16 else t
+
+    for a, b in zip(ref, got):
+        assert torch.equal(bits(a), bits(b))
+    parity.check_attn(w, x, got[0], got[1])
