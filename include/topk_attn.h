@@ -1,8 +1,7 @@
 /*
  * topk_attn.h -- C ABI of the MI355X (gfx950) top-k attention library.
  *
- * The library computes the forward pass of top-k attention (arXiv 2106.06899,
- * Section 2.2, Eq. 4):
+ * The library computes top-k attention (arXiv 2106.06899, Section 2.2, Eq. 4):
  *
  *     out = activation( top-k( Q K^T ) ) V
  *
@@ -10,7 +9,15 @@
  * an activation runs over those k survivors only, and the k matching value rows
  * are summed with the resulting weights. Queries are processed in chunks of
  * `chunk` rows (Section 2.2, "Query chunking"); the chunk size bounds the
- * working memory and never changes the result.
+ * working memory and never changes the result. The feed-forward layer written
+ * as attention (Eq. 3: keys W1, values W2, ReLU) has calls of its own (topk_ffn*).
+ *
+ * Entry points: the forward calls (topk_attn, topk_ffn); their *_with_cache
+ * variants, which also write each row's selection for training; the backward
+ * calls (topk_attn_backward, topk_ffn_backward), which recompute from that cache
+ * and the inputs only (Section 2.2, "Input checkpointing"); workspace queries and
+ * registration; two process-wide settings (topk_set_memory_budget,
+ * topk_set_backward_lists); and debug and test hooks.
  *
  * Conventions shared by every call:
  *  - Every tensor pointer is a caller-owned DEVICE pointer to contiguous row-major
@@ -28,6 +35,9 @@
  *    the calling thread, or (when none is registered) stream-ordered memory the
  *    library allocates and frees on `hip_stream`.
  *  - Calls on different streams are safe if they use different workspaces.
+ *    Each call reads the process-wide settings once, when it is made; a change
+ *    applies to the calls made after it (and changes what the workspace queries
+ *    return).
  */
 #ifndef TOPK_ATTN_H
 #define TOPK_ATTN_H

@@ -10,6 +10,7 @@
 #include <string.h>
 
 #include <algorithm>
+#include <atomic>
 #include <string>
 #include <vector>
 
@@ -53,7 +54,7 @@ struct StageTimer {
 
 constexpr size_t ALIGN = 256;
 constexpr size_t DEFAULT_BUDGET = size_t(8) << 30;  // workspace cap when the library allocates
-size_t g_budget = DEFAULT_BUDGET;                    // process-wide, set by topk_set_memory_budget
+std::atomic<size_t> g_budget{DEFAULT_BUDGET};        // process-wide, set by topk_set_memory_budget
 constexpr int64_t DEFAULT_CHUNK = 1024;
 constexpr int64_t FUSED_CAPH = 512;                   // candidates kept per (query, half-wave)
 
@@ -244,7 +245,7 @@ int run(Problem whole, hipStream_t st, bool report) {
   Problem parts[2];
   Plan plans[2];
   const int np = split_rows(whole, parts);
-  size_t budget = g_ws ? g_ws_bytes : g_budget, need = 0;
+  size_t budget = g_ws ? g_ws_bytes : g_budget.load(std::memory_order_relaxed), need = 0;
   for (int q = 0; q < np; ++q) {
     choose_path(parts[q], &plans[q]);
     plan_sizes(parts[q], &plans[q], budget);
@@ -409,11 +410,12 @@ int debug_ptrs(int32_t* idx_out, float* score_out) {
 size_t workspace_for(const Problem& whole) {
   Problem parts[2];
   const int np = split_rows(whole, parts);
+  const size_t budget = g_budget.load(std::memory_order_relaxed);
   size_t need = 0;
   for (int q = 0; q < np; ++q) {
     Plan pl;
     choose_path(parts[q], &pl);
-    plan_sizes(parts[q], &pl, g_budget);
+    plan_sizes(parts[q], &pl, budget);
     const size_t n = plan_total(pl, parts[q]);
     need = n > need ? n : need;
   }
@@ -421,11 +423,11 @@ size_t workspace_for(const Problem& whole) {
 }
 
 // ---------------------------------------------------------------- backward
-int g_list_mode = TOPK_LISTS_AUTO;  // process-wide, set by topk_set_backward_lists
+std::atomic<int> g_list_mode{TOPK_LISTS_AUTO};  // process-wide, set by topk_set_backward_lists
 
 size_t bwd_bytes(const BwdProblem& bp) {
   const int64_t nkeys = bp.BH * bp.Lk, npairs = bp.BH * bp.Lq * bp.k;
-  const BwdLayout L = bwd_layout(bp.BH, bp.Lq, bp.Lk, bp.k, g_list_mode);
+  const BwdLayout L = bwd_layout(bp.BH, bp.Lq, bp.Lk, bp.k, bp.list_mode);
   const int64_t scanned = std::max(nkeys + 1, L.nhist + 1), nb = (scanned + 1023) / 1024;
   size_t total = up((size_t)npairs * 8) + up((size_t)(nkeys + 1) * 4) + up((size_t)npairs * 4) + up((size_t)nb * 4);
   if (L.bucketed) total += up((size_t)npairs * 8) + up((size_t)(L.nhist + 1) * 4);
@@ -436,7 +438,7 @@ size_t bwd_bytes(const BwdProblem& bp) {
 BwdBufs bwd_carve(const BwdProblem& bp, char* ws) {
   const int64_t nkeys = bp.BH * bp.Lk, npairs = bp.BH * bp.Lq * bp.k;
   BwdBufs b{};
-  b.L = bwd_layout(bp.BH, bp.Lq, bp.Lk, bp.k, g_list_mode);
+  b.L = bwd_layout(bp.BH, bp.Lq, bp.Lk, bp.k, bp.list_mode);
   const int64_t scanned = std::max(nkeys + 1, b.L.nhist + 1), nb = (scanned + 1023) / 1024;
   size_t off = 0;
   b.pair = (float2*)(ws + off);
@@ -464,7 +466,8 @@ int bwd_problem(BwdProblem* bp, const void* Q, const void* K, const void* V, con
   if (rc) return rc;
   if (BH * Lq > (int64_t(1) << 31) / k || BH * Lk >= (int64_t(1) << 31) - 1)
     return fail(TOPK_E_UNSUPPORTED, "the backward pass needs rows * k and heads * keys below 2^31");
-  if (g_list_mode == TOPK_LISTS_BUCKET && !bwd_layout(BH, Lq, Lk, k, g_list_mode).bucketed)
+  const int list_mode = g_list_mode.load(std::memory_order_relaxed);
+  if (list_mode == TOPK_LISTS_BUCKET && !bwd_layout(BH, Lq, Lk, k, list_mode).bucketed)
     return fail(TOPK_E_UNSUPPORTED, "bucket-sorted backward lists need at most 2^19 keys per head (got %lld)",
                 (long long)Lk);
   if (check_ptrs) {
@@ -493,6 +496,7 @@ int bwd_problem(BwdProblem* bp, const void* Q, const void* K, const void* V, con
   bp->scale = scale;
   bp->dtype = dtype == TOPK_BF16 ? T_BF16 : T_F32;
   bp->act = act;
+  bp->list_mode = list_mode;
   return TOPK_OK;
 }
 
@@ -650,7 +654,7 @@ size_t topk_ffn_backward_workspace_bytes(int64_t N, int64_t d_model, int64_t d_f
 
 int topk_set_memory_budget(size_t bytes) {
   g_err.clear();
-  g_budget = bytes ? bytes : DEFAULT_BUDGET;
+  g_budget.store(bytes ? bytes : DEFAULT_BUDGET, std::memory_order_relaxed);
   return TOPK_OK;
 }
 
@@ -658,7 +662,7 @@ int topk_set_backward_lists(int mode) {
   g_err.clear();
   if (mode != TOPK_LISTS_AUTO && mode != TOPK_LISTS_BUCKET && mode != TOPK_LISTS_ATOMIC)
     return fail(TOPK_E_INVAL, "backward list mode must be TOPK_LISTS_AUTO, _BUCKET or _ATOMIC (got %d)", mode);
-  g_list_mode = mode;
+  g_list_mode.store(mode, std::memory_order_relaxed);
   return TOPK_OK;
 }
 

@@ -100,6 +100,7 @@ struct BwdProblem {
   float scale;
   int dtype;
   int act;
+  int list_mode;  // how pairs are grouped by key, fixed for the whole call
 };
 
 // How the backward pass groups the selected pairs by key. Heads of up to 2^19 keys
