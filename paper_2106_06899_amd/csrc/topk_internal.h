@@ -15,8 +15,8 @@ enum ElemType { T_F32 = 0, T_BF16 = 1 };
 enum ScanMode { MODE_ALL = 0, MODE_SAMPLE = 1 };
 
 constexpr int REDO_CAP = 1024;          // redo rows recomputed by the wide fallback kernels
-constexpr int REDO_SPLIT = 2048;        // keys per work item of the wide fallback
-constexpr int REDO_SCORE_BLOCKS = 512;  // workgroups of the wide fallback's score kernel
+constexpr int REDO_SPLIT = 512;         // keys per work item of the wide fallback
+constexpr int REDO_SCORE_BLOCKS = 1024; // workgroups of the wide fallback's score kernel
 constexpr int REDO_BLOCKS = 64;         // workgroups of the fallback for rows beyond REDO_CAP
 constexpr int MAX_SELECT_K = 2048;  // largest k the workgroup select / finalize handle
 

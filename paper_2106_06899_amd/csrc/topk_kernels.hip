@@ -781,10 +781,13 @@ __global__ __launch_bounds__(256, ScanShape<G>::OCC) void k_fused_scan(ScanArgs 
         if (8 * (v >> 2) + (v & 3) > room) acc[g][v] = -INFINITY;
     }
   };
+  // maxima of finite scores (and -inf): the NaN-propagating maximum, which needs no
+  // canonicalising instructions and fuses into three-input maxima
+  auto fmax_ = [](float x, float y) { return __builtin_elementwise_maximum(x, y); };
   auto block_max = [&](const f32x16& acc) {
     float m = acc[0];
 #pragma unroll
-    for (int v = 1; v < 16; ++v) m = fmaxf(m, acc[v]);
+    for (int v = 1; v < 16; ++v) m = fmax_(m, acc[v]);
     return m;
   };
 
@@ -840,16 +843,19 @@ __global__ __launch_bounds__(256, ScanShape<G>::OCC) void k_fused_scan(ScanArgs 
   // A slot holds one dirty half (8 scores) of a lane block: scores 8*hb .. 8*hb+7.
   // slot meta = (32-key block index << 8) | (hb << 7) | (group << 6) | lane
   static_assert(G <= 2, "the slot meta holds one group bit");
-  int scount = 0;  // wave-uniform
-  auto drain = [&]() {
+  // The ring is circular: slots [rhead, rtail) (positions modulo STAGE_CAP) wait for
+  // the drain; both counters are wave-uniform.
+  static_assert((STAGE_CAP & (STAGE_CAP - 1)) == 0, "ring size must be a power of two");
+  int rhead = 0, rtail = 0;
+  auto drain_to = [&](int end) {
     __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
     __builtin_amdgcn_wave_barrier();
     __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
-    for (int base = 0; base < scount; base += 64) {
-      const int slot = base + lane;
+    for (int base = rhead; base < end; base += 64) {
+      const int idx = base + lane, slot = idx & (STAGE_CAP - 1);
       uint32_t mask = 0, meta = 0;
-      const float* sp = &stage[wave][slot < STAGE_CAP ? slot : 0][0];
-      if (slot < scount) {
+      const float* sp = &stage[wave][slot][0];
+      if (idx < end) {
         meta = stage_meta[wave][slot];
         const float t = tau_lds[wave][(meta >> 6 & 1) * 32 + (meta & 31)];
         // slots 4..7 of every 8 read their two 16-byte chunks in the other order,
@@ -881,21 +887,22 @@ __global__ __launch_bounds__(256, ScanShape<G>::OCC) void k_fused_scan(ScanArgs 
         } while (mask);
       }
     }
-    scount = 0;
+    rhead = end;
     __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
     __builtin_amdgcn_wave_barrier();
     __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
   };
+  auto drain = [&]() { drain_to(rtail); };
   // A lane whose block maximum beats its query's threshold stages its dirty half
   // (the lower one when both are dirty); lanes with both halves dirty stage the
   // upper half in a second, rarely needed, round. Two 16-byte writes per lane and
   // round instead of four.
   auto filter = [&](int g, const f32x16& acc, int64_t t, int rb) {
-    float hA = fmaxf(acc[0], acc[1]), hB = fmaxf(acc[8], acc[9]);
+    float hA = fmax_(acc[0], acc[1]), hB = fmax_(acc[8], acc[9]);
 #pragma unroll
     for (int v = 2; v < 8; ++v) {
-      hA = fmaxf(hA, acc[v]);
-      hB = fmaxf(hB, acc[8 + v]);
+      hA = fmax_(hA, acc[v]);
+      hB = fmax_(hB, acc[8 + v]);
     }
     const bool dA = hA > tau[g], dB = hB > tau[g];
     const bool dirty = dA || dB;
@@ -904,11 +911,12 @@ __global__ __launch_bounds__(256, ScanShape<G>::OCC) void k_fused_scan(ScanArgs 
     const bool both = dA && dB;
     const uint64_t bal2 = __ballot(both);
     const int n1 = __popcll(bal), n2 = __popcll(bal2);
-    if (scount + n1 + n2 > STAGE_CAP) drain();
+    if (rtail - rhead + n1 + n2 > STAGE_CAP) drain();
     const uint32_t mb = (uint32_t)((t * KT + rb * 32) / 32) << 8 | (uint32_t)(g << 6) | (uint32_t)lane;
     if (dirty) {
-      const int slot = scount + (int)__builtin_amdgcn_mbcnt_hi((uint32_t)(bal >> 32),
-                                                               __builtin_amdgcn_mbcnt_lo((uint32_t)bal, 0u));
+      const int slot = (rtail + (int)__builtin_amdgcn_mbcnt_hi((uint32_t)(bal >> 32),
+                                                              __builtin_amdgcn_mbcnt_lo((uint32_t)bal, 0u))) &
+                       (STAGE_CAP - 1);
       float4* sp = (float4*)&stage[wave][slot][0];
       // the half to stage, selected in registers (a bitwise mux per score, so the
       // compiler does not turn it into an indexed read of the accumulator)
@@ -923,15 +931,16 @@ __global__ __launch_bounds__(256, ScanShape<G>::OCC) void k_fused_scan(ScanArgs 
     }
     if (bal2) {
       if (both) {
-        const int slot = scount + n1 + (int)__builtin_amdgcn_mbcnt_hi((uint32_t)(bal2 >> 32),
-                                                                      __builtin_amdgcn_mbcnt_lo((uint32_t)bal2, 0u));
+        const int slot = (rtail + n1 + (int)__builtin_amdgcn_mbcnt_hi((uint32_t)(bal2 >> 32),
+                                                                     __builtin_amdgcn_mbcnt_lo((uint32_t)bal2, 0u))) &
+                         (STAGE_CAP - 1);
         float4* sp = (float4*)&stage[wave][slot][0];
         sp[0] = make_float4(acc[8], acc[9], acc[10], acc[11]);
         sp[1] = make_float4(acc[12], acc[13], acc[14], acc[15]);
         stage_meta[wave][slot] = mb | 128u;
       }
     }
-    scount += n1 + n2;
+    rtail += n1 + n2;
   };
   // Main scan: a stream of 32-key blocks. When a block opens a new tile, that
   // tile's wait and barrier (and the loads of the tile SCAN_NB - 1 further on,
@@ -963,7 +972,13 @@ __global__ __launch_bounds__(256, ScanShape<G>::OCC) void k_fused_scan(ScanArgs 
       for (int g = 0; g < G; ++g) filter(g, acc[g], t, (int)(blkno - t * NRB));
     };
     for (int64_t blkno = 0; blkno < nblocks; ++blkno) {
-      if (blkno > 0 && blkno % NRB == 0) open_tile(blkno / NRB);
+      if (blkno > 0 && blkno % NRB == 0) {
+        open_tile(blkno / NRB);
+        // drain whole 64-slot rounds right after the next tile's loads are issued:
+        // the candidate stores then complete while this tile is computed, instead
+        // of delaying the wait for the next tile's loads
+        if (rtail - rhead >= 64) drain_to(rhead + ((rtail - rhead) & ~63));
+      }
       f32x16 x[G];
       compute(blkno, x);
       filter_all(x, blkno);
@@ -1497,18 +1512,27 @@ __global__ __launch_bounds__(256) void k_redo_scores(Problem pb, Pass ps, PassBu
     __syncthreads();
     const T* Kh = (const T*)pb.K + rr.bh * pb.kv_head_stride;
     float* row = bufs.scores + r * pb.Lk;
+    // two keys per thread, their loads interleaved (REDO_SPLIT = 2 * 256)
+    static_assert(REDO_SPLIT == 512, "two keys per thread");
     const int64_t j1 = (sp + 1) * REDO_SPLIT < nv ? (sp + 1) * REDO_SPLIT : nv;
-    for (int64_t j = sp * REDO_SPLIT + threadIdx.x; j < j1; j += 256) {
-      const T* kr = Kh + j * pb.d;
-      float acc = 0.f;
-      for (int64_t f = 0; f < pb.d; f += 8) {
-        float x[8];
-        load8<T>(kr + f, x);
+    const int64_t ja = sp * REDO_SPLIT + threadIdx.x, jb = ja + 256;
+    const T* ka = Kh + (ja < j1 ? ja : 0) * pb.d;
+    const T* kb = Kh + (jb < j1 ? jb : 0) * pb.d;
+    float acc_a = 0.f, acc_b = 0.f;
+    // unrolled so that several 16-byte loads of both rows are in flight at once
+#pragma unroll 4
+    for (int64_t f = 0; f < pb.d; f += 8) {
+      float xa[8], xb[8];
+      load8<T>(ka + f, xa);
+      load8<T>(kb + f, xb);
 #pragma unroll
-        for (int e = 0; e < 8; ++e) acc = fmaf(qrow[f + e], x[e], acc);
+      for (int e = 0; e < 8; ++e) {
+        acc_a = fmaf(qrow[f + e], xa[e], acc_a);
+        acc_b = fmaf(qrow[f + e], xb[e], acc_b);
       }
-      row[j] = acc;
     }
+    if (ja < j1) row[ja] = acc_a;
+    if (jb < j1) row[jb] = acc_b;
     __syncthreads();
   }
 }
