@@ -311,6 +311,53 @@ def bench_chunk_sweep(args):
         del layer
 
 
+def bench_memory_sweep(args):
+    """Memory and time of the c3 workload (16 heads, d 64, k 64, chunk 1024, planted
+    top set) at several sequence lengths L = Lq = Lk: the peak of PyTorch's allocator
+    during a call (the inputs, the output and the library's workspace, which the
+    binding allocates as a PyTorch tensor) minus the inputs and the output, the
+    workspace the library asks for, and the time per call. One JSON line per length,
+    then one with the growth per doubling of L (the method's memory is linear in L)."""
+    import torch
+    import paper_2106_06899_amd as tk
+    from paper_2106_06899_amd import workloads as wl
+    dev = torch.device("cuda:0")
+    lengths = [int(t) for t in args.mem_lengths.split(",")]
+    extra = {}
+    for L in lengths:
+        w = wl.WORKLOADS["c3"].scaled(Lq=L, Lk=L)
+        print(f"[bench] memory sweep L={L}: generating", file=sys.stderr, flush=True)
+        x = wl.make_inputs(w)
+        q, k, v = (torch.from_numpy(np.ascontiguousarray(x[n].bits)).view(torch.bfloat16).to(dev)
+                   for n in ("Q", "K", "V"))
+        del x
+        io_bytes = 4 * q.numel() * q.element_size()  # Q, K, V and the output
+
+        def step():
+            tk.attn(q, k, v, w.k, w.chunk, w.causal, w.scale)
+
+        torch.cuda.synchronize()
+        torch.cuda.reset_peak_memory_stats(dev)
+        ms = _timed(step, args.steps, args.warmup)
+        peak = torch.cuda.max_memory_allocated(dev)
+        ws = tk.attn_workspace_bytes(w.B, w.H, L, L, w.d, w.k, w.chunk, w.causal)
+        extra[L] = peak - io_bytes
+        print(json.dumps({
+            "metric": "top-k attention peak memory above inputs and output vs sequence length",
+            "value": extra[L] / 2**30, "unit": "GiB", "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
+            "ms_per_step": ms, "queries_per_s": w.queries / (ms / 1e3), "higher_is_better": False,
+            "dtype": "bf16", "data": "synthetic",
+            "config": {"workload": f"c3 shape at L {L}: 1x16 heads, d 64, k 64, chunk 1024, planted top set",
+                       "seq_len": L, "path": tk.attn_path(w.B, w.H, L, L, w.d, w.k, w.chunk, w.causal)},
+            "peak_gib": peak / 2**30, "inputs_and_output_gib": io_bytes / 2**30,
+            "workspace_gib": ws / 2**30}), flush=True)
+        del q, k, v
+    growth = {f"{a}->{b}": extra[b] / extra[a] for a, b in zip(lengths, lengths[1:]) if b == 2 * a}
+    print(json.dumps({"metric": "growth of peak memory above inputs and output per doubling of L",
+                      "value": max(growth.values()) if growth else None, "unit": "ratio",
+                      "higher_is_better": False, "per_doubling": growth}), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -325,6 +372,9 @@ def main():
                     help="write the scan's HBM bytes per launch from four rocprofv3 counter_collection.csv files")
     ap.add_argument("--copy-bytes", type=int, default=1 << 30)
     ap.add_argument("--traffic-command", default="")
+    ap.add_argument("--memory-sweep", action="store_true",
+                    help="peak memory and time of the c3 workload at several sequence lengths")
+    ap.add_argument("--mem-lengths", default="4096,8192,16384,32768,65536", help="lengths for --memory-sweep")
     ap.add_argument("--layer", action="store_true",
                     help="time the multi-head attention layer (BERT-base shape, causal, k 128, chunk 1024)")
     ap.add_argument("--lengths", default="4096,16384,65536", help="sequence lengths for --layer")
@@ -355,6 +405,9 @@ def main():
               file=sys.stderr)
         sys.exit(2)
 
+    if args.memory_sweep:
+        bench_memory_sweep(args)
+        return
     if args.layer:
         bench_layer(args)
         return

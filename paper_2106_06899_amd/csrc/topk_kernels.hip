@@ -672,8 +672,10 @@ __global__ __launch_bounds__(256, ScanShape<G>::OCC) void k_fused_scan(ScanArgs 
   constexpr int QB = scan_queries_per_wg<G>();
   static_assert(LPW >= 1 && TILEB % 4096 == 0, "tile must split evenly over the 4 waves");
   __shared__ __attribute__((aligned(16))) unsigned char ks[SCAN_NB][TILEB];
-  // staging slot = 8 scores (32 bytes): one dirty half of a lane block
-  __shared__ __attribute__((aligned(16))) float stage[4][STAGE_CAP][8];
+  // staging slot = 8 scores: one dirty half of a lane block, as two 16-byte chunks
+  // held in separate arrays (chunk c of slot s at stage[wave][c][s]), so the writes
+  // and reads of consecutive slots by consecutive lanes are free of bank conflicts
+  __shared__ __attribute__((aligned(16))) float4 stage[4][2][STAGE_CAP];
   __shared__ uint32_t stage_meta[4][STAGE_CAP];
   __shared__ float tau_lds[4][32 * G];
   __shared__ uint32_t cnt_lds[4][64 * G];
@@ -854,17 +856,12 @@ __global__ __launch_bounds__(256, ScanShape<G>::OCC) void k_fused_scan(ScanArgs 
     for (int base = rhead; base < end; base += 64) {
       const int idx = base + lane, slot = idx & (STAGE_CAP - 1);
       uint32_t mask = 0, meta = 0;
-      const float* sp = &stage[wave][slot][0];
       if (idx < end) {
         meta = stage_meta[wave][slot];
         const float t = tau_lds[wave][(meta >> 6 & 1) * 32 + (meta & 31)];
-        // slots 4..7 of every 8 read their two 16-byte chunks in the other order,
-        // so the 8 lanes one LDS cycle serves hit 8 different bank groups
-        const uint32_t r = (uint32_t)(slot >> 2) & 1u;
 #pragma unroll
-        for (uint32_t q4 = 0; q4 < 2; ++q4) {
-          const uint32_t cc = q4 ^ r;
-          const float4 x = *(const float4*)(sp + 4 * cc);
+        for (uint32_t cc = 0; cc < 2; ++cc) {
+          const float4 x = stage[wave][cc][slot];
           const uint32_t m4 = (x.x > t ? 1u : 0u) | (x.y > t ? 2u : 0u) | (x.z > t ? 4u : 0u) | (x.w > t ? 8u : 0u);
           mask |= m4 << (4 * cc);
         }
@@ -880,7 +877,7 @@ __global__ __launch_bounds__(256, ScanShape<G>::OCC) void k_fused_scan(ScanArgs 
           mask &= mask - 1;
           // score u = 8*hb + v of the block is key 8*(u/4) + u%4 = u + (u & ~3) past the block's first key
           const uint32_t u = 8u * hb + v;
-          const float sc = sp[v];
+          const float sc = ((const float*)&stage[wave][v >> 2][slot])[v & 3];
           if (pos < (uint32_t)a.caph)
             dst[pos] = ((uint64_t)__float_as_uint(sc) << 32) | (uint64_t)(nj - (u + (u & 12u)));
           ++pos;
@@ -917,7 +914,6 @@ __global__ __launch_bounds__(256, ScanShape<G>::OCC) void k_fused_scan(ScanArgs 
       const int slot = (rtail + (int)__builtin_amdgcn_mbcnt_hi((uint32_t)(bal >> 32),
                                                               __builtin_amdgcn_mbcnt_lo((uint32_t)bal, 0u))) &
                        (STAGE_CAP - 1);
-      float4* sp = (float4*)&stage[wave][slot][0];
       // the half to stage, selected in registers (a bitwise mux per score, so the
       // compiler does not turn it into an indexed read of the accumulator)
       const uint32_t sel = dA ? 0xFFFFFFFFu : 0u;
@@ -925,8 +921,8 @@ __global__ __launch_bounds__(256, ScanShape<G>::OCC) void k_fused_scan(ScanArgs 
 #pragma unroll
       for (int v = 0; v < 8; ++v)
         x[v] = __uint_as_float((__float_as_uint(acc[v]) & sel) | (__float_as_uint(acc[8 + v]) & ~sel));
-      sp[0] = make_float4(x[0], x[1], x[2], x[3]);
-      sp[1] = make_float4(x[4], x[5], x[6], x[7]);
+      stage[wave][0][slot] = make_float4(x[0], x[1], x[2], x[3]);
+      stage[wave][1][slot] = make_float4(x[4], x[5], x[6], x[7]);
       stage_meta[wave][slot] = mb | (dA ? 0u : 128u);
     }
     if (bal2) {
@@ -934,9 +930,8 @@ __global__ __launch_bounds__(256, ScanShape<G>::OCC) void k_fused_scan(ScanArgs 
         const int slot = (rtail + n1 + (int)__builtin_amdgcn_mbcnt_hi((uint32_t)(bal2 >> 32),
                                                                      __builtin_amdgcn_mbcnt_lo((uint32_t)bal2, 0u))) &
                          (STAGE_CAP - 1);
-        float4* sp = (float4*)&stage[wave][slot][0];
-        sp[0] = make_float4(acc[8], acc[9], acc[10], acc[11]);
-        sp[1] = make_float4(acc[12], acc[13], acc[14], acc[15]);
+        stage[wave][0][slot] = make_float4(acc[8], acc[9], acc[10], acc[11]);
+        stage[wave][1][slot] = make_float4(acc[12], acc[13], acc[14], acc[15]);
         stage_meta[wave][slot] = mb | 128u;
       }
     }
