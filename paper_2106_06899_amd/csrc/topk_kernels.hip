@@ -415,12 +415,22 @@ __global__ __launch_bounds__(256, 2) void k_tile_scores_mfma(Problem pb, Pass ps
       for (int b = 0; b < 4; ++b) {
         const uint32_t kb = (uint32_t)(key0 + wk + b * 32 + 4 * half);
         // scores of this block as a list of set bits: the wave loops as often as its
-        // busiest lane (the score is picked by a select over the 16 registers)
+        // busiest lane; the score is picked from the 16 registers by a binary tree of
+        // bitwise muxes, one level per bit of its index
         for (uint32_t m = pass[a][b]; m; m &= m - 1) {
           const uint32_t v = (uint32_t)__builtin_ctz(m);
-          float x = acc[a][b][0];
+          const f32x16& x16 = acc[a][b];
+          uint32_t t8[8], t4[4], t2[2];
+          const uint32_t s0 = 0u - (v & 1u), s1 = 0u - ((v >> 1) & 1u), s2 = 0u - ((v >> 2) & 1u),
+                         s3 = 0u - ((v >> 3) & 1u);
 #pragma unroll
-          for (int u = 1; u < 16; ++u) x = v == (uint32_t)u ? acc[a][b][u] : x;
+          for (int u = 0; u < 8; ++u)
+            t8[u] = (__float_as_uint(x16[2 * u + 1]) & s0) | (__float_as_uint(x16[2 * u]) & ~s0);
+#pragma unroll
+          for (int u = 0; u < 4; ++u) t4[u] = (t8[2 * u + 1] & s1) | (t8[2 * u] & ~s1);
+#pragma unroll
+          for (int u = 0; u < 2; ++u) t2[u] = (t4[2 * u + 1] & s2) | (t4[2 * u] & ~s2);
+          const float x = __uint_as_float((t2[1] & s3) | (t2[0] & ~s3));
           if (pos < cap)
             dst[pos] = ((uint64_t)__float_as_uint(x) << 32) | (uint64_t)(0xFFFFFFFFu - (kb + 8 * (v >> 2) + (v & 3)));
           ++pos;
