@@ -1116,20 +1116,26 @@ __device__ __forceinline__ void wave_radix_select(const uint64_t (&key)[E], int 
     kmin = a0 < kmin ? a0 : kmin;
     kmax = a1 > kmax ? a1 : kmax;
   }
-  // bytes above the highest differing bit are common to every candidate
+  // bits above the highest differing bit are common to every candidate; the first
+  // digit starts at that bit (not at a byte boundary), so it splits the candidates
+  // over as many bins as 8 bits can (scores above a threshold often share their top
+  // byte, which would pile a byte-aligned first pass onto a few bins)
   const uint64_t diff = kmin ^ kmax;
-  int shift = diff == 0 ? 8 : ((63 - __builtin_clzll(diff)) / 8 + 1) * 8;
+  int shift = diff == 0 ? 1 : 64 - __builtin_clzll(diff);  // bits [0, shift) differ
   uint64_t prefix = (shift >= 64) ? 0 : (kmax >> shift) << shift;
   uint32_t kr = k_eff;
   while (shift > 0 && kr < (uint32_t)n) {
-    shift -= 8;
+    const int top = shift;  // keys still in play share every bit at or above top
+    const int width = top < 8 ? top : 8;
+    shift = top - width;
     reinterpret_cast<uint4*>(hist)[lane] = make_uint4(0u, 0u, 0u, 0u);
     __syncthreads();
-    const uint64_t pre_hi = shift + 8 >= 64 ? 0 : prefix >> (shift + 8);
+    const uint64_t pre_hi = top >= 64 ? 0 : prefix >> top;
+    const uint32_t dmask = (1u << width) - 1u;
 #pragma unroll
     for (int e = 0; e < E; ++e) {
-      const bool match = lane + 64 * e < n && (shift + 8 >= 64 || (key[e] >> (shift + 8)) == pre_hi);
-      if (match) atomicAdd(&hist[(uint32_t)(key[e] >> shift) & 255u], 1u);
+      const bool match = lane + 64 * e < n && (top >= 64 || (key[e] >> top) == pre_hi);
+      if (match) atomicAdd(&hist[(uint32_t)(key[e] >> shift) & dmask], 1u);
     }
     __syncthreads();
     const uint4 h4 = reinterpret_cast<const uint4*>(hist)[63 - lane];  // bins 255-4l .. 252-4l

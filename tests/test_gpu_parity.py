@@ -367,3 +367,47 @@ def test_one_chunk_per_pass_is_bit_identical(base, kw, path):
     for a, b in zip(ref, got):
         assert torch.equal(bits(a), bits(b))
     parity.check_attn(w, x, got[0], got[1])
+
+
+# Ties: every score of a row equal (Q = 0), so the total order (score desc, index asc)
+# keeps the k lowest valid key indices, in increasing order; and scores confined to a
+# narrow band (Q scaled down), where the keys of the candidates share their top bits
+# and differ only low in the score or in the index.
+TIE_CASES = [
+    ("c3", dict(H=2, Lq=300, Lk=6000, chunk=256), 1),        # fused path, sampled threshold
+    ("c2", dict(B=1, H=2, Lq=200, Lk=512, chunk=128), 1),     # fused path, every key a candidate
+    ("c4", dict(B=1, H=2, Lq=300, Lk=4096, chunk=128), 4),    # filtered chunk-tile path (causal)
+    ("c5", dict(N=200, d_model=256, d_ff=3000, k=256, chunk=64), 4),  # filtered chunk-tile (FFN)
+    ("c1", dict(Lq=200, Lk=700, chunk=64), 2),                # chunk-tile path, fp32
+]
+
+
+@pytest.mark.parametrize("base,kw,path", TIE_CASES)
+@pytest.mark.parametrize("band", [0.0, 1e-3])
+def test_ties_keep_the_lowest_indices(base, kw, path, band):
+    w = wl.WORKLOADS[base].scaled(**kw)
+    _say("ties", band, w)
+    x = wl.make_inputs(w)
+    qn = "Q" if w.kind == "attn" else "X"
+    x[qn] = wl._store((x[qn].values * np.float32(band)).astype(np.float32), w.dtype)
+    if w.kind == "attn":
+        assert tk.attn_path(w.B, w.H, w.Lq, w.Lk, w.d, w.k, w.chunk, w.causal,
+                            tk.TOPK_BF16 if w.dtype == wl.BF16 else tk.TOPK_F32) == path
+        out, idx, sc = parity.run_attn(w, x)
+        rep = {}
+        parity.check_attn(w, x, out, idx, report=rep)
+    else:
+        assert tk.ffn_path(w.N, w.d_model, w.d_ff, w.k, w.chunk) == path
+        out, idx, sc = parity.run_ffn(w, x)
+        rep = {}
+        parity.check_ffn(w, x, out, idx, report=rep)
+    _say("ties", band, "ok", rep)
+    if band == 0.0:  # all scores 0: the lowest valid indices, ascending
+        g = idx.cpu().numpy().reshape(-1, w.k)
+        L = w.Lq if w.kind == "attn" else w.N
+        rows = np.arange(g.shape[0]) % L
+        nvalid = np.minimum(rows + 1, w.Lk) if (w.kind == "attn" and w.causal) else np.full(g.shape[0], w.Lk if w.kind == "attn" else w.d_ff)
+        k_eff = np.minimum(w.k, nvalid)
+        want = np.where(np.arange(w.k)[None, :] < k_eff[:, None], np.arange(w.k)[None, :], -1)
+        assert np.array_equal(g, want), f"first bad row {int(np.argmax(np.any(g != want, axis=1)))}"
+        assert np.all(sc.cpu().numpy().reshape(-1, w.k)[want >= 0] == 0.0)
