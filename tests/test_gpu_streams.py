@@ -55,3 +55,40 @@ def test_two_streams_match_serial_results():
             for i, (x, y) in enumerate(zip(got, ref)):
                 assert torch.equal(x, y), f"stream result {name}[{i}] differs in repetition {rep}"
     _say("streams ok")
+
+
+def test_two_host_threads_match_serial_results():
+    """Two host threads, each on a stream of its own (the workspace registration and the
+    last-error message are per thread)."""
+    import threading
+    wa, (qa, ka, va) = _attn_inputs("c3", H=2, Lq=512, Lk=4096, chunk=256)
+    wb, (qb, kb, vb) = _attn_inputs("c2", B=2, H=3, Lq=384, Lk=512, chunk=128)
+    ga = parity.to_dev(parity.grad_out((wa.B, wa.H, wa.Lq, wa.d), wa.dtype, 92))
+    gb = parity.to_dev(parity.grad_out((wb.B, wb.H, wb.Lq, wb.d), wb.dtype, 93))
+    refs = {"a": _forward_backward(wa, qa, ka, va, ga), "b": _forward_backward(wb, qb, kb, vb, gb)}
+    torch.cuda.synchronize()
+    results, errors = {}, []
+
+    def work(name, w, q, k, v, g):
+        try:
+            s = torch.cuda.Stream()
+            with torch.cuda.stream(s):
+                outs = [_forward_backward(w, q, k, v, g) for _ in range(3)]
+            s.synchronize()
+            results[name] = outs
+        except Exception as e:  # reported by the main thread
+            errors.append(f"{name}: {e!r}")
+
+    threads = [threading.Thread(target=work, args=("a", wa, qa, ka, va, ga)),
+               threading.Thread(target=work, args=("b", wb, qb, kb, vb, gb))]
+    for t in threads:
+        t.start()
+    for t in threads:
+        t.join(timeout=60)
+    assert not errors, errors
+    for name, outs in results.items():
+        for rep, got in enumerate(outs):
+            for i, (x, y) in enumerate(zip(got, refs[name])):
+                assert torch.equal(x, y), f"thread {name} result {i} differs in repetition {rep}"
+    assert set(results) == {"a", "b"}
+    _say("threads ok")
