@@ -619,9 +619,9 @@ __global__ __launch_bounds__(256) void k_tile_select(Problem pb, Pass ps, const 
 
 // ------------------------------------------------------------------ fused path: scan
 // One workgroup = 4 waves x 32*G queries of one head (G = 2). Each wave keeps the B operand
-// of G 32-query column groups in registers; key tiles of 64 keys stream through a
-// ring of SCAN_NB LDS buffers that are filled by direct global-to-LDS loads issued
-// SCAN_NB - 1 tiles ahead (no register staging). Each wave computes S^T = K Q^T
+// of G 32-query column groups in registers; key tiles of 64 keys stream through two
+// LDS buffers that are filled by direct global-to-LDS loads issued one tile ahead
+// (no register staging). Each wave computes S^T = K Q^T
 // with v_mfma_f32_32x32x16_bf16, so lane l holds 16 keys' scores of query l % 32 of
 // a group (keys 8*(v/4) + 4*(l/32) + v%4 of the 32-key block, v = 0..15); one LDS
 // read of the K operand feeds all G groups. The feature dimension is split between
@@ -652,10 +652,10 @@ struct ScanArgs {
 
 constexpr int SCAN_KT = 64;  // keys per K tile
 
-// Launch shape of the scan: G = 32-query groups per wave, NB = K tiles resident
-// in the LDS ring, CAP = staged 8-score half blocks per wave (a wave drains its ring
-// when the next block's dirty lanes would not fit, so a drain is one 64-lane
-// round), OCC = waves per SIMD the register and LDS sizes allow (36 KB of LDS per
+// Launch shape of the scan: G = 32-query groups per wave, NB = K tile buffers in
+// LDS, CAP = staged 8-score half blocks per wave (whole 64-slot rounds drain at
+// tile boundaries; a block whose dirty lanes would not fit drains the ring first),
+// OCC = waves per SIMD the register and LDS sizes allow (37 KB of LDS per
 // workgroup: four workgroups per CU).
 template <int G>
 struct ScanShape;
@@ -681,7 +681,11 @@ __global__ __launch_bounds__(256, ScanShape<G>::OCC) void k_fused_scan(ScanArgs 
   constexpr int LPW = TILEB / 1024 / 4;   // 1 KB direct loads per wave per tile
   constexpr int QB = scan_queries_per_wg<G>();
   static_assert(LPW >= 1 && TILEB % 4096 == 0, "tile must split evenly over the 4 waves");
-  __shared__ __attribute__((aligned(16))) unsigned char ks[SCAN_NB][TILEB];
+  // the two K tile buffers, used alternately; as two arrays (not one indexed array) so
+  // that every access below names its buffer at compile time
+  static_assert(SCAN_NB == 2, "two K tile buffers");
+  __shared__ __attribute__((aligned(16))) unsigned char ks0[TILEB];
+  __shared__ __attribute__((aligned(16))) unsigned char ks1[TILEB];
   // staging slot = 8 scores: one dirty half of a lane block, as two 16-byte chunks
   // held in separate arrays (chunk c of slot s at stage[wave][c][s]), so the writes
   // and reads of consecutive slots by consecutive lanes are free of bank conflicts
@@ -726,38 +730,44 @@ __global__ __launch_bounds__(256, ScanShape<G>::OCC) void k_fused_scan(ScanArgs 
 #pragma unroll
   for (int g = 0; g < G; ++g) cnt_lds[wave][g * 64 + lane] = 0;
 
-  // direct loads of tile t into ring buffer buf: lane `lane` of this wave's j-th
-  // load fills LDS position cidx = (wave*LPW + j)*64 + lane with part
+  // direct loads of tile t into buffer dst: lane `lane` of this wave's j-th load
+  // fills LDS position cidx = (wave*LPW + j)*64 + lane with part
   // (cidx % CH) ^ (row & 7) of key row cidx / CH (rows past Lk load the last key;
   // their scores are masked)
-  auto issue = [&](int64_t t, int buf) {
+  auto issue = [&](int64_t t, unsigned char* dst) {
 #pragma unroll
     for (int j = 0; j < LPW; ++j) {
       const int cidx = (wave * LPW + j) * 64 + lane, r = cidx / CH, p = (cidx % CH) ^ (r & 7);
       int64_t key = t * KT + r;
       key = key < a.Lk ? key : a.Lk - 1;
       __builtin_amdgcn_global_load_lds((const void*)(Kh + key * D + p * 8),
-                                       (__attribute__((address_space(3))) void*)&ks[buf][(wave * LPW + j) * 1024], 16,
+                                       (__attribute__((address_space(3))) void*)&dst[(wave * LPW + j) * 1024], 16,
                                        0, 0);
     }
   };
-  // Runs body(tile, lds) over tiles 0, step, 2*step, ... (count of them) with
-  // SCAN_NB - 1 tiles in flight. Before tile t is read, this wave's loads of t are
-  // complete (with a ring of three only the loads of t + 1 may still be
-  // outstanding; loads complete in order) and the barrier publishes every wave's
-  // part; the barrier also proves that no wave still reads the buffer the next
-  // load overwrites.
+  // Runs step_fn(t, cur, nxt) for t = 0 .. count - 1 with the buffers alternating,
+  // unrolled by two so that each call names its buffers at compile time: the
+  // compiler then knows that reads of one buffer do not overlap the direct loads
+  // into the other, and does not make them wait for those loads.
+  auto alternate = [&](int64_t count, auto&& step_fn) {
+    for (int64_t t = 0; t < count; t += 2) {
+      step_fn(t, ks0, ks1);
+      if (t + 1 < count) step_fn(t + 1, ks1, ks0);
+    }
+  };
+  // Runs body(tile, lds) over tiles 0, step, 2*step, ... (count of them) with one
+  // tile in flight. Before tile t is read, this wave's loads of t are complete and
+  // the barrier publishes every wave's part; the barrier also proves that no wave
+  // still reads the buffer the next load overwrites.
   auto pipeline = [&](int64_t count, int64_t step, auto&& body) {
     if (count <= 0) return;
-    static_assert(SCAN_NB == 2 || SCAN_NB == 3, "ring of two or three tiles");
-    for (int i = 0; i < SCAN_NB - 1 && i < count; ++i) issue(i * step, i);
-    for (int64_t t = 0; t < count; ++t) {
-      if (SCAN_NB == 3 && t + 1 < count) __builtin_amdgcn_s_waitcnt(TOPK_WAIT_VM(LPW));
-      else __builtin_amdgcn_s_waitcnt(TOPK_WAIT_VM(0));
+    issue(0, ks0);
+    alternate(count, [&](int64_t t, const unsigned char* cur, unsigned char* nxt) {
+      __builtin_amdgcn_s_waitcnt(TOPK_WAIT_VM(0));
       __syncthreads();
-      if (t + SCAN_NB - 1 < count) issue((t + SCAN_NB - 1) * step, (int)((t + SCAN_NB - 1) % SCAN_NB));
-      body(t * step, &ks[t % SCAN_NB][0]);
-    }
+      if (t + 1 < count) issue((t + 1) * step, nxt);
+      body(t * step, cur);
+    });
     __syncthreads();
   };
   // scores of 32 keys (block rb of the tile) for all G query groups
@@ -947,48 +957,32 @@ __global__ __launch_bounds__(256, ScanShape<G>::OCC) void k_fused_scan(ScanArgs 
     }
     rtail += n1 + n2;
   };
-  // Main scan: a stream of 32-key blocks. When a block opens a new tile, that
-  // tile's wait and barrier (and the loads of the tile SCAN_NB - 1 further on,
-  // into the buffer of the tile just finished) come first.
-  {
-    const int64_t nblocks = ntiles * NRB;
-    auto open_tile = [&](int64_t t) {
-      if (SCAN_NB == 3 && t + 1 < ntiles) __builtin_amdgcn_s_waitcnt(TOPK_WAIT_VM(LPW));
-      else __builtin_amdgcn_s_waitcnt(TOPK_WAIT_VM(0));
-      __syncthreads();
-      if (t + SCAN_NB - 1 < ntiles) issue(t + SCAN_NB - 1, (int)((t + SCAN_NB - 1) % SCAN_NB));
-    };
-    auto compute = [&](int64_t blkno, f32x16 (&acc)[G]) {
-      const int64_t t = blkno / NRB;
-      const int rb = (int)(blkno - t * NRB);
-      block_scores(&ks[t % SCAN_NB][0], rb, acc);
+  // Main scan: tile by tile. A tile's wait and barrier, and the loads of the next
+  // tile into the other buffer, come first; then its 32-key blocks.
+  issue(0, ks0);
+  alternate(ntiles, [&](int64_t t, const unsigned char* cur, unsigned char* nxt) {
+    __builtin_amdgcn_s_waitcnt(TOPK_WAIT_VM(0));
+    __syncthreads();
+    // drain whole 64-slot rounds at the tile boundary, before the next tile's loads
+    // are issued: the drain's LDS counter updates then have no direct loads to wait
+    // for, and its candidate stores complete while this tile is computed instead of
+    // delaying a later wait
+    if (t > 0 && rtail - rhead >= 64) drain_to(rhead + ((rtail - rhead) & ~63));
+    if (t + 1 < ntiles) issue(t + 1, nxt);
+#pragma unroll
+    for (int rb = 0; rb < NRB; ++rb) {
+      f32x16 x[G];
+      block_scores(cur, rb, x);
       if (tail && t == ntiles - 1) {
         const int64_t jb = t * KT + rb * 32 + 4 * half;
 #pragma unroll
-        for (int g = 0; g < G; ++g) mask_keys(acc[g], jb);
+        for (int g = 0; g < G; ++g) mask_keys(x[g], jb);
       }
-      mask_future(acc, t, rb);
-    };
-    for (int i = 0; i < SCAN_NB - 1 && i < ntiles; ++i) issue(i, i);
-    open_tile(0);
-    auto filter_all = [&](const f32x16 (&acc)[G], int64_t blkno) {
-      const int64_t t = blkno / NRB;
+      mask_future(x, t, rb);
 #pragma unroll
-      for (int g = 0; g < G; ++g) filter(g, acc[g], t, (int)(blkno - t * NRB));
-    };
-    for (int64_t blkno = 0; blkno < nblocks; ++blkno) {
-      if (blkno > 0 && blkno % NRB == 0) {
-        open_tile(blkno / NRB);
-        // drain whole 64-slot rounds right after the next tile's loads are issued:
-        // the candidate stores then complete while this tile is computed, instead
-        // of delaying the wait for the next tile's loads
-        if (rtail - rhead >= 64) drain_to(rhead + ((rtail - rhead) & ~63));
-      }
-      f32x16 x[G];
-      compute(blkno, x);
-      filter_all(x, blkno);
+      for (int g = 0; g < G; ++g) filter(g, x[g], t, rb);
     }
-  }
+  });
   drain();
 #pragma unroll
   for (int g = 0; g < G; ++g)
