@@ -103,16 +103,22 @@ __device__ __forceinline__ uint32_t team_excl_scan(uint32_t x, uint32_t* tmp) {
   return base + incl - x;
 }
 
+// Digits a sampled threshold resolves: the sign, the exponent and the top 7 bits of the
+// mantissa of the R-th largest sample (finer resolution only trims a few candidates).
+constexpr int THRESH_PASSES = 2;
+
 // Exact radix select of the k_eff largest keys among n (distinct) 64-bit keys,
 // 8 bits per pass from the top. On return the selected set is exactly
-// { key : (key >> shift) >= (prefix >> shift) }.
+// { key : (key >> shift) >= (prefix >> shift) }. With max_passes < 8 it stops early
+// and the set holds the k_eff largest keys and possibly more (the rest of the last
+// digit's bucket), which is all a threshold needs.
 template <int NT, class GetKey>
 __device__ void team_radix_select(const GetKey& getkey, int64_t n, uint32_t k_eff, uint32_t* hist,
-                                  uint32_t* misc, int* shift_out, uint64_t* prefix_out) {
+                                  uint32_t* misc, int* shift_out, uint64_t* prefix_out, int max_passes = 8) {
   uint64_t prefix = 0;
   int shift = 64;
   uint32_t kr = k_eff;
-  for (int pass = 0; pass < 8; ++pass) {
+  for (int pass = 0; pass < max_passes; ++pass) {
     shift -= 8;
     for (int b = threadIdx.x; b < 256; b += NT) hist[b] = 0;
     __syncthreads();
@@ -1093,10 +1099,12 @@ __device__ __forceinline__ void wave_sort_store(const uint64_t* sbuf, uint32_t k
 // Radix select on n <= E * 64 distinct keys held in registers (key[e] is element
 // e*64 + lane; elements >= n are ignored). Returns (shift, prefix): the k_eff
 // largest keys are exactly those with (key >> shift) >= (prefix >> shift). The
-// block is one wave (hist: 256 words of LDS).
+// block is one wave (hist: 256 words of LDS). With max_passes, the select stops after
+// that many digits: the set then holds the k_eff largest keys and possibly more (the
+// rest of the last digit's bucket), which is all a threshold needs.
 template <int E>
 __device__ __forceinline__ void wave_radix_select(const uint64_t (&key)[E], int n, uint32_t k_eff, uint32_t* hist,
-                                                  int* shift_out, uint64_t* prefix_out) {
+                                                  int* shift_out, uint64_t* prefix_out, int max_passes = 8) {
   const int lane = threadIdx.x & 63;
   uint64_t kmin = ~0ull, kmax = 0ull;
 #pragma unroll
@@ -1120,7 +1128,7 @@ __device__ __forceinline__ void wave_radix_select(const uint64_t (&key)[E], int 
   int shift = diff == 0 ? 1 : 64 - __builtin_clzll(diff);  // bits [0, shift) differ
   uint64_t prefix = (shift >= 64) ? 0 : (kmax >> shift) << shift;
   uint32_t kr = k_eff;
-  while (shift > 0 && kr < (uint32_t)n) {
+  for (int pass = 0; pass < max_passes && shift > 0 && kr < (uint32_t)n; ++pass) {
     const int top = shift;  // keys still in play share every bit at or above top
     const int width = top < 8 ? top : 8;
     shift = top - width;
@@ -1253,8 +1261,9 @@ __global__ __launch_bounds__(64) void k_cand_select(Problem pb, Pass ps, PassBuf
 // ------------------------------------------------------------------ filtered chunk-tile path
 // Per row, the threshold is the R-th largest of its valid sampled scores (every
 // FILTER_KSTRIDE-th key), R a few standard deviations above the sample's expected
-// share mu of the top k_eff. About R * FILTER_KSTRIDE scores of the row are then at
-// or above it; a row with fewer than R valid samples keeps every valid key. The
+// share mu of the top k_eff, resolved to THRESH_PASSES radix digits (it may lie a
+// little below that sample, never above). About R * FILTER_KSTRIDE scores of the row
+// are then at or above it; a row with fewer than R valid samples keeps every valid key. The
 // candidate select proves each row's set complete (at least k_eff entries, no
 // overflow) or sends the row to the exact fallback.
 __global__ __launch_bounds__(64) void k_filter_threshold(Problem pb, Pass ps, PassBufs bufs) {
@@ -1271,7 +1280,7 @@ __global__ __launch_bounds__(64) void k_filter_threshold(Problem pb, Pass ps, Pa
   float ts = -INFINITY;
   if (R < ns) {
     const float* row = bufs.samp + p * ((pb.Lk + FILTER_KSTRIDE - 1) / FILTER_KSTRIDE);
-    auto rth = [&](auto tag) {  // the R-th largest of the row's ns samples
+    auto rth = [&](auto tag) {  // the R-th largest of the row's ns samples, or a little less
       constexpr int E = decltype(tag)::value;
       uint64_t key[E];
 #pragma unroll
@@ -1281,7 +1290,7 @@ __global__ __launch_bounds__(64) void k_filter_threshold(Problem pb, Pass ps, Pa
       }
       int shift;
       uint64_t prefix;
-      wave_radix_select<E>(key, (int)ns, (uint32_t)R, hist, &shift, &prefix);
+      wave_radix_select<E>(key, (int)ns, (uint32_t)R, hist, &shift, &prefix, THRESH_PASSES);
       uint32_t m = 0xFFFFFFFFu;
 #pragma unroll
       for (int e = 0; e < E; ++e)
@@ -1316,10 +1325,10 @@ __global__ __launch_bounds__(256) void k_filter_threshold_wg(Problem pb, Pass ps
     auto getkey = [&](int64_t e) { return make_key(row[e], (uint32_t)e); };
     int shift;
     uint64_t prefix;
-    team_radix_select<256>(getkey, ns, (uint32_t)R, hist, misc, &shift, &prefix);
+    team_radix_select<256>(getkey, ns, (uint32_t)R, hist, misc, &shift, &prefix, THRESH_PASSES);
     if (threadIdx.x == 0) lowest = 0xFFFFFFFFu;
     __syncthreads();
-    uint32_t m = 0xFFFFFFFFu;  // the smallest selected score: the R-th largest sample
+    uint32_t m = 0xFFFFFFFFu;  // the smallest selected score: at most the R-th largest sample
     for (int64_t e = threadIdx.x; e < ns; e += 256) {
       const uint64_t key = getkey(e);
       if ((key >> shift) >= (prefix >> shift)) m = min(m, (uint32_t)(key >> 32));
@@ -1362,9 +1371,10 @@ hipError_t launch_filter(const Problem& pb, const Pass& ps, const PassBufs& b, i
 //  * rows of at most 64 * CAND_REGS keys take every key;
 //  * longer rows take every score >= ts, ts being the R-th largest of
 //    64 * CAND_REGS evenly spaced sampled scores, R a few standard deviations
-//    above the sample's expected share of the top k. For R <= 96 (long rows) ts
-//    is the R-th largest of the per-lane top two of the sample, which leaves at
-//    least R sampled scores >= ts at a fraction of the cost;
+//    above the sample's expected share of the top k, resolved to THRESH_PASSES
+//    radix digits (it may lie a little below that sample, never above). For
+//    R <= 96 (long rows) ts comes from the per-lane top two of the sample, which
+//    leaves at least R sampled scores >= ts at a fraction of the cost;
 //  * a row whose gathered set is short of k_eff keys or overflows goes to the
 //    redo list (exact fallback from the tile row).
 constexpr int TSW_MAX_N = 8192;
@@ -1417,7 +1427,7 @@ __global__ __launch_bounds__(64) void k_tile_select_wave(Problem pb, Pass ps, co
         t2 = fmaxf(t2, lo);
       }
       uint64_t k2[2] = {make_key(t1, 2u * lane), make_key(t2, 2u * lane + 1u)};
-      wave_radix_select<2>(k2, 128, (uint32_t)R, hist, &shift, &prefix);
+      wave_radix_select<2>(k2, 128, (uint32_t)R, hist, &shift, &prefix, THRESH_PASSES);
       uint32_t m = 0xFFFFFFFFu;
 #pragma unroll
       for (int e = 0; e < 2; ++e)
@@ -1428,7 +1438,7 @@ __global__ __launch_bounds__(64) void k_tile_select_wave(Problem pb, Pass ps, co
       uint64_t key[CAND_REGS];
 #pragma unroll
       for (int e = 0; e < CAND_REGS; ++e) key[e] = make_key(smp[e], (uint32_t)(lane + 64 * e));
-      wave_radix_select<CAND_REGS>(key, CAPW, (uint32_t)R, hist, &shift, &prefix);
+      wave_radix_select<CAND_REGS>(key, CAPW, (uint32_t)R, hist, &shift, &prefix, THRESH_PASSES);
       uint32_t m = 0xFFFFFFFFu;
 #pragma unroll
       for (int e = 0; e < CAND_REGS; ++e)
