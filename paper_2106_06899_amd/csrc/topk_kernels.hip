@@ -664,7 +664,9 @@ constexpr int SCAN_KT = 64;  // keys per K tile
 // OCC = waves per SIMD the register and LDS sizes allow (37 KB of LDS per
 // workgroup: four workgroups per CU); OCC_CAUSAL = the same under the causal mask,
 // whose extra registers would spill at four waves per SIMD (three waves without
-// spills measured 20 % faster).
+// spills measured 20 % faster). For d = 128 (twice the registers for the queries'
+// operand, 53 KB of LDS) the kernel asks for two waves per SIMD only, so that the
+// compiler never spills to reach more; it gets three where its registers allow.
 template <int G>
 struct ScanShape;
 template <>
@@ -677,7 +679,8 @@ constexpr int scan_queries_per_wg() { return 4 * 32 * G; }
 
 
 template <int D, int R, int G, bool CAUSAL>
-__global__ __launch_bounds__(256, CAUSAL ? ScanShape<G>::OCC_CAUSAL : ScanShape<G>::OCC) void k_fused_scan(ScanArgs a) {
+__global__ __launch_bounds__(256, D == 64 ? (CAUSAL ? ScanShape<G>::OCC_CAUSAL : ScanShape<G>::OCC) : 2) void k_fused_scan(
+    ScanArgs a) {
   static_assert(ScanShape<G>::CAP >= 128, "a ring holds one block's 64 lanes, both halves");
   constexpr int SCAN_NB = ScanShape<G>::NB;
   constexpr int STAGE_CAP = ScanShape<G>::CAP;
