@@ -1224,7 +1224,7 @@ __device__ __forceinline__ void cand_select_regs(const uint64_t* b0, const uint6
 // BIG: rows of up to 2048 candidates and k <= 512 (the filtered path's larger lists)
 template <bool BIG>
 __device__ __forceinline__ void cand_select_row(const Problem& pb, const Pass& ps, const PassBufs& bufs, int64_t p,
-                                                uint64_t* sbuf, uint32_t* hist) {
+                                                uint64_t* sbuf, uint32_t* hist, uint32_t* misc) {
   constexpr int KCAP = BIG ? 512 : 256, NMAX = BIG ? 128 * CAND_REGS : 64 * CAND_REGS;
   const RowRef rr = row_of(pb, ps, p);
   if (!rr.ok) return;
@@ -1246,7 +1246,12 @@ __device__ __forceinline__ void cand_select_row(const Problem& pb, const Pass& p
     if (n <= 128) cand_select_regs<2>(b0, b0 + bufs.caph, (int)c0, n, k_eff, pb.k, sbuf, hist, out);
     else if (n <= 256) cand_select_regs<4>(b0, b0 + bufs.caph, (int)c0, n, k_eff, pb.k, sbuf, hist, out);
     else if (n <= 512) cand_select_regs<8>(b0, b0 + bufs.caph, (int)c0, n, k_eff, pb.k, sbuf, hist, out);
-    else cand_select_regs<CAND_REGS>(b0, b0 + bufs.caph, (int)c0, n, k_eff, pb.k, sbuf, hist, out);
+    else {
+      // rare long lists: the exact select over the words where they are (global
+      // memory), so that the common short lists keep few registers (more waves)
+      auto getkey = [&](int64_t e) { return raw_to_key(e < c0 ? b0[e] : b0[bufs.caph + (e - c0)]); };
+      team_topk<64>(getkey, n, k_eff, (uint32_t)pb.k, sbuf, pow2_at_least(k_eff), hist, misc, out);
+    }
   } else {
     if (n <= 512) cand_select_regs<8, KCAP>(b0, b0 + bufs.caph, (int)c0, n, k_eff, pb.k, sbuf, hist, out);
     else if (n <= 1024) cand_select_regs<CAND_REGS, KCAP>(b0, b0 + bufs.caph, (int)c0, n, k_eff, pb.k, sbuf, hist, out);
@@ -1258,7 +1263,8 @@ template <bool BIG>
 __global__ __launch_bounds__(64) void k_cand_select(Problem pb, Pass ps, PassBufs bufs) {
   __shared__ uint64_t sbuf[BIG ? 512 : 256];
   __shared__ uint32_t hist[256];
-  cand_select_row<BIG>(pb, ps, bufs, blockIdx.x, sbuf, hist);
+  __shared__ uint32_t misc[8];
+  cand_select_row<BIG>(pb, ps, bufs, blockIdx.x, sbuf, hist, misc);
 }
 
 // ------------------------------------------------------------------ filtered chunk-tile path

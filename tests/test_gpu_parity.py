@@ -49,6 +49,8 @@ ATTN_CASES = {
     "c1_fp32_tile": ("c1", dict(Lq=300, Lk=777, chunk=100)),
     "c2_bf16_fused_all": ("c2", dict(B=2, H=3, Lq=200, Lk=512, chunk=128)),
     "c2_bf16_fused_all_ragged": ("c2", dict(B=1, H=2, Lq=130, Lk=333, chunk=64)),
+    # every key a candidate and more than 512 of them: the select's long-list path
+    "c2_bf16_fused_all_long_lists": ("c2", dict(B=1, H=2, Lq=150, Lk=1000, chunk=64)),
     "c3_bf16_fused_sample": ("c3", dict(H=2, Lq=300, Lk=9000, chunk=256)),
     "c3_bf16_fused_sample_k32": ("c3", dict(H=1, Lq=257, Lk=4600, k=32, chunk=1024)),
     "c4_bf16_causal_tile": ("c4", dict(B=1, H=2, Lq=600, Lk=600, chunk=256)),
