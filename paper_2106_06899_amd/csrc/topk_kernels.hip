@@ -2463,7 +2463,10 @@ __global__ __launch_bounds__(256) void k_bwd_bucket_lists(BwdProblem bp, BwdLayo
   }
 }
 
-template <typename T, int NCL>
+// SORTED: the lists come from the atomic counters (unordered), and lists of up to 1024
+// pairs are sorted first; the bucket-sorted lists need no sort, and their kernel then
+// carries none of the sort's registers.
+template <typename T, int NCL, bool SORTED>
 __global__ __launch_bounds__(256) void k_bwd_keys(BwdProblem bp, BwdBufs b) {
   constexpr int EPC = RowChunks<T>::EPC, U = BWD_UNROLL;
   __shared__ int32_t lst[4][1024];
@@ -2539,7 +2542,7 @@ __global__ __launch_bounds__(256) void k_bwd_keys(BwdProblem bp, BwdBufs b) {
     wave_sync_lds();
     accumulate([&](int e) { return lst[wave][e]; });
   };
-  if (b.L.bucketed) accumulate([&](int e) { return b.list[beg + e]; });
+  if (!SORTED) accumulate([&](int e) { return b.list[beg + e]; });
   else if (n <= 64) sorted(std::integral_constant<int, 1>{});
   else if (n <= 128) sorted(std::integral_constant<int, 2>{});
   else if (n <= 256) sorted(std::integral_constant<int, 4>{});
@@ -2597,7 +2600,19 @@ hipError_t launch_backward(const BwdProblem& bp, const BwdBufs& b, hipStream_t s
     const int64_t gf = (npairs + 255) / 256;
     k_bwd_fill<<<(unsigned)(gf < 65536 ? gf : 65536), 256, 0, st>>>(bp, b);
   }
-  TOPK_BWD(k_bwd_keys, grid_keys)
+#define TOPK_BWD_KEYS(SORTED)                                                                             \
+  if (bp.dtype == T_BF16 && ncl == 1) k_bwd_keys<uint16_t, 1, SORTED><<<grid_keys, 256, 0, st>>>(bp, b);      \
+  else if (bp.dtype == T_BF16 && ncl == 2) k_bwd_keys<uint16_t, 2, SORTED><<<grid_keys, 256, 0, st>>>(bp, b); \
+  else if (bp.dtype == T_F32 && ncl == 1) k_bwd_keys<float, 1, SORTED><<<grid_keys, 256, 0, st>>>(bp, b);     \
+  else if (bp.dtype == T_F32 && ncl == 2) k_bwd_keys<float, 2, SORTED><<<grid_keys, 256, 0, st>>>(bp, b);     \
+  else if (bp.dtype == T_F32 && ncl == 4) k_bwd_keys<float, 4, SORTED><<<grid_keys, 256, 0, st>>>(bp, b);     \
+  else return hipErrorInvalidValue;
+  if (L.bucketed) {
+    TOPK_BWD_KEYS(false)
+  } else {
+    TOPK_BWD_KEYS(true)
+  }
+#undef TOPK_BWD_KEYS
 #undef TOPK_BWD
   return hipGetLastError();
 }
