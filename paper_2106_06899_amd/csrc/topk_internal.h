@@ -17,6 +17,7 @@ enum ScanMode { MODE_ALL = 0, MODE_SAMPLE = 1 };
 constexpr int REDO_CAP = 1024;          // redo rows recomputed by the wide fallback kernels
 constexpr int REDO_SPLIT = 512;         // keys per work item of the wide fallback
 constexpr int REDO_SCORE_BLOCKS = 1024; // workgroups of the wide fallback's score kernel
+constexpr int64_t FINALIZE_SLICE_BYTES = (int64_t)8 << 20;  // value matrices above this gather in column slices
 constexpr int REDO_BLOCKS = 64;         // workgroups of the fallback for rows beyond REDO_CAP
 constexpr int MAX_SELECT_K = 2048;  // largest k the workgroup select / finalize handle
 

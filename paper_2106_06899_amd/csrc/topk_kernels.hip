@@ -1650,9 +1650,33 @@ template <> struct Vec16<float> {
   }
 };
 
-template <typename T>
+// Reorders a row's n <= 64 * E (weight, key index) pairs in LDS by increasing key
+// index (the indices are distinct), through the register bitonic network.
+template <int E>
+__device__ __forceinline__ void sort_by_key_index(float* w, uint32_t* jj, int n) {
+  const int lane = threadIdx.x & 63;
+  uint64_t r[E];
+#pragma unroll
+  for (int e = 0; e < E; ++e) {
+    const int t = e * 64 + lane;  // descending on ~index = ascending on index; pads (0) go last
+    r[e] = t < n ? ((uint64_t)(~jj[t]) << 32) | __float_as_uint(w[t]) : 0ull;
+  }
+  wave_sort_desc<E>(r);
+  __syncthreads();
+#pragma unroll
+  for (int e = 0; e < E; ++e) {
+    const int t = e * 64 + lane;
+    if (t < n) {
+      jj[t] = ~(uint32_t)(r[e] >> 32);
+      w[t] = __uint_as_float((uint32_t)r[e]);
+    }
+  }
+  __syncthreads();
+}
+
+template <typename T, int NSLICES>
 __device__ __forceinline__ void finalize_row(const Problem& pb, const Pass& ps, const uint64_t* sel, int64_t p,
-                                             float* w, uint32_t* jj) {
+                                             float* w, uint32_t* jj, int slice) {
   constexpr int E = Vec16<T>::E;
   const RowRef rr = row_of(pb, ps, p);
   if (!rr.ok) return;
@@ -1672,8 +1696,10 @@ __device__ __forceinline__ void finalize_row(const Problem& pb, const Pass& ps, 
       w[t] = s;
       jj[t] = (uint32_t)j < jmax ? (uint32_t)j : jmax;  // keeps a bad selection from reading out of bounds
     }
-    if (pb.idx_out) pb.idx_out[grow * pb.k + t] = j;
-    if (pb.score_out) pb.score_out[grow * pb.k + t] = s;
+    if (slice == 0) {
+      if (pb.idx_out) pb.idx_out[grow * pb.k + t] = j;
+      if (pb.score_out) pb.score_out[grow * pb.k + t] = s;
+    }
   }
   __syncthreads();
   float inv = 1.f;
@@ -1693,14 +1719,23 @@ __device__ __forceinline__ void finalize_row(const Problem& pb, const Pass& ps, 
     for (int64_t t = lane; t < k_eff; t += 64) w[t] = fmaxf(w[t], 0.f);
   }
   __syncthreads();
+  if (NSLICES > 1 && k_eff > 1 && k_eff <= 512) {
+    // wide value rows: gather the survivors in increasing key order, so that the
+    // waves sharing an XCD walk its slice of the value matrix in the same direction
+    if (k_eff <= 64) sort_by_key_index<1>(w, jj, (int)k_eff);
+    else if (k_eff <= 128) sort_by_key_index<2>(w, jj, (int)k_eff);
+    else if (k_eff <= 256) sort_by_key_index<4>(w, jj, (int)k_eff);
+    else sort_by_key_index<8>(w, jj, (int)k_eff);
+  }
   const T* Vh = (const T*)pb.V + rr.bh * pb.kv_head_stride;
   T* orow = (T*)pb.out + grow * pb.d;
-  const int nvec = (int)(pb.d / E);                 // 16-byte vectors per value row
+  const int nvec = (int)(pb.d / E) / NSLICES;      // 16-byte vectors of this slice per value row
+  const int vbeg = slice * nvec, vend = vbeg + nvec;
   int np2 = 1;                                      // lanes per row slot: a power of two >= nvec
   while (np2 < nvec && np2 < 64) np2 <<= 1;
   const int slots = 64 / np2;                       // rows gathered per instruction
   const int vlane = lane % np2, slot = lane / np2;
-  for (int v0 = vlane; v0 < nvec; v0 += 64) {
+  for (int v0 = vbeg + vlane; v0 < vend; v0 += 64) {
     float acc[E];
 #pragma unroll
     for (int e = 0; e < E; ++e) acc[e] = 0.f;
@@ -1737,14 +1772,24 @@ __device__ __forceinline__ void finalize_row(const Problem& pb, const Pass& ps, 
   }
 }
 
-template <typename T>
+template <typename T, int NSLICES>
 __global__ __launch_bounds__(64) void k_finalize(Problem pb, Pass ps, const uint64_t* sel) {
+  static_assert(8 % NSLICES == 0, "slices are dealt to the 8 XCDs");
   extern __shared__ float fsh[];
-  // same XCD-aware renumbering as the scan: neighbouring rows (same head, same
-  // value rows) run on one XCD
   const int64_t G = gridDim.x, bid = blockIdx.x;
-  const int64_t p = (G % 8 == 0) ? (bid % 8) * (G / 8) + bid / 8 : bid;
-  finalize_row<T>(pb, ps, sel, p, fsh, (uint32_t*)(fsh + pb.k));
+  int64_t p;
+  int slice = 0;
+  if (NSLICES > 1) {
+    // column slices: workgroups are dealt to the XCDs in turn, so slice bid % NSLICES
+    // runs only on the XCDs whose L2 holds that slice's columns
+    slice = (int)(bid % NSLICES);
+    p = bid / NSLICES;
+  } else {
+    // same XCD-aware renumbering as the scan: neighbouring rows (same head, same
+    // value rows) run on one XCD
+    p = (G % 8 == 0) ? (bid % 8) * (G / 8) + bid / 8 : bid;
+  }
+  finalize_row<T, NSLICES>(pb, ps, sel, p, fsh, (uint32_t*)(fsh + pb.k), slice);
 }
 
 // ------------------------------------------------------------------ MFMA layout probe
@@ -1866,10 +1911,19 @@ hipError_t launch_redo(const Problem& pb, const Pass& ps, const PassBufs& b, hip
 
 hipError_t launch_finalize(const Problem& pb, const Pass& ps, const PassBufs& b, hipStream_t st) {
   const size_t sh = (size_t)pb.k * 8;
-  if (pb.dtype == T_BF16)
-    k_finalize<uint16_t><<<(unsigned)pass_rows(pb, ps), 64, sh, st>>>(pb, ps, b.sel);
-  else
-    k_finalize<float><<<(unsigned)pass_rows(pb, ps), 64, sh, st>>>(pb, ps, b.sel);
+  // value matrices larger than an L2 with rows of at least 1 KiB: eight column
+  // slices, one per XCD, so each XCD's L2 caches an eighth of the matrix
+  const int64_t esz = pb.dtype == T_BF16 ? 2 : 4, nvec = pb.d * esz / 16;
+  const bool sliced = pb.Lk * pb.d * esz > FINALIZE_SLICE_BYTES && nvec % 64 == 0;
+  const int64_t g = pass_rows(pb, ps) * (sliced ? 8 : 1);
+  if (g > 0x7FFFFFFF) return hipErrorInvalidValue;
+  if (pb.dtype == T_BF16) {
+    if (sliced) k_finalize<uint16_t, 8><<<(unsigned)g, 64, sh, st>>>(pb, ps, b.sel);
+    else k_finalize<uint16_t, 1><<<(unsigned)g, 64, sh, st>>>(pb, ps, b.sel);
+  } else {
+    if (sliced) k_finalize<float, 8><<<(unsigned)g, 64, sh, st>>>(pb, ps, b.sel);
+    else k_finalize<float, 1><<<(unsigned)g, 64, sh, st>>>(pb, ps, b.sel);
+  }
   return hipGetLastError();
 }
 

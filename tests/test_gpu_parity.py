@@ -105,6 +105,12 @@ FFN_CASES = {
     # over more than 1024 samples
     "ffn_filter_k300_wg_threshold": dict(N=200, d_model=128, d_ff=20000, k=300, chunk=64),
     "ffn_fused_sample": dict(N=130, d_model=128, d_ff=20000, k=100, chunk=0),
+    # value matrices over 8 MiB with rows of at least 1 KiB: the gather runs in eight
+    # column slices, each re-ordering the survivors by key index (register sorts of
+    # 128 and 512 entries; 4-byte elements)
+    "ffn_sliced_gather_k100": dict(N=150, d_model=512, d_ff=9000, k=100, chunk=64),
+    "ffn_sliced_gather_k512": dict(N=70, d_model=1024, d_ff=5000, k=512, chunk=32),
+    "ffn_sliced_gather_f32": dict(N=90, d_model=256, d_ff=9000, k=40, chunk=50, dtype=wl.F32),
 }
 
 
@@ -117,6 +123,17 @@ def test_ffn_parity(name):
     rep = {}
     parity.check_ffn(w, x, out, idx, report=rep)
     _say(name, "ok", rep, "path", tk.ffn_path(w.N, w.d_model, w.d_ff, w.k, w.chunk))
+
+
+@pytest.mark.parametrize("name", ["ffn_sliced_gather_k100", "ffn_sliced_gather_f32"])
+def test_sliced_gather_plain_equals_debug(name):
+    """The column-sliced gather gives the same bits whether or not the selection is written."""
+    w = wl.WORKLOADS["c5"].scaled(**FFN_CASES[name])
+    _say(name, w)
+    x = wl.make_inputs(w)
+    out_dbg, _, _ = parity.run_ffn(w, x)
+    out = parity.run_ffn(w, x, debug=False)
+    assert torch.equal(out, out_dbg)
 
 
 @pytest.mark.parametrize("base,kw", [
