@@ -1911,19 +1911,26 @@ hipError_t launch_redo(const Problem& pb, const Pass& ps, const PassBufs& b, hip
 
 hipError_t launch_finalize(const Problem& pb, const Pass& ps, const PassBufs& b, hipStream_t st) {
   const size_t sh = (size_t)pb.k * 8;
-  // value matrices larger than an L2 with rows of at least 1 KiB: eight column
-  // slices, one per XCD, so each XCD's L2 caches an eighth of the matrix
-  const int64_t esz = pb.dtype == T_BF16 ? 2 : 4, nvec = pb.d * esz / 16;
-  const bool sliced = pb.Lk * pb.d * esz > FINALIZE_SLICE_BYTES && nvec % 64 == 0;
-  const int64_t g = pass_rows(pb, ps) * (sliced ? 8 : 1);
+  // value matrices larger than an L2: up to eight column slices, each a whole number of
+  // 128-byte lines (a slice that split a line would fetch it on two XCDs), so each
+  // XCD's L2 caches its slice of the matrix only
+  const int64_t esz = pb.dtype == T_BF16 ? 2 : 4, row = pb.d * esz;
+  int S = 1;
+  if (pb.Lk * row > FINALIZE_SLICE_BYTES)
+    for (int c = 8; c > 1 && S == 1; c >>= 1)
+      if (row % (128 * c) == 0) S = c;
+  const int64_t g = pass_rows(pb, ps) * S;
   if (g > 0x7FFFFFFF) return hipErrorInvalidValue;
-  if (pb.dtype == T_BF16) {
-    if (sliced) k_finalize<uint16_t, 8><<<(unsigned)g, 64, sh, st>>>(pb, ps, b.sel);
-    else k_finalize<uint16_t, 1><<<(unsigned)g, 64, sh, st>>>(pb, ps, b.sel);
-  } else {
-    if (sliced) k_finalize<float, 8><<<(unsigned)g, 64, sh, st>>>(pb, ps, b.sel);
-    else k_finalize<float, 1><<<(unsigned)g, 64, sh, st>>>(pb, ps, b.sel);
-  }
+#define TOPK_FINALIZE(T_)                                                                   \
+  do {                                                                                      \
+    if (S == 8) k_finalize<T_, 8><<<(unsigned)g, 64, sh, st>>>(pb, ps, b.sel);              \
+    else if (S == 4) k_finalize<T_, 4><<<(unsigned)g, 64, sh, st>>>(pb, ps, b.sel);         \
+    else if (S == 2) k_finalize<T_, 2><<<(unsigned)g, 64, sh, st>>>(pb, ps, b.sel);         \
+    else k_finalize<T_, 1><<<(unsigned)g, 64, sh, st>>>(pb, ps, b.sel);                     \
+  } while (0)
+  if (pb.dtype == T_BF16) TOPK_FINALIZE(uint16_t);
+  else TOPK_FINALIZE(float);
+#undef TOPK_FINALIZE
   return hipGetLastError();
 }
 

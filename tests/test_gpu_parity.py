@@ -105,12 +105,15 @@ FFN_CASES = {
     # over more than 1024 samples
     "ffn_filter_k300_wg_threshold": dict(N=200, d_model=128, d_ff=20000, k=300, chunk=64),
     "ffn_fused_sample": dict(N=130, d_model=128, d_ff=20000, k=100, chunk=0),
-    # value matrices over 8 MiB with rows of at least 1 KiB: the gather runs in eight
-    # column slices, each re-ordering the survivors by key index (register sorts of
-    # 128 and 512 entries; 4-byte elements)
+    # value matrices over 8 MiB: the gather runs in column slices of whole 128-byte
+    # lines, each re-ordering the survivors by key index (eight slices with register
+    # sorts of 128 and 512 entries; 4-byte elements; four 384-byte slices at d 768;
+    # four 128-byte slices at d 256)
     "ffn_sliced_gather_k100": dict(N=150, d_model=512, d_ff=9000, k=100, chunk=64),
     "ffn_sliced_gather_k512": dict(N=70, d_model=1024, d_ff=5000, k=512, chunk=32),
     "ffn_sliced_gather_f32": dict(N=90, d_model=256, d_ff=9000, k=40, chunk=50, dtype=wl.F32),
+    "ffn_sliced_gather_d768": dict(N=60, d_model=768, d_ff=6000, k=64, chunk=32),
+    "ffn_sliced_gather_d256": dict(N=80, d_model=256, d_ff=20000, k=70, chunk=40),
 }
 
 
@@ -125,7 +128,7 @@ def test_ffn_parity(name):
     _say(name, "ok", rep, "path", tk.ffn_path(w.N, w.d_model, w.d_ff, w.k, w.chunk))
 
 
-@pytest.mark.parametrize("name", ["ffn_sliced_gather_k100", "ffn_sliced_gather_f32"])
+@pytest.mark.parametrize("name", ["ffn_sliced_gather_k100", "ffn_sliced_gather_f32", "ffn_sliced_gather_d768"])
 def test_sliced_gather_plain_equals_debug(name):
     """The column-sliced gather gives the same bits whether or not the selection is written."""
     w = wl.WORKLOADS["c5"].scaled(**FFN_CASES[name])
