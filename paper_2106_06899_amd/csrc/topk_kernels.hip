@@ -1620,11 +1620,14 @@ __global__ __launch_bounds__(256) void k_redo_rest(Problem pb, Pass ps, PassBufs
 // rows are read as 16-byte vectors: with NV vectors per row, 64/NV rows are
 // gathered per wave instruction (d = 64 bf16: 8 rows), each lane accumulating its
 // vector's columns in fp32; the row slots are then reduced across lanes.
+#ifndef FIN_U
+#define FIN_U 4
+#endif
 template <typename T> struct Vec16;
 template <> struct Vec16<uint16_t> {
   static constexpr int E = 8;
-  static __device__ __forceinline__ void load(const uint16_t* p, float (&x)[8]) {
-    const uint4 v = *(const uint4*)p;
+  static __device__ __forceinline__ uint4 raw(const uint16_t* p) { return *(const uint4*)p; }
+  static __device__ __forceinline__ void unpack(const uint4 v, float (&x)[8]) {
     const uint32_t w[4] = {v.x, v.y, v.z, v.w};
 #pragma unroll
     for (int e = 0; e < 4; ++e) {
@@ -1632,6 +1635,7 @@ template <> struct Vec16<uint16_t> {
       x[2 * e + 1] = __uint_as_float(w[e] & 0xFFFF0000u);
     }
   }
+  static __device__ __forceinline__ void load(const uint16_t* p, float (&x)[8]) { unpack(raw(p), x); }
   static __device__ __forceinline__ void store(uint16_t* p, const float (&x)[8]) {
     uint32_t w[4];
 #pragma unroll
@@ -1641,10 +1645,11 @@ template <> struct Vec16<uint16_t> {
 };
 template <> struct Vec16<float> {
   static constexpr int E = 4;
-  static __device__ __forceinline__ void load(const float* p, float (&x)[4]) {
-    const float4 v = *(const float4*)p;
-    x[0] = v.x; x[1] = v.y; x[2] = v.z; x[3] = v.w;
+  static __device__ __forceinline__ uint4 raw(const float* p) { return *(const uint4*)p; }
+  static __device__ __forceinline__ void unpack(const uint4 v, float (&x)[4]) {
+    x[0] = __uint_as_float(v.x); x[1] = __uint_as_float(v.y); x[2] = __uint_as_float(v.z); x[3] = __uint_as_float(v.w);
   }
+  static __device__ __forceinline__ void load(const float* p, float (&x)[4]) { unpack(raw(p), x); }
   static __device__ __forceinline__ void store(float* p, const float (&x)[4]) {
     *(float4*)p = make_float4(x[0], x[1], x[2], x[3]);
   }
@@ -1728,6 +1733,7 @@ __device__ __forceinline__ void finalize_row(const Problem& pb, const Pass& ps, 
     else sort_by_key_index<8>(w, jj, (int)k_eff);
   }
   const T* Vh = (const T*)pb.V + rr.bh * pb.kv_head_stride;
+  const uint32_t d32 = (uint32_t)pb.d;  // row offsets j * d are 32 x 32 -> 64-bit products
   T* orow = (T*)pb.out + grow * pb.d;
   const int nvec = (int)(pb.d / E) / NSLICES;      // 16-byte vectors of this slice per value row
   const int vbeg = slice * nvec, vend = vbeg + nvec;
@@ -1740,20 +1746,30 @@ __device__ __forceinline__ void finalize_row(const Problem& pb, const Pass& ps, 
 #pragma unroll
     for (int e = 0; e < E; ++e) acc[e] = 0.f;
     {
+      // FIN_U independent gathers in flight: every raw load is issued before the first
+      // is unpacked; the sum still runs over t in increasing order
+      const T* vcol = Vh + v0 * E;
       int64_t t = slot;
-      for (; t + 3 * slots < k_eff; t += 4 * slots) {  // four independent gathers in flight
-        float x0[E], x1[E], x2[E], x3[E];
-        Vec16<T>::load(Vh + (int64_t)jj[t] * pb.d + v0 * E, x0);
-        Vec16<T>::load(Vh + (int64_t)jj[t + slots] * pb.d + v0 * E, x1);
-        Vec16<T>::load(Vh + (int64_t)jj[t + 2 * slots] * pb.d + v0 * E, x2);
-        Vec16<T>::load(Vh + (int64_t)jj[t + 3 * slots] * pb.d + v0 * E, x3);
-        const float w0 = w[t], w1 = w[t + slots], w2 = w[t + 2 * slots], w3 = w[t + 3 * slots];
+      for (; t + (FIN_U - 1) * slots < k_eff; t += FIN_U * slots) {
+        uint4 raw[FIN_U];
 #pragma unroll
-        for (int e = 0; e < E; ++e) acc[e] = fmaf(w3, x3[e], fmaf(w2, x2[e], fmaf(w1, x1[e], fmaf(w0, x0[e], acc[e]))));
+        for (int q = 0; q < FIN_U; ++q) raw[q] = Vec16<T>::raw(vcol + (uint64_t)jj[t + q * slots] * d32);
+        // keep the scheduler from sinking loads below the first unpack (it otherwise
+        // waits for each load before issuing the next ones); the sliced gathers, bound
+        // by the fabric rather than by latency, measured faster without
+        if (NSLICES == 1) __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+        for (int q = 0; q < FIN_U; ++q) {
+          float x[E];
+          Vec16<T>::unpack(raw[q], x);
+          const float wt = w[t + q * slots];
+#pragma unroll
+          for (int e = 0; e < E; ++e) acc[e] = fmaf(wt, x[e], acc[e]);
+        }
       }
       for (; t < k_eff; t += slots) {
         float x[E];
-        Vec16<T>::load(Vh + (int64_t)jj[t] * pb.d + v0 * E, x);
+        Vec16<T>::load(vcol + (uint64_t)jj[t] * d32, x);
         const float wt = w[t];
 #pragma unroll
         for (int e = 0; e < E; ++e) acc[e] = fmaf(wt, x[e], acc[e]);
