@@ -2194,28 +2194,29 @@ __global__ __launch_bounds__(256) void k_bwd_rows(BwdProblem bp, BwdBufs b) {
         const int e = e0 + q * lm.S + lm.slot;
         jq[q] = __shfl(jg, e & 63, 64);
         dq[q] = __shfl(dsl, e & 63, 64);
-        if (e < n && jq[q] >= 0) {
+        // no branch on the entry: skipped slots load key row 0 and are not summed
+        // (a load under a data-dependent branch made the compiler wait for every
+        // earlier load before it)
+        const int64_t jr = e < n && jq[q] >= 0 ? jq[q] : 0;
 #pragma unroll
-          for (int u = 0; u < NCL; ++u) {
-            const int c = lm.part + lm.G * u;
-            if (c < lm.CH) xk[q][u] = load16<T>(bp.K, kv0 + (int64_t)jq[q] * d + (int64_t)c * EPC);
-          }
+        for (int u = 0; u < NCL; ++u) {
+          // lanes past the row's last chunk read its last chunk; their sums are never stored
+          const int c = lm.part + lm.G * u < lm.CH ? lm.part + lm.G * u : lm.CH - 1;
+          xk[q][u] = load16<T>(bp.K, kv0 + jr * d + (int64_t)c * EPC);
         }
       }
 #pragma unroll
       for (int q = 0; q < U; ++q) {
+        // skipped slots add 0 * (a finite key row): no branch, so every load above is
+        // consumed on every path and none has to be waited for early
         const int e = e0 + q * lm.S + lm.slot;
-        if (e < n && jq[q] >= 0) {
+        const float dqe = e < n && jq[q] >= 0 ? dq[q] : 0.f;
 #pragma unroll
-          for (int u = 0; u < NCL; ++u) {
-            const int c = lm.part + lm.G * u;
-            if (c < lm.CH) {
-              float x[EPC];
-              unpack<T>(xk[q][u], x);
+        for (int u = 0; u < NCL; ++u) {
+          float x[EPC];
+          unpack<T>(xk[q][u], x);
 #pragma unroll
-              for (int t = 0; t < EPC; ++t) acc[u][t] = fmaf(dq[q], x[t], acc[u][t]);
-            }
-          }
+          for (int t = 0; t < EPC; ++t) acc[u][t] = fmaf(dqe, x[t], acc[u][t]);
         }
       }
     }
@@ -2565,20 +2566,26 @@ __global__ __launch_bounds__(256) void k_bwd_keys(BwdProblem bp, BwdBufs b) {
     for (int e0 = 0; e0 < n; e0 += U * lm.S) {
       uint4 xo[U][NCL], xq[U][NCL];
       float2 c[U];
+      // the U list entries first, then every gather, without branches (slots past the
+      // list repeat its last entry and are skipped below): a wait for one entry inside
+      // a branch became a wait for every gather issued before it
+      int32_t pq[U];
 #pragma unroll
       for (int q = 0; q < U; ++q) {
         const int e = e0 + q * lm.S + lm.slot;
-        if (e < n) {
-          const int32_t p = get(e);
-          c[q] = b.pair[p];
-          const int64_t row = (int64_t)((uint32_t)p / kk) * d;
+        pq[q] = get(e < n ? e : n - 1);
+      }
 #pragma unroll
-          for (int u = 0; u < NCL; ++u) {
-            const int ch = lm.part + lm.G * u;
-            if (ch < lm.CH) {
-              xo[q][u] = load16<T>(bp.dout, row + (int64_t)ch * EPC);
-              xq[q][u] = load16<T>(bp.Q, row + (int64_t)ch * EPC);
-            }
+      for (int q = 0; q < U; ++q) {
+        const int32_t p = pq[q];
+        c[q] = b.pair[p];
+        const int64_t row = (int64_t)((uint32_t)p / kk) * d;
+#pragma unroll
+        for (int u = 0; u < NCL; ++u) {
+          const int ch = lm.part + lm.G * u;
+          if (ch < lm.CH) {
+            xo[q][u] = load16<T>(bp.dout, row + (int64_t)ch * EPC);
+            xq[q][u] = load16<T>(bp.Q, row + (int64_t)ch * EPC);
           }
         }
       }
