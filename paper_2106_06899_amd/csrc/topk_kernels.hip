@@ -2126,30 +2126,27 @@ __global__ __launch_bounds__(256) void k_bwd_rows(BwdProblem bp, BwdBufs b) {
       for (int q = 0; q < U; ++q) {
         const int e = e0 + q * lm.S + lm.slot;
         jq[q] = __shfl(jl, e & 63, 64);
-        if (e < n && valid_key(jq[q])) {
+        // no branches around the gathers (see pass 3): skipped slots and lanes past the
+        // row's last chunk read value row 0 / the last chunk, and their products are
+        // discarded below
+        const int64_t jr = e < n && valid_key(jq[q]) ? jq[q] : 0;
 #pragma unroll
-          for (int u = 0; u < NCL; ++u) {
-            const int c = lm.part + lm.G * u;
-            if (c < lm.CH) xv[q][u] = load16<T>(bp.V, kv0 + (int64_t)jq[q] * d + (int64_t)c * EPC);
-          }
+        for (int u = 0; u < NCL; ++u) {
+          const int c = lm.part + lm.G * u < lm.CH ? lm.part + lm.G * u : lm.CH - 1;
+          xv[q][u] = load16<T>(bp.V, kv0 + jr * d + (int64_t)c * EPC);
         }
       }
 #pragma unroll
       for (int q = 0; q < U; ++q) {
         const int e = e0 + q * lm.S + lm.slot;
         const bool ok = e < n && valid_key(jq[q]);
-        float dw = 0.f;
-        if (ok) {
+        float dw = 0.f;  // lanes past the last chunk add x * 0 (gout is 0 there)
 #pragma unroll
-          for (int u = 0; u < NCL; ++u) {
-            const int c = lm.part + lm.G * u;
-            if (c < lm.CH) {
-              float x[EPC];
-              unpack<T>(xv[q][u], x);
+        for (int u = 0; u < NCL; ++u) {
+          float x[EPC];
+          unpack<T>(xv[q][u], x);
 #pragma unroll
-              for (int t = 0; t < EPC; ++t) dw = fmaf(x[t], gout[u][t], dw);
-            }
-          }
+          for (int t = 0; t < EPC; ++t) dw = fmaf(x[t], gout[u][t], dw);
         }
         for (int off = 1; off < lm.G; off <<= 1) dw += __shfl_xor(dw, off, 64);
         const float s = __shfl(sl, e & 63, 64);
