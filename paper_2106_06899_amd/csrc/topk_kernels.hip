@@ -2478,10 +2478,13 @@ __global__ __launch_bounds__(256) void k_bwd_bucket_lists(BwdProblem bp, BwdLayo
   // this wave's pairs per key; BK_BATCH chunks of loads in flight
   for (int32_t e0 = wb; e0 < we; e0 += 64 * BK_BATCH) {
     uint32_t kq[BK_BATCH];
+    // loads without a branch (lanes past the end re-read the last entry), so that the
+    // compiler issues all of them before the first wait
 #pragma unroll
     for (int u = 0; u < BK_BATCH; ++u) {
       const int32_t e = e0 + u * 64 + lane;
-      kq[u] = e < we ? (uint32_t)(stage[e] >> 32) & kmask : 0xFFFFFFFFu;
+      const uint32_t hi = (uint32_t)(stage[e < we ? e : we - 1] >> 32);
+      kq[u] = e < we ? hi & kmask : 0xFFFFFFFFu;
     }
 #pragma unroll
     for (int u = 0; u < BK_BATCH; ++u)
@@ -2514,7 +2517,7 @@ __global__ __launch_bounds__(256) void k_bwd_bucket_lists(BwdProblem bp, BwdLayo
 #pragma unroll
     for (int u = 0; u < BK_BATCH; ++u) {
       const int32_t e = e0 + u * 64 + lane;
-      vq[u] = e < we ? stage[e] : 0ull;
+      vq[u] = stage[e < we ? e : we - 1];  // lanes past the end: not ok below
     }
 #pragma unroll
     for (int u = 0; u < BK_BATCH; ++u) {
