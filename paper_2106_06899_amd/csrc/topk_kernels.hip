@@ -1615,14 +1615,13 @@ __global__ __launch_bounds__(256) void k_redo_rest(Problem pb, Pass ps, PassBufs
 }
 
 // ------------------------------------------------------------------ finalize
-// One wave per row: activation over the k_eff survivors (softmax with the Eq. 1
-// temperature, or ReLU), then the weighted sum of the selected value rows. Value
-// rows are read as 16-byte vectors: with NV vectors per row, 64/NV rows are
-// gathered per wave instruction (d = 64 bf16: 8 rows), each lane accumulating its
-// vector's columns in fp32; the row slots are then reduced across lanes.
-#ifndef FIN_U
-#define FIN_U 4
-#endif
+// One wave per row (or per row and column slice): activation over the k_eff
+// survivors (softmax with the Eq. 1 temperature, or ReLU), then the weighted sum of
+// the selected value rows (Eq. 4; the value rows are W2's rows for Eq. 3). Value
+// rows are read as 16-byte vectors: with NV vectors per row (or slice), 64/NV rows
+// are gathered per wave instruction (d = 64 bf16: 8 rows), each lane accumulating
+// its vector's columns in fp32; the row slots are then reduced across lanes.
+constexpr int FIN_U = 4;  // value-row gathers a finalize lane has in flight together
 template <typename T> struct Vec16;
 template <> struct Vec16<uint16_t> {
   static constexpr int E = 8;
@@ -1746,7 +1745,7 @@ __device__ __forceinline__ void finalize_row(const Problem& pb, const Pass& ps, 
 #pragma unroll
     for (int e = 0; e < E; ++e) acc[e] = 0.f;
     {
-      // FIN_U independent gathers in flight: every raw load is issued before the first
+      // FIN_U independent gathers: every raw load is issued before the first
       // is unpacked; the sum still runs over t in increasing order
       const T* vcol = Vh + v0 * E;
       int64_t t = slot;
