@@ -5,33 +5,35 @@ TEST INFRASTRUCTURE. Only ``tests/``, ``__graft_entry__.smoke()`` and the
 HIP library and its Python binding) never calls it, and this module shares no
 code with that path.
 
-It follows the forward pass of the paper's pseudo-code (Section 2.2, "Improving
-efficiency through top-k attention") for one query chunk at a time, in the order
-the paper gives the steps:
+What is computed is the definition itself, row by row. For one head with keys
+k_j and values v_j (j = 0 .. Lk-1) and a query row q_i:
 
-1. ``dots = Q_C K^T``                         -- the chunk's score tile (Eq. 4);
-2. masked entries set to -inf                   -- the binary mask B of Eq. 2 (causal);
-3. ``top_dots, top_indices = row_wise_topk``    -- keep each row's k largest entries;
-4. ``top_actv = activation(top_dots)``          -- softmax over the k survivors (Eq. 1
-   with temperature) or ReLU (Eq. 3);
-5. ``actv = matrix(top_actv, top_indices)``     -- scatter into a dense zero matrix;
-6. ``out = actv V``                             -- dense product.
+* valid keys: every key, or only j <= i under the causal mask (Eq. 2: the masked
+  entries get -inf, so they can never be among the largest);
+* scores: s_ij = q_i . k_j (the dot products of Eq. 4, before any temperature);
+* survivors S_i: the k_eff = min(k, number of valid keys) valid keys that come first
+  when the keys are ordered by score, highest first (Eq. 4 keeps the k largest
+  entries of each row);
+* weights: the softmax of scale * s_ij over the survivors only (Eq. 1 with its
+  temperature, applied to the row that Eq. 4 left), or, for the feed-forward
+  layer, w_ij = max(s_ij, 0) (Eq. 3);
+* output: o_i = sum over j in S_i of w_ij v_j.
 
-Query chunking (Section 2.2, "Query chunking") only bounds memory; each chunk is
-computed from ``Q_C, K, V`` alone, so the result does not depend on the chunk size.
+Query chunking (Section 2.2) bounds how many rows are processed at once; each row
+depends only on its own query and on all keys and values, so the chunk size does not
+change any result. Here it only sets how many rows are scored together.
 
-Readings of points the paper leaves open:
+Readings of points the paper leaves open (the same on the GPU side):
 
-* selection uses the raw score ``q.k``; the temperature ``scale`` (= 1/lambda of
-  Eq. 1) multiplies scores only inside the softmax, and is the float32 value the
-  caller passes, upcast to fp64;
-* the softmax runs over the k survivors only (non-selected entries are masked out,
-  i.e. -inf, not zero);
-* ties are broken by the lower key index: rows are ordered by (score desc, index asc);
-* causal rows with fewer than k valid keys (key j valid iff j <= i, 0-based) keep
-  all of them (k_eff = min(k, i + 1)); padding indices are -1;
-* the feed-forward layer has no bias and no temperature; ReLU is applied after the
-  selection, so negative survivors stay selected with weight 0.
+* the temperature ``scale`` (= 1/lambda of Eq. 1) multiplies scores inside the
+  softmax only; selection uses the raw score, and the value used is the float32
+  number the caller passes, upcast to fp64;
+* non-selected entries are excluded from the softmax (-inf), not set to zero;
+* equal scores are ordered by the lower key index first;
+* a causal row with fewer than k valid keys keeps all of them (k_eff = i + 1);
+  index outputs are padded with -1 and score outputs with -inf;
+* the feed-forward layer has no bias and no temperature, and ReLU is applied to the
+  survivors, so a selected negative score stays selected with weight 0.
 
 Every input is upcast exactly to float64 (bf16 and fp32 values are representable).
 """
@@ -40,123 +42,126 @@ from __future__ import annotations
 import numpy as np
 
 
-# --------------------------------------------------------------------------- step 1-2
-def chunk_scores(Qc: np.ndarray, K: np.ndarray, row0: int | None = None, causal: bool = False) -> np.ndarray:
-    """The chunk's score tile ``dots = Q_C K^T`` in fp64 (Eq. 4), with the Eq. 2 mask.
+def _f64(a):
+    return np.asarray(a, dtype=np.float64)
 
-    Qc: [C, d] queries of the chunk, K: [Lk, d] keys. With ``causal`` the query row r
-    of the chunk has absolute index ``row0 + r`` and key j is valid iff j <= row0 + r;
-    invalid entries are -inf (B = -inf in Eq. 2). ``row0`` may also be an array of
-    absolute row indices (one per row of Qc).
+
+# --------------------------------------------------------------------------- valid keys (Eq. 2)
+def valid_lengths(i, Lk: int, causal: bool) -> np.ndarray:
+    """Number of valid keys of query rows with absolute indices ``i`` (array): keys
+    0 .. n-1 are valid, n = min(i + 1, Lk) under the causal mask (top-left aligned,
+    0-based), n = Lk otherwise."""
+    i = np.asarray(i, dtype=np.int64)
+    return np.minimum(i + 1, Lk) if causal else np.full(i.shape, Lk, dtype=np.int64)
+
+
+# --------------------------------------------------------------------------- scores (Eq. 4)
+def scores(Qr, K, n_valid) -> np.ndarray:
+    """fp64 scores s[r, j] = Qr[r] . K[j] of query rows Qr [R, d] against every key
+    K [Lk, d]; -inf where key j is not valid for row r (j >= n_valid[r])."""
+    s = _f64(Qr) @ _f64(K).T
+    j = np.arange(s.shape[1])
+    s[j[None, :] >= np.asarray(n_valid)[:, None]] = -np.inf
+    return s
+
+
+def selected_scores(Qr, K, idx) -> np.ndarray:
+    """fp64 scores Qr[r] . K[idx[r, m]] of given (row, key) pairs; -inf where idx = -1."""
+    valid = idx >= 0
+    s = np.einsum("rt,rmt->rm", _f64(Qr), _f64(K)[np.where(valid, idx, 0)])
+    return np.where(valid, s, -np.inf)
+
+
+# --------------------------------------------------------------------------- survivors (Eq. 4)
+def select(S: np.ndarray, k: int):
+    """The survivors of each row of the score matrix S [R, Lk] (-inf = invalid key).
+
+    A row's survivors are its k_eff = min(k, #valid) valid keys that come first in the
+    order (score desc, index asc). With t the k-th largest entry of the row, they are
+    every key scoring above t plus, among the keys scoring exactly t, the ones with the
+    lowest indices (np.partition finds t).
+
+    Returns ``idx`` [R, k] int64 in that order (-1 pads), ``top`` [R, k] their scores
+    (-inf pads), ``k_eff`` [R], ``sigma_k`` (the last survivor's score) and
+    ``sigma_k1`` (the best non-survivor's score; NaN when every valid key survives).
     """
-    dots = np.asarray(Qc, dtype=np.float64) @ np.asarray(K, dtype=np.float64).T
-    if causal:
-        rows = np.asarray(row0 if np.ndim(row0) else row0 + np.arange(dots.shape[0]))
-        cols = np.arange(dots.shape[1])
-        dots[cols[None, :] > rows[:, None]] = -np.inf
-    return dots
-
-
-# --------------------------------------------------------------------------- step 3
-def row_wise_topk(dots: np.ndarray, k: int):
-    """Each row's k largest entries in the order (score desc, index asc) (Eq. 4).
-
-    ``dots`` is [R, Lk] fp64 with -inf at masked entries. A row with fewer than k
-    valid entries keeps all of them (k_eff = min(k, #valid)).
-
-    Returns ``top_idx`` [R, k] int64 (-1 pads), ``top_dots`` [R, k] fp64 (-inf pads),
-    ``k_eff`` [R], and the tie-band values ``sigma_k`` (the k_eff-th selected score)
-    and ``sigma_k1`` (the next valid score, NaN when every valid key is selected).
-    """
-    R, Lk = dots.shape
+    R, Lk = S.shape
     if not 1 <= k <= Lk:
         raise ValueError("need 1 <= k <= Lk")
-    valid = dots > -np.inf
+    valid = S > -np.inf
     n_valid = valid.sum(axis=1)
     k_eff = np.minimum(k, n_valid)
-
-    # t = the k-th largest entry of each row (masked entries count as -inf).
-    neg = -dots
     if k < Lk:
-        part = np.partition(neg, (k - 1, k), axis=1)
-        t = -part[:, k - 1]
-        t_next = -part[:, k]
+        part = -np.partition(-S, (k - 1, k), axis=1)
+        t, t_next = part[:, k - 1], part[:, k]
     else:
-        t = dots.min(axis=1)
-        t_next = np.full(R, -np.inf)
+        t, t_next = S.min(axis=1), np.full(R, -np.inf)
+    above = S > t[:, None]
+    at_t = (S == t[:, None]) & valid
+    room = k_eff - above.sum(axis=1)
+    keep = above | (at_t & (np.cumsum(at_t, axis=1) <= room[:, None]))
+    assert np.array_equal(keep.sum(axis=1), k_eff)
 
-    # Everything strictly above t is in; entries equal to t fill the rest, lowest index first.
-    above = dots > t[:, None]
-    equal = (dots == t[:, None]) & valid
-    need = k_eff - above.sum(axis=1)
-    take_equal = equal & (np.cumsum(equal, axis=1) <= need[:, None])
-    chosen = above | take_equal
-    assert np.array_equal(chosen.sum(axis=1), k_eff)
-
-    rows, cols = np.nonzero(chosen)                       # row-major: cols ascending per row
+    # the kept keys of each row in index order, then sorted by (score desc, index asc);
+    # pads (index -1, score -inf) go last
+    rows, cols = np.nonzero(keep)
     slot = np.arange(rows.size) - np.repeat(np.cumsum(k_eff) - k_eff, k_eff)
-    top_idx = np.full((R, k), -1, dtype=np.int64)
-    top_dots = np.full((R, k), -np.inf)
-    top_idx[rows, slot] = cols
-    top_dots[rows, slot] = dots[rows, cols]
-
-    # Order each row by (score desc, index asc); pads (-inf, -1) go last.
-    idx_key = np.where(top_idx < 0, np.iinfo(np.int64).max, top_idx)
-    order = np.lexsort((idx_key, -top_dots), axis=1)
-    top_idx = np.take_along_axis(top_idx, order, axis=1)
-    top_dots = np.take_along_axis(top_dots, order, axis=1)
-
-    sigma_k = top_dots[np.arange(R), k_eff - 1]
+    idx = np.full((R, k), -1, dtype=np.int64)
+    top = np.full((R, k), -np.inf)
+    idx[rows, slot] = cols
+    top[rows, slot] = S[rows, cols]
+    order = np.lexsort((np.where(idx < 0, Lk, idx), -top), axis=1)
+    idx = np.take_along_axis(idx, order, axis=1)
+    top = np.take_along_axis(top, order, axis=1)
+    sigma_k = top[np.arange(R), k_eff - 1]
     sigma_k1 = np.where(n_valid > k, t_next, np.nan)
-    return top_idx, top_dots, k_eff, sigma_k, sigma_k1
+    return idx, top, k_eff, sigma_k, sigma_k1
 
 
-# --------------------------------------------------------------------------- step 4
-def softmax_over_survivors(top_dots: np.ndarray, scale: float) -> np.ndarray:
-    """Row softmax of ``scale * top_dots`` over the selected entries only (Eq. 1, Eq. 4).
-
-    Pads (-inf) get weight 0. ``scale`` is the temperature 1/lambda of Eq. 1.
-    """
-    s = np.float64(np.float32(scale)) * top_dots
-    m = np.max(s, axis=1, keepdims=True)
-    e = np.where(np.isfinite(top_dots), np.exp(s - m), 0.0)
+# --------------------------------------------------------------------------- weights (Eq. 1, Eq. 3)
+def softmax_weights(top: np.ndarray, scale: float) -> np.ndarray:
+    """Softmax of ``scale * score`` over each row's survivors (Eq. 1 with temperature
+    1/scale, restricted to the survivors of Eq. 4); pads (-inf) get weight 0."""
+    z = np.float64(np.float32(scale)) * top
+    m = np.max(z, axis=1, keepdims=True)
+    e = np.where(np.isfinite(top), np.exp(z - m), 0.0)
     return e / e.sum(axis=1, keepdims=True)
 
 
-def relu_over_survivors(top_dots: np.ndarray) -> np.ndarray:
-    """ReLU of the selected entries (Eq. 3 recast through Eq. 4); pads get weight 0."""
-    return np.where(np.isfinite(top_dots), np.maximum(top_dots, 0.0), 0.0)
+def relu_weights(top: np.ndarray) -> np.ndarray:
+    """ReLU of each survivor's score (Eq. 3); pads get weight 0."""
+    return np.where(np.isfinite(top), np.maximum(top, 0.0), 0.0)
 
 
-# --------------------------------------------------------------------------- step 5-6
-def scatter_dense(top_actv: np.ndarray, top_idx: np.ndarray, Lk: int) -> np.ndarray:
-    """``actv = matrix(top_actv, top_indices)``: a dense [R, Lk] matrix of zeros holding
-    each row's activations at its selected columns."""
-    R = top_idx.shape[0]
-    actv = np.zeros((R, Lk))
-    r, c = np.nonzero(top_idx >= 0)
-    actv[r, top_idx[r, c]] = top_actv[r, c]
-    return actv
-
-
-def chunk_forward(Qc, K, V, k, activation, scale=1.0, row0=0, causal=False):
-    """Top-k attention for one query chunk (Section 2.2 forward pseudo-code).
-
-    Returns a dict: ``out`` [C, dv] fp64, ``idx`` [C, k], ``top`` [C, k] raw scores,
-    ``k_eff``, ``sigma_k``, ``sigma_k1``.
-    """
-    dots = chunk_scores(Qc, K, row0, causal)
-    top_idx, top_dots, k_eff, sk, sk1 = row_wise_topk(dots, k)
-    del dots
+def weights(top, activation: str, scale: float = 1.0) -> np.ndarray:
     if activation == "softmax":
-        top_actv = softmax_over_survivors(top_dots, scale)
-    elif activation == "relu":
-        top_actv = relu_over_survivors(top_dots)
-    else:
-        raise ValueError(activation)
-    actv = scatter_dense(top_actv, top_idx, K.shape[0])
-    out = actv @ np.asarray(V, dtype=np.float64)
-    return {"out": out, "idx": top_idx, "top": top_dots, "k_eff": k_eff, "sigma_k": sk, "sigma_k1": sk1}
+        return softmax_weights(top, scale)
+    if activation == "relu":
+        return relu_weights(top)
+    raise ValueError(activation)
+
+
+# --------------------------------------------------------------------------- output
+def weighted_sum(w: np.ndarray, idx: np.ndarray, V) -> np.ndarray:
+    """o[r] = sum_m w[r, m] V[idx[r, m]] over the survivors (pads skipped)."""
+    V = _f64(V)
+    valid = idx >= 0
+    rows = V[np.where(valid, idx, 0)]                  # [R, k, dv]
+    return np.einsum("rm,rmt->rt", np.where(valid, w, 0.0), rows)
+
+
+# --------------------------------------------------------------------------- rows of one head
+def topk_rows(Qr, K, V, k, n_valid, activation, scale=1.0):
+    """The definition for query rows Qr [R, d] of one head with keys K and values V
+    [Lk, *]: row r may use keys 0 .. n_valid[r]-1.
+
+    Returns a dict: ``out`` [R, dv] fp64, ``idx`` [R, k], ``top`` [R, k] raw scores,
+    ``k_eff``, ``sigma_k``, ``sigma_k1`` (see ``select``)."""
+    S = scores(Qr, K, n_valid)
+    idx, top, k_eff, sk, sk1 = select(S, k)
+    del S
+    out = weighted_sum(weights(top, activation, scale), idx, V)
+    return {"out": out, "idx": idx, "top": top, "k_eff": k_eff, "sigma_k": sk, "sigma_k1": sk1}
 
 
 # --------------------------------------------------------------------------- whole calls
@@ -166,82 +171,68 @@ def _stack(parts, shape_prefix):
 
 
 def oracle_attn(Q, K, V, k, chunk, causal, scale):
-    """top-k attention over [B, H, L, d] inputs, chunk by chunk (Eq. 4 + query chunking).
-
-    Outputs have shape [B, H, Lq, ...].
-    """
+    """Top-k attention over [B, H, L, d] inputs; ``chunk`` rows of a head at a time
+    (0 or None: the whole head). Outputs have shape [B, H, Lq, ...]."""
     B, H, Lq, _ = Q.shape
-    chunk = Lq if chunk in (0, None) else int(chunk)
+    Lk = K.shape[2]
+    C = Lq if chunk in (0, None) else int(chunk)
     res = []
     for b in range(B):
         for h in range(H):
-            for c0 in range(0, Lq, chunk):
-                res.append(chunk_forward(Q[b, h, c0:c0 + chunk], K[b, h], V[b, h], k, "softmax",
-                                         scale, c0, causal))
+            for c0 in range(0, Lq, C):
+                i = np.arange(c0, min(c0 + C, Lq))
+                res.append(topk_rows(Q[b, h, i], K[b, h], V[b, h], k, valid_lengths(i, Lk, causal), "softmax",
+                                     scale))
     return _stack(res, (B, H, Lq))
 
 
 def oracle_ffn(X, W1, W2, k, chunk):
-    """top-k feed-forward layer: keys are the rows of W1, values the rows of W2, ReLU
-    activation (Eq. 3 through Eq. 4), token chunk by token chunk. Outputs [N, ...]."""
-    N = X.shape[0]
-    chunk = N if chunk in (0, None) else int(chunk)
-    res = [chunk_forward(X[c0:c0 + chunk], W1, W2, k, "relu") for c0 in range(0, N, chunk)]
+    """Top-k feed-forward layer: the keys are the rows of W1, the values the rows of
+    W2, ReLU weights, no temperature (Eq. 3 through Eq. 4); ``chunk`` tokens at a time.
+    Outputs [N, ...]."""
+    N, d_ff = X.shape[0], W1.shape[0]
+    C = N if chunk in (0, None) else int(chunk)
+    res = [topk_rows(X[c0:c0 + C], W1, W2, k, np.full(min(C, N - c0), d_ff), "relu") for c0 in range(0, N, C)]
     return _stack(res, (N,))
 
 
-def oracle_attn_rows(Q, K, V, k, causal, scale, rows):
-    """The oracle on a subset of query rows; ``rows`` is an int array [R, 3] of (b, h, i).
+ROW_BATCH = 1024  # rows scored together by the *_rows functions (bounds the [rows, Lk] score matrix)
 
-    Each (b, h) group of rows is one query chunk (chunking does not change the result).
-    Results are returned in the order of ``rows``.
-    """
+
+def oracle_attn_rows(Q, K, V, k, causal, scale, rows):
+    """The oracle on chosen query rows; ``rows`` is an int array [R, 3] of (b, h, i).
+    Results are returned in the order of ``rows``."""
     rows = np.asarray(rows, dtype=np.int64)
+    Lk = K.shape[2]
     out = {}
     for (b, h) in sorted({(int(r[0]), int(r[1])) for r in rows}):
-        pos = np.nonzero((rows[:, 0] == b) & (rows[:, 1] == h))[0]
-        i = rows[pos, 2]
-        r = chunk_forward(Q[b, h][i], K[b, h], V[b, h], k, "softmax", scale, i, causal)
-        for key, val in r.items():
-            if key not in out:
-                out[key] = np.empty((rows.shape[0],) + val.shape[1:], dtype=val.dtype)
-            out[key][pos] = val
+        same = np.nonzero((rows[:, 0] == b) & (rows[:, 1] == h))[0]
+        for s0 in range(0, same.size, ROW_BATCH):
+            pos = same[s0:s0 + ROW_BATCH]
+            i = rows[pos, 2]
+            r = topk_rows(Q[b, h][i], K[b, h], V[b, h], k, valid_lengths(i, Lk, causal), "softmax", scale)
+            for key, val in r.items():
+                if key not in out:
+                    out[key] = np.empty((rows.shape[0],) + val.shape[1:], dtype=val.dtype)
+                out[key][pos] = val
     return out
 
 
 def oracle_ffn_rows(X, W1, W2, k, rows):
-    """The feed-forward oracle on a subset of token rows (int array [R])."""
+    """The feed-forward oracle on chosen token rows (int array [R]), in that order."""
     rows = np.asarray(rows, dtype=np.int64)
-    return chunk_forward(X[rows], W1, W2, k, "relu")
+    parts = [topk_rows(X[rows[s0:s0 + ROW_BATCH]], W1, W2, k, np.full(rows[s0:s0 + ROW_BATCH].size, W1.shape[0]),
+                       "relu") for s0 in range(0, rows.size, ROW_BATCH)]
+    return _stack(parts, (rows.size,))
 
 
 # --------------------------------------------------------------------------- given index sets
 def from_indices(Qr, K, V, idx, activation, scale=1.0):
-    """Steps 4-6 on a GIVEN index set per row (e.g. the one the GPU selected).
-
-    Qr: [R, d] query rows, idx: [R, k] (-1 pads). Scores of the given keys are
-    recomputed in fp64; returns ``out`` [R, dv] and the weights ``w`` [R, k].
-    """
-    Qr = np.asarray(Qr, dtype=np.float64)
-    K = np.asarray(K, dtype=np.float64)
-    valid = idx >= 0
-    safe = np.where(valid, idx, 0)
-    top = np.einsum("rd,rkd->rk", Qr, K[safe])
-    top = np.where(valid, top, -np.inf)
-    if activation == "softmax":
-        w = softmax_over_survivors(top, scale)
-    else:
-        w = relu_over_survivors(top)
-    actv = scatter_dense(w, idx, K.shape[0])
-    return actv @ np.asarray(V, dtype=np.float64), w
-
-
-def key_scores(Qr, K, idx):
-    """fp64 scores q_r . K[idx[r, t]] for arbitrary (row, key) pairs (-1 -> NaN)."""
-    Qr = np.asarray(Qr, dtype=np.float64)
-    valid = idx >= 0
-    s = np.einsum("rd,rkd->rk", Qr, np.asarray(K, dtype=np.float64)[np.where(valid, idx, 0)])
-    return np.where(valid, s, np.nan)
+    """Weights and output for GIVEN survivor sets (e.g. the ones the GPU selected):
+    Qr [R, d] query rows, idx [R, k] (-1 pads). Scores of the given keys are
+    recomputed in fp64. Returns ``out`` [R, dv] and the weights ``w`` [R, k]."""
+    w = weights(selected_scores(Qr, K, idx), activation, scale)
+    return weighted_sum(w, idx, V), w
 
 
 # --------------------------------------------------------------------------- acceptance rules

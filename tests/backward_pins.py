@@ -89,7 +89,7 @@ def pin_bwd_ffn_vs_finite_differences(bo):
     G = rng.standard_normal((N, dm))
     r = fwd.oracle_ffn(X, W1, W2, k, 0)
     idx = r["idx"]
-    top = fwd.key_scores(X, W1, idx)
+    top = fwd.selected_scores(X, W1, idx)
     assert np.any(top < -1e-3) and np.all(np.abs(top) > 1e-3), "pin data must select negative scores, none near 0"
     assert np.all(r["sigma_k"] - r["sigma_k1"] > 1e-3), "near tie in pin data"  # k < d_ff: every row has one
 

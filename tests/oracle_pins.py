@@ -32,7 +32,7 @@ def pin_scores_vs_loops(o):
     Q = rng.standard_normal((6, 5))
     K = rng.standard_normal((9, 5))
     for causal, row0 in ((False, 0), (True, 0), (True, 2)):
-        got = o.chunk_scores(Q, K, row0, causal)
+        got = o.scores(Q, K, o.valid_lengths(row0 + np.arange(6), 9, causal))
         ref = brute.scores(Q.tolist(), K.tolist(), causal, rows=range(row0, row0 + 6))
         for r in range(6):
             for j in range(9):
@@ -59,7 +59,7 @@ def pin_selection_vs_subsets(o):
                 for r in range(dots.shape[0]):
                     dots[r, r + 1:] = -np.inf
             for k in range(1, Lk + 1):
-                idx, top, k_eff, sk, sk1 = o.row_wise_topk(dots.copy(), k)
+                idx, top, k_eff, sk, sk1 = o.select(dots.copy(), k)
                 for r in range(dots.shape[0]):
                     row = [None if not np.isfinite(v) else float(v) for v in dots[r]]
                     want = brute.topk_subset(row, k)
@@ -85,7 +85,7 @@ def pin_k1_is_argmax_row(o):
     Q = rng.integers(-2, 3, size=(16, 3)).astype(np.float64)
     K = rng.integers(-2, 3, size=(7, 3)).astype(np.float64)
     V = rng.standard_normal((7, 4))
-    r = o.chunk_forward(Q, K, V, 1, "softmax", scale=0.37)
+    r = o.topk_rows(Q, K, V, 1, np.full(16, 7), "softmax", scale=0.37)
     S = Q @ K.T
     for i in range(16):
         j = int(np.flatnonzero(S[i] == S[i].max())[0])
@@ -258,6 +258,99 @@ def pin_from_indices_matches(o):
         out, w = o.from_indices(Q[0, 0], K[0, 0], V[0, 0], r["idx"][0, 0], "softmax", 0.8)
         _close(out, r["out"][0, 0], 1e-12, "from_indices")
         _close(w.sum(axis=1), np.ones(L), 1e-12, "softmax weights sum to 1")
+
+
+# ---------------------------------------------------------------- the row-subset variants (Eq. 4, Eq. 2)
+def pin_selected_scores_vs_loops(o):
+    """Scores of given (row, key) pairs vs explicit loops; -1 pads give -inf."""
+    rng = _rng(24)
+    Q = rng.standard_normal((5, 4))
+    K = rng.standard_normal((11, 4))
+    idx = rng.integers(-1, 11, size=(5, 6))
+    got = o.selected_scores(Q, K, idx)
+    for r in range(5):
+        for m in range(6):
+            j = int(idx[r, m])
+            if j < 0:
+                assert got[r, m] == -np.inf
+            else:
+                assert abs(got[r, m] - brute.dot(Q[r], K[j])) <= 1e-12, f"pair ({r}, {j})"
+
+
+def pin_rows_variants_match_whole_calls(o):
+    """oracle_attn_rows on rows drawn across heads and chunk boundaries, shuffled and with
+    repeats, returns exactly what the whole call gives at those rows, in the order asked
+    (causal rows take their own position for the mask); the same for oracle_ffn_rows.
+    Run with a small row batch so that one (b, h) group spans several batches."""
+    rng = _rng(25)
+    B, H, L, d, k = 2, 2, 37, 5, 6
+    Q, K, V = (rng.standard_normal((B, H, L, d)) for _ in range(3))
+    grid = np.stack(np.meshgrid(np.arange(B), np.arange(H), np.arange(L), indexing="ij"), -1).reshape(-1, 3)
+    rows = np.concatenate([grid[rng.permutation(len(grid))[:90]], grid[[0, 5, 37, 40]]])
+    saved = o.ROW_BATCH
+    o.ROW_BATCH = 7
+    try:
+        for causal in (False, True):
+            full = o.oracle_attn(Q, K, V, k, 8, causal, 0.45)
+            got = o.oracle_attn_rows(Q, K, V, k, causal, 0.45, rows)
+            at = (rows[:, 0], rows[:, 1], rows[:, 2])
+            assert np.array_equal(got["idx"], full["idx"][at]), f"rows idx (causal={causal})"
+            assert np.array_equal(got["k_eff"], full["k_eff"][at]), f"rows k_eff (causal={causal})"
+            _close(got["out"], full["out"][at], 1e-12, f"rows out (causal={causal})")
+            _close(np.nan_to_num(got["sigma_k1"], nan=7.0), np.nan_to_num(full["sigma_k1"][at], nan=7.0), 1e-12,
+                   "rows sigma_k1")
+        X = rng.standard_normal((29, d))
+        W1, W2 = rng.standard_normal((23, d)), rng.standard_normal((23, d))
+        full = o.oracle_ffn(X, W1, W2, 4, 6)
+        trow = np.concatenate([rng.permutation(29), [3, 3, 28]])
+        got = o.oracle_ffn_rows(X, W1, W2, 4, trow)
+        assert np.array_equal(got["idx"], full["idx"][trow]), "ffn rows idx"
+        _close(got["out"], full["out"][trow], 1e-12, "ffn rows out")
+    finally:
+        o.ROW_BATCH = saved
+
+
+# ---------------------------------------------------------------- the output acceptance metric
+def pin_output_rel_errors_rejects_wrong_rows(o):
+    """The per-row output ratio (row max-norm error over row max-norm reference, with a
+    floor only for zero-weight rows): exact rows give 0; a row moved by 2.5e-2 of its
+    largest entry fails the bf16 bound 2e-2 and one moved by 2e-5 fails the fp32 bound
+    1e-5, in that row only; a single wrong element is enough; a feed-forward row whose
+    survivors all score <= 0 (zero weights, zero reference) fails for any non-zero output
+    and passes for zero."""
+    rng = _rng(26)
+    R, dv = 6, 9
+    ref = rng.standard_normal((R, dv))
+    w = np.abs(rng.standard_normal((R, 4)))
+    vmax = 3.0
+    assert np.all(o.output_rel_errors(ref.copy(), ref, w, vmax) == 0.0)
+    for rel, rtol in ((2.5e-2, 2e-2), (2e-5, 1e-5)):
+        g = ref.copy()
+        r, t = 2, int(np.argmax(np.abs(ref[2])))
+        g[r, t] += rel * np.max(np.abs(ref[r]))
+        ratio = o.output_rel_errors(g, ref, w, vmax)
+        assert ratio.shape == (R,)
+        assert ratio[r] > rtol and abs(ratio[r] - rel) <= 1e-9 * rel, f"perturbed row ratio {ratio[r]}"
+        assert np.all(np.delete(ratio, r) == 0.0), "only the perturbed row may fail"
+        g = ref.copy()
+        g[4, 7] = ref[4, 7] + 0.4 * rel * np.max(np.abs(ref[4]))   # a smaller move passes
+        assert o.output_rel_errors(g, ref, w, vmax)[4] <= rtol
+    # zero-weight row (all survivors <= 0 under ReLU): reference 0, floor 0
+    ref0 = ref.copy()
+    ref0[1] = 0.0
+    w0 = w.copy()
+    w0[1] = 0.0
+    g = ref0.copy()
+    assert o.output_rel_errors(g, ref0, w0, vmax)[1] == 0.0
+    g[1, 3] = 1e-3
+    assert o.output_rel_errors(g, ref0, w0, vmax)[1] > 1.0
+    # near-zero reference with weights: the floor (1e-6 max|V| sum|w|) keeps the ratio finite
+    ref1 = ref.copy()
+    ref1[5] = 1e-12
+    g = ref1.copy()
+    g[5] += 1e-9
+    fl = 1e-6 * vmax * np.sum(np.abs(w[5]))
+    assert abs(o.output_rel_errors(g, ref1, w, vmax)[5] - 1e-9 / fl) <= 1e-9 * (1e-9 / fl)
 
 
 ALL_PINS = [v for kname, v in sorted(globals().items()) if kname.startswith("pin_")]

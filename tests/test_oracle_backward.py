@@ -24,55 +24,67 @@ def _caught(monkeypatch, name, fake):
 
 
 def _mut_act_no_scale(orig):
-    return lambda s, g, valid, act, scale: orig(s, g, valid, act, 1.0)
+    return lambda s, a, valid, act, scale: orig(s, a, valid, act, 1.0)
 
 
 def _mut_act_no_centering(orig):
-    def f(s, g, valid, act, scale):
-        w, d = orig(s, g, valid, act, scale)
+    def f(s, a, valid, act, scale):
+        w, d = orig(s, a, valid, act, scale)
         if act == "softmax":
-            d = np.float64(np.float32(scale)) * w * np.where(valid, g, 0.0)
+            d = np.float64(np.float32(scale)) * w * np.where(valid, a, 0.0)
         return w, d
     return f
 
 
 def _mut_act_relu_ungated(orig):
-    def f(s, g, valid, act, scale):
-        w, d = orig(s, g, valid, act, scale)
+    def f(s, a, valid, act, scale):
+        w, d = orig(s, a, valid, act, scale)
         if act == "relu":
-            d = np.where(valid, g, 0.0)
+            d = np.where(valid, a, 0.0)
         return w, d
     return f
 
 
-def _mut_dots_off_by_one_key(orig):
-    def f(Qc, K, idx):
+def _mut_scores_off_by_one_key(orig):
+    def f(Qr, K, idx):
         shifted = np.where(idx >= 0, (idx + 1) % K.shape[0], idx)
-        return orig(Qc, K, shifted)
+        return orig(Qr, K, shifted)
     return f
 
 
-def _mut_chunk_dk_uses_k(orig):
-    def f(Qc, K, V, top_idx, d_out, activation, scale=1.0, top_dots=None):
-        dq, dk, dv = orig(Qc, K, V, top_idx, d_out, activation, scale, top_dots)
-        return dq, dv, dk  # d_K and d_V swapped
+def _mut_dk_dv_swapped(orig):
+    def f(*a, **kw):
+        dq, dk, dv = orig(*a, **kw)
+        return dq, dv, dk
     return f
 
 
-def _mut_chunk_dq_sign(orig):
+def _mut_dq_sign(orig):
     def f(*a, **kw):
         dq, dk, dv = orig(*a, **kw)
         return -dq, dk, dv
     return f
 
 
+def _mut_dv_unweighted(orig):
+    # d_V as the plain sum of the selecting rows' output gradients (weights dropped)
+    def f(Qh, Kh, Vh, idx, G, activation, scale=1.0, chunk=None):
+        dq, dk, dv = orig(Qh, Kh, Vh, idx, G, activation, scale, chunk)
+        dv = np.zeros_like(dv)
+        rr, mm = np.nonzero(idx >= 0)
+        np.add.at(dv, idx[rr, mm], np.asarray(G, dtype=np.float64)[rr])
+        return dq, dk, dv
+    return f
+
+
 MUTATIONS = {
-    "softmax VJP without the temperature": ("activation_backward", _mut_act_no_scale),
-    "softmax VJP without centring": ("activation_backward", _mut_act_no_centering),
-    "ReLU VJP not gated by s > 0": ("activation_backward", _mut_act_relu_ungated),
-    "recomputed scores of the neighbouring key": ("selected_dots", _mut_dots_off_by_one_key),
-    "d_K and d_V swapped": ("chunk_backward", _mut_chunk_dk_uses_k),
-    "d_Q sign flipped": ("chunk_backward", _mut_chunk_dq_sign),
+    "softmax VJP without the temperature": ("score_grads", _mut_act_no_scale),
+    "softmax VJP without centring": ("score_grads", _mut_act_no_centering),
+    "ReLU VJP not gated by s > 0": ("score_grads", _mut_act_relu_ungated),
+    "recomputed scores of the neighbouring key": ("selected_scores", _mut_scores_off_by_one_key),
+    "d_K and d_V swapped": ("head_backward", _mut_dk_dv_swapped),
+    "d_Q sign flipped": ("head_backward", _mut_dq_sign),
+    "d_V without the weights": ("head_backward", _mut_dv_unweighted),
 }
 
 
