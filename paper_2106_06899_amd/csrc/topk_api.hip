@@ -209,8 +209,8 @@ PassBufs carve(const Problem& pb, const Plan& pl, char* ws) {
     off += up(rows * 8);
     b.scores = (float*)(ws + off);
     off += up((size_t)(REDO_CAP + REDO_BLOCKS) * pb.Lk * 4);
+    b.cand_single = 1;  // one list per row: the fused scan and the filtered GEMM both append to it
     if (pl.path == PATH_FILTER) {
-      b.cand_single = 1;
       b.samp = (float*)(ws + off);
       off += up(rows * (size_t)((pb.Lk + FILTER_KSTRIDE - 1) / FILTER_KSTRIDE) * 4);
       b.thr = (float*)(ws + off);

@@ -84,6 +84,15 @@ __device__ __forceinline__ int64_t valid_keys(const Problem& pb, int64_t i) {
 }
 
 // ------------------------------------------------------------------ team primitives
+// Orders one wave's LDS accesses around this point for the compiler; the hardware
+// runs a wave's LDS instructions in order, so a wave sees its own earlier writes
+// and atomics without a workgroup barrier.
+__device__ __forceinline__ void wave_sync_lds() {
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+  __builtin_amdgcn_wave_barrier();
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+}
+
 // A "team" is one workgroup of NT threads (NT = 64 or 256); all sync is __syncthreads.
 template <int NT>
 __device__ __forceinline__ uint32_t team_excl_scan(uint32_t x, uint32_t* tmp) {
@@ -641,8 +650,9 @@ __global__ __launch_bounds__(256) void k_tile_select(Problem pb, Pass ps, const 
 // per-wave LDS staging ring. When the ring fills, the whole wave drains it: each
 // lane takes one staged block, finds its passing scores and appends them as
 // 64-bit words  (raw fp32 score bits << 32) | (~key)  to the query's candidate
-// buffer in global memory (one buffer per query and half-wave; one LDS counter
-// update per block reserves the positions). The select converts the words to
+// list in global memory (one list per query, shared by its two half-waves, so a
+// wave keeps half as many partly written lines in flight; one LDS counter update
+// per block reserves the positions). The select converts the words to
 // order-preserving keys.
 struct ScanArgs {
   const uint16_t* Q;
@@ -703,7 +713,7 @@ __global__ __launch_bounds__(256, D == 64 ? (CAUSAL ? ScanShape<G>::OCC_CAUSAL :
   __shared__ __attribute__((aligned(16))) float4 stage[4][2][STAGE_CAP];
   __shared__ uint32_t stage_meta[4][STAGE_CAP];
   __shared__ float tau_lds[4][32 * G];
-  __shared__ uint32_t cnt_lds[4][64 * G];
+  __shared__ uint32_t cnt_lds[4][32 * G];
 
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63, half = lane >> 5, n = lane & 31;
   // XCD-aware order: the hardware deals workgroups round-robin over the 8 XCDs;
@@ -739,7 +749,8 @@ __global__ __launch_bounds__(256, D == 64 ? (CAUSAL ? ScanShape<G>::OCC_CAUSAL :
     }
   }
 #pragma unroll
-  for (int g = 0; g < G; ++g) cnt_lds[wave][g * 64 + lane] = 0;
+  for (int g = 0; g < G; ++g)
+    if (half == 0) cnt_lds[wave][g * 32 + n] = 0;
 
   // direct loads of tile t into buffer dst: lane `lane` of this wave's j-th load
   // fills LDS position cidx = (wave*LPW + j)*64 + lane with part
@@ -899,17 +910,18 @@ __global__ __launch_bounds__(256, D == 64 ? (CAUSAL ? ScanShape<G>::OCC_CAUSAL :
       }
       if (mask) {
         const uint32_t ql = meta & 63, g = meta >> 6 & 1, h = ql >> 5, hb = meta >> 7 & 1;
-        // one counter update per slot reserves room for all its passing scores
-        uint32_t pos = atomicAdd(&cnt_lds[wave][g * 64 + ql], (uint32_t)__builtin_popcount(mask));
+        // one counter update per slot reserves room for all its passing scores in the
+        // query's list (both half-waves append to the same list)
+        uint32_t pos = atomicAdd(&cnt_lds[wave][g * 32 + (ql & 31)], (uint32_t)__builtin_popcount(mask));
         const uint32_t nj = 0xFFFFFFFFu - ((meta >> 8) * 32u + 4u * h);
-        uint64_t* dst = a.cand + ((wave_row0 + g * 32 + (ql & 31)) * 2 + h) * a.caph;
+        uint64_t* dst = a.cand + (wave_row0 + g * 32 + (ql & 31)) * 2 * a.caph;
         do {
           const uint32_t v = __builtin_ctz(mask);
           mask &= mask - 1;
           // score u = 8*hb + v of the block is key 8*(u/4) + u%4 = u + (u & ~3) past the block's first key
           const uint32_t u = 8u * hb + v;
           const float sc = ((const float*)&stage[wave][v >> 2][slot])[v & 3];
-          if (pos < (uint32_t)a.caph)
+          if (pos < (uint32_t)(2 * a.caph))
             dst[pos] = ((uint64_t)__float_as_uint(sc) << 32) | (uint64_t)(nj - (u + (u & 12u)));
           ++pos;
         } while (mask);
@@ -997,7 +1009,7 @@ __global__ __launch_bounds__(256, D == 64 ? (CAUSAL ? ScanShape<G>::OCC_CAUSAL :
   drain();
 #pragma unroll
   for (int g = 0; g < G; ++g)
-    if (ok[g]) a.cnt[(wave_row0 + g * 32 + n) * 2 + half] = (int32_t)cnt_lds[wave][g * 64 + lane];
+    if (ok[g] && half == 0) a.cnt[(wave_row0 + g * 32 + n) * 2] = (int32_t)cnt_lds[wave][g * 32 + n];
 }
 
 // ------------------------------------------------------------------ fused path: select
@@ -1101,10 +1113,11 @@ __device__ __forceinline__ void wave_sort_store(const uint64_t* sbuf, uint32_t k
 
 // Radix select on n <= E * 64 distinct keys held in registers (key[e] is element
 // e*64 + lane; elements >= n are ignored). Returns (shift, prefix): the k_eff
-// largest keys are exactly those with (key >> shift) >= (prefix >> shift). The
-// block is one wave (hist: 256 words of LDS). With max_passes, the select stops after
-// that many digits: the set then holds the k_eff largest keys and possibly more (the
-// rest of the last digit's bucket), which is all a threshold needs.
+// largest keys are exactly those with (key >> shift) >= (prefix >> shift). One
+// wave runs it (hist: 256 words of LDS of its own); it synchronises only itself.
+// With max_passes, the select stops after that many digits: the set then holds the
+// k_eff largest keys and possibly more (the rest of the last digit's bucket), which
+// is all a threshold needs.
 template <int E>
 __device__ __forceinline__ void wave_radix_select(const uint64_t (&key)[E], int n, uint32_t k_eff, uint32_t* hist,
                                                   int* shift_out, uint64_t* prefix_out, int max_passes = 8) {
@@ -1136,7 +1149,7 @@ __device__ __forceinline__ void wave_radix_select(const uint64_t (&key)[E], int 
     const int width = top < 8 ? top : 8;
     shift = top - width;
     reinterpret_cast<uint4*>(hist)[lane] = make_uint4(0u, 0u, 0u, 0u);
-    __syncthreads();
+    wave_sync_lds();
     const uint64_t pre_hi = top >= 64 ? 0 : prefix >> top;
     const uint32_t dmask = (1u << width) - 1u;
 #pragma unroll
@@ -1144,7 +1157,7 @@ __device__ __forceinline__ void wave_radix_select(const uint64_t (&key)[E], int 
       const bool match = lane + 64 * e < n && (top >= 64 || (key[e] >> top) == pre_hi);
       if (match) atomicAdd(&hist[(uint32_t)(key[e] >> shift) & dmask], 1u);
     }
-    __syncthreads();
+    wave_sync_lds();
     const uint4 h4 = reinterpret_cast<const uint4*>(hist)[63 - lane];  // bins 255-4l .. 252-4l
     const uint32_t c4[4] = {h4.w, h4.z, h4.y, h4.x};                   // descending digit order
     const uint32_t local = c4[0] + c4[1] + c4[2] + c4[3];
@@ -1166,7 +1179,7 @@ __device__ __forceinline__ void wave_radix_select(const uint64_t (&key)[E], int 
     digit = (uint32_t)__builtin_amdgcn_readlane((int)digit, src);
     above = (uint32_t)__builtin_amdgcn_readlane((int)above, src);
     cnt = (uint32_t)__builtin_amdgcn_readlane((int)cnt, src);
-    __syncthreads();  // hist is cleared again by the next pass
+    wave_sync_lds();  // hist is cleared again by the next pass
     prefix |= (uint64_t)digit << shift;
     kr -= above;
     if (cnt == kr) break;  // every key of this bucket is selected
@@ -1223,7 +1236,7 @@ __device__ __forceinline__ void wave_select_store(const uint64_t (&key)[E], int 
     if (take && pos < KCAP) sbuf[pos] = key[e];
     base += __popcll(m);
   }
-  __syncthreads();
+  wave_sync_lds();
   int sorted;
   if (k_eff <= 64) wave_rank_store<1>(sbuf, k_eff, k, out), sorted = 64;
   else if (k_eff <= 128) wave_sort_store<2>(sbuf, k_eff, k, out), sorted = 128;
@@ -2006,12 +2019,6 @@ hipError_t launch_mfma_probe(int32_t* rows, int32_t* cols, hipStream_t st) {
 __global__ void k_bwd_zero(int32_t* p, int64_t n) {
   for (int64_t e = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; e < n; e += (int64_t)gridDim.x * blockDim.x)
     p[e] = 0;
-}
-
-__device__ __forceinline__ void wave_sync_lds() {
-  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
-  __builtin_amdgcn_wave_barrier();
-  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
 }
 
 __device__ __forceinline__ float wave_sum(float x) {
