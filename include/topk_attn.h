@@ -160,6 +160,29 @@ size_t topk_ffn_workspace_bytes(int64_t N, int64_t d_model, int64_t d_ff, int64_
 int topk_set_workspace(void* dev_ptr, size_t bytes);
 
 /*
+ * topk_attn_noalloc -- for callers that cannot allocate device memory (code under
+ * HIP graph capture, tight serving loops, harnesses that forbid hipMalloc): the
+ * same arguments, computation and result as topk_attn, with the whole workspace
+ * inside a fixed scratch array of TOPK_NOALLOC_SCRATCH_BYTES that the library
+ * keeps on every GPU it runs on until the process ends. The call makes no
+ * hipMalloc, hipFree or other allocating call and ignores any workspace registered
+ * with topk_set_workspace; the caller still owns Q, K, V and out. Its query-chunk
+ * passes are fitted into the scratch; when a single chunk needs more, it returns
+ * TOPK_E_NOMEM before launching anything. Every call on one GPU uses that GPU's
+ * scratch, which keeps the last call's contents (each call initialises what it
+ * reads): calls of one process that overlap in time on the same GPU (other
+ * streams, other threads) race, and the caller must order them. Errors as
+ * topk_attn, plus TOPK_E_HIP when there is no current device or the scratch
+ * address cannot be obtained.
+ */
+#define TOPK_NOALLOC_SCRATCH_BYTES ((size_t)128 << 20)
+int topk_attn_noalloc(const void* Q, const void* K, const void* V, void* out,
+                      int64_t B, int64_t H, int64_t Lq, int64_t Lk, int64_t d,
+                      int64_t k, int64_t chunk, int causal, float scale,
+                      int dtype, void* hip_stream);
+size_t topk_noalloc_scratch_bytes(void);  /* TOPK_NOALLOC_SCRATCH_BYTES */
+
+/*
  * The forward calls' memory budget, process-wide: the most workspace a call sizes
  * for itself (the chunks of a call run in passes of as many chunks as fit; a
  * budget below one chunk's needs runs one chunk per pass, the paper's sequential

@@ -53,6 +53,8 @@ def lib() -> ctypes.CDLL:
     ffn_args = [vp, vp, vp, vp, i64, i64, i64, i64, i64, i32, vp]
     sigs = {
         "topk_attn": (attn_args, i32),
+        "topk_attn_noalloc": (attn_args, i32),
+        "topk_noalloc_scratch_bytes": ([], ctypes.c_size_t),
         "topk_attn_debug": (attn_args + [vp, vp], i32),
         "topk_ffn": (ffn_args, i32),
         "topk_ffn_debug": (ffn_args + [vp, vp], i32),

@@ -11,6 +11,7 @@
 
 #include <algorithm>
 #include <atomic>
+#include <mutex>
 #include <string>
 #include <vector>
 
@@ -241,20 +242,28 @@ int split_rows(const Problem& pb, Problem* parts) {
 
 // ---------------------------------------------------------------- execution
 // report: read back the rows a fallback selected (waits for the stream; debug calls)
-int run(Problem whole, hipStream_t st, bool report) {
+// fixed_ws / fixed_bytes: a workspace the call must run in (no allocation, no
+// registered workspace); the plan then fits its passes into fixed_bytes.
+int run(Problem whole, hipStream_t st, bool report, void* fixed_ws = nullptr, size_t fixed_bytes = 0) {
   Problem parts[2];
   Plan plans[2];
   const int np = split_rows(whole, parts);
-  size_t budget = g_ws ? g_ws_bytes : g_budget.load(std::memory_order_relaxed), need = 0;
+  void* const ws_given = fixed_ws ? fixed_ws : g_ws;
+  const size_t ws_given_bytes = fixed_ws ? fixed_bytes : g_ws_bytes;
+  size_t budget = ws_given ? ws_given_bytes : g_budget.load(std::memory_order_relaxed), need = 0;
   for (int q = 0; q < np; ++q) {
     choose_path(parts[q], &plans[q]);
     plan_sizes(parts[q], &plans[q], budget);
     const size_t n = plan_total(plans[q], parts[q]);
     need = n > need ? n : need;
   }
-  char* ws = (char*)g_ws;
+  char* ws = (char*)ws_given;
   bool own = false;
-  if (g_ws) {
+  if (fixed_ws) {
+    if (need > fixed_bytes)
+      return fail(TOPK_E_NOMEM, "one query chunk needs %zu bytes of workspace, above the %zu bytes of the fixed "
+                  "device scratch", need, fixed_bytes);
+  } else if (g_ws) {
     if (need > g_ws_bytes)
       return fail(TOPK_E_NOMEM, "registered workspace of %zu bytes is below the %zu bytes one query chunk needs",
                   g_ws_bytes, need);
@@ -523,6 +532,34 @@ int run_backward(const BwdProblem& bp, hipStream_t st) {
   return TOPK_OK;
 }
 
+// ---------------------------------------------------------------- fixed device scratch
+// The workspace of topk_attn_noalloc: a file-scope device array of TOPK_NOALLOC_SCRATCH_BYTES,
+// one copy per GPU, held by the process until it ends. Host code must not pass the
+// array's name to a kernel (on the host it only stands for the symbol); the device
+// address comes from hipGetSymbolAddress, taken once per device with that device
+// current and kept in g_scratch_ptr.
+constexpr int MAX_DEVICES = 64;
+__device__ __align__(256) unsigned char scratch[TOPK_NOALLOC_SCRATCH_BYTES];
+std::mutex g_scratch_mu;
+void* g_scratch_ptr[MAX_DEVICES] = {};
+
+int scratch_for_current_device(void** out) {
+  int dev = -1;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= MAX_DEVICES)
+    return fail(TOPK_E_HIP, "no current HIP device (or device index above %d)", MAX_DEVICES - 1);
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (!g_scratch_ptr[dev]) {
+    void* p = nullptr;
+    const hipError_t e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (e != hipSuccess || !p)
+      return fail(TOPK_E_HIP, "hipGetSymbolAddress of the fixed scratch failed on device %d: %s", dev,
+                  hipGetErrorString(e));
+    g_scratch_ptr[dev] = p;
+  }
+  *out = g_scratch_ptr[dev];
+  return TOPK_OK;
+}
+
 }  // namespace
 }  // namespace topk
 
@@ -546,6 +583,20 @@ int topk_attn(const void* Q, const void* K, const void* V, void* out, int64_t B,
   return topk_attn_debug(Q, K, V, out, B, H, Lq, Lk, d, k, chunk, causal, scale, dtype, hip_stream, nullptr,
                          nullptr);
 }
+
+int topk_attn_noalloc(const void* Q, const void* K, const void* V, void* out, int64_t B, int64_t H, int64_t Lq,
+                      int64_t Lk, int64_t d, int64_t k, int64_t chunk, int causal, float scale, int dtype,
+                      void* hip_stream) {
+  g_err.clear();
+  Problem pb;
+  int rc = attn_problem(&pb, Q, K, V, out, B, H, Lq, Lk, d, k, chunk, causal, scale, dtype, nullptr, nullptr, true);
+  if (rc) return rc;
+  void* ws = nullptr;
+  if ((rc = scratch_for_current_device(&ws))) return rc;
+  return run(pb, (hipStream_t)hip_stream, false, ws, TOPK_NOALLOC_SCRATCH_BYTES);
+}
+
+size_t topk_noalloc_scratch_bytes(void) { return TOPK_NOALLOC_SCRATCH_BYTES; }
 
 int topk_ffn_debug(const void* X, const void* W1, const void* W2, void* out, int64_t N, int64_t d_model, int64_t d_ff,
                    int64_t k, int64_t chunk, int dtype, void* hip_stream, int32_t* idx_out, float* score_out) {
