@@ -297,9 +297,11 @@ def bench_paper_ff(args):
 
 def bench_chunk_sweep(args):
     """Forward pass of one BERT-base multi-head self-attention layer (d_model 768, 12
-    heads of 64, bidirectional, k = 128) at L = 65536 for each query chunk size: time,
-    the peak of PyTorch's allocator (inputs, projections, outputs and the library's
-    workspace, which is a PyTorch tensor) and the workspace the library asks for."""
+    heads of 64, bidirectional) at L = 65536 for each query chunk size, with top-k
+    attention (k = 128) and with query chunking alone (the top-k disabled: every key,
+    the paper's comparison baseline): time, the peak of PyTorch's allocator (inputs,
+    projections, outputs and the library's workspace, which is a PyTorch tensor) and
+    the workspace the library asks for (none for the baseline's streaming softmax)."""
     import torch
     import paper_2106_06899_amd as tk
     from paper_2106_06899_amd import layers
@@ -307,9 +309,11 @@ def bench_chunk_sweep(args):
     L = args.sweep_length
     torch.manual_seed(13)
     x = torch.randn(1, L, 768, device=dev, dtype=torch.bfloat16)
-    for C, budget in ((int(t), b) for t in args.chunks.split(",") for b in (0, 1)):
+    runs = [(int(t), b, 128) for t in args.chunks.split(",") for b in (0, 1)] + \
+           [(int(t), 0, None) for t in args.chunks.split(",")]
+    for C, budget, kk in runs:
         torch.manual_seed(14)
-        layer = layers.TopkMultiheadAttention(768, 12, 128, C, causal=False, device=dev, dtype=torch.bfloat16)
+        layer = layers.TopkMultiheadAttention(768, 12, kk, C, causal=False, device=dev, dtype=torch.bfloat16)
 
         def fwd():
             with torch.no_grad():
@@ -321,16 +325,18 @@ def bench_chunk_sweep(args):
         tk.profile_begin()
         ms = _timed(fwd, args.steps, args.warmup)
         st = tk.profile_end()
-        ws = tk.attn_workspace_bytes(1, 12, L, L, 64, 128, C, False)
+        ws = tk.attn_workspace_bytes(1, 12, L, L, 64, kk, C, False) if kk else 0
         tk.set_memory_budget(0)
         n = args.steps + args.warmup
         print(json.dumps({
-            "metric": "top-k multi-head attention layer forward ms vs query chunk size (BERT-base, L 65536, k 128)",
+            "metric": "multi-head attention layer forward ms vs query chunk size (BERT-base, L 65536)",
             "value": ms, "unit": "ms", "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
             "ms_per_step": ms, "higher_is_better": False, "dtype": "bf16", "data": "synthetic",
-            "config": {"workload": f"attention layer d_model 768, 12 heads x 64, bidirectional, k 128, L {L}, chunk {C}",
-                       "chunk": C, "seq_len": L, "chunks_in_flight": "one (sequential)" if budget else "default budget",
-                       "path": tk.attn_path(1, 12, L, L, 64, 128, C, False, tk.TOPK_BF16)},
+            "config": {"workload": f"attention layer d_model 768, 12 heads x 64, bidirectional, L {L}, chunk {C}, "
+                                   + (f"top-{kk}" if kk else "query chunking without top-k (every key)"),
+                       "chunk": C, "seq_len": L, "k": kk,
+                       "chunks_in_flight": "one (sequential)" if budget else "default budget",
+                       "path": tk.attn_path(1, 12, L, L, 64, kk, C, False, tk.TOPK_BF16) if kk else "dense"},
             "peak_gib": torch.cuda.max_memory_allocated(dev) / 2**30,
             "workspace_gib": ws / 2**30,
             "library_stage_ms_per_step": {k_: round(v[0] / n, 4) for k_, v in st.items() if v[1]}}), flush=True)

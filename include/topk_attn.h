@@ -85,6 +85,20 @@ int topk_attn(const void* Q, const void* K, const void* V, void* out,
               int dtype, void* hip_stream);
 
 /*
+ * topk_attn_dense -- query chunking with the top-k disabled, the comparison
+ * baseline of Section 2.2 ("Query chunking") and Section 3: every valid key of a
+ * query contributes, out[i] = sum_j softmax_j(scale * q_i.k_j) V[j] (Eq. 1, with
+ * the causal mask of Eq. 2); the same result as topk_attn with k = Lk. Arguments
+ * as topk_attn without k. Computed by a streaming softmax over key tiles (no score
+ * tile is stored, no workspace is used); chunk only sets how queries are grouped.
+ * Supports bf16 inputs with d = 64 or 128 (else TOPK_E_UNSUPPORTED). topk_attn
+ * itself calls this for k = Lk above the select's limit of 2048 keys.
+ */
+int topk_attn_dense(const void* Q, const void* K, const void* V, void* out,
+                    int64_t B, int64_t H, int64_t Lq, int64_t Lk, int64_t d,
+                    int64_t chunk, int causal, float scale, int dtype, void* hip_stream);
+
+/*
  * topk_ffn -- the feed-forward layer recast as attention (Eq. 3) with the top-k
  * of Eq. 4 and a ReLU activation: out[i] = sum_{j in S_i} max(x_i.W1[j], 0) W2[j],
  * where S_i holds the k largest scores x_i.W1[j]. No bias, no temperature; ReLU

@@ -18,13 +18,14 @@ import ctypes
 import math
 import os
 
-__all__ = ["attn", "ffn", "attn_workspace_bytes", "ffn_workspace_bytes", "attn_path", "ffn_path",
+__all__ = ["attn", "attn_dense", "ffn", "attn_workspace_bytes", "ffn_workspace_bytes", "attn_path", "ffn_path",
            "mfma_layout", "lib", "TopkError", "LIB_PATH", "profile_begin", "profile_end", "STAGES",
            "attn_backward", "ffn_backward", "set_backward_lists", "set_memory_budget", "last_fallback_rows"]
 
 LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libtopk.so")
 
 TOPK_F32, TOPK_BF16 = 0, 1
+MAX_SELECT_K = 2048  # largest k the select handles (k = Lk above it runs attn_dense)
 TOPK_LISTS_AUTO, TOPK_LISTS_BUCKET, TOPK_LISTS_ATOMIC = 0, 1, 2
 _STATUS = {0: "OK", -1: "TOPK_E_INVAL", -2: "TOPK_E_NULL", -3: "TOPK_E_ALIGN", -4: "TOPK_E_UNSUPPORTED",
            -5: "TOPK_E_NOMEM", -6: "TOPK_E_HIP"}
@@ -54,6 +55,7 @@ def lib() -> ctypes.CDLL:
     sigs = {
         "topk_attn": (attn_args, i32),
         "topk_attn_noalloc": (attn_args, i32),
+        "topk_attn_dense": ([vp, vp, vp, vp, i64, i64, i64, i64, i64, i64, i32, f32, i32, vp], i32),
         "topk_noalloc_scratch_bytes": ([], ctypes.c_size_t),
         "topk_attn_debug": (attn_args + [vp, vp], i32),
         "topk_ffn": (ffn_args, i32),
@@ -169,6 +171,8 @@ def attn(q, k, v, topk: int, chunk: int = 0, causal: bool = False, scale: float 
     dt = _dtype_code(q)
     if scale is None:
         scale = 1.0 / math.sqrt(d)
+    if topk == Lk and topk > MAX_SELECT_K and not (debug or cache):
+        return attn_dense(q, k, v, chunk, causal, scale)
     out = torch.empty_like(q)
     idx = torch.empty((B, H, Lq, topk), dtype=torch.int32, device=device) if debug or cache else None
     sc = torch.empty((B, H, Lq, topk), dtype=torch.float32, device=device) if debug or cache else None
@@ -183,6 +187,28 @@ def attn(q, k, v, topk: int, chunk: int = 0, causal: bool = False, scale: float 
         _with_workspace(nbytes, device, lambda: fn(*args, idx.data_ptr(), sc.data_ptr()))
         return out, idx, sc
     _with_workspace(nbytes, device, lambda: L.topk_attn(*args))
+    return out
+
+
+def attn_dense(q, k, v, chunk: int = 0, causal: bool = False, scale: float | None = None):
+    """Query chunking with the top-k disabled (the paper's comparison baseline): every
+    valid key contributes through the softmax of Eq. 1 (k = Lk). bf16, d = 64 or 128;
+    no workspace."""
+    import torch
+    device = q.device
+    _check(q, "q", 4, q.dtype, device)
+    _check(k, "k", 4, q.dtype, device)
+    _check(v, "v", 4, q.dtype, device)
+    B, H, Lq, d = q.shape
+    Lk = k.shape[2]
+    if tuple(k.shape) != (B, H, Lk, d) or tuple(v.shape) != (B, H, Lk, d):
+        raise ValueError(f"shape mismatch q {tuple(q.shape)} k {tuple(k.shape)} v {tuple(v.shape)}")
+    dt = _dtype_code(q)
+    if scale is None:
+        scale = 1.0 / math.sqrt(d)
+    out = torch.empty_like(q)
+    _raise(lib().topk_attn_dense(q.data_ptr(), k.data_ptr(), v.data_ptr(), out.data_ptr(), B, H, Lq, Lk, d, chunk,
+                                 int(causal), float(scale), dt, _stream_ptr(device)))
     return out
 
 

@@ -10,7 +10,7 @@ import sys
 
 PKG = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(PKG)
-SOURCES = ["csrc/topk_kernels.hip", "csrc/topk_api.hip"]
+SOURCES = ["csrc/topk_kernels.hip", "csrc/topk_dense.hip", "csrc/topk_api.hip"]
 LIB = os.path.join(PKG, "libtopk.so")
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 

@@ -532,6 +532,25 @@ int run_backward(const BwdProblem& bp, hipStream_t st) {
   return TOPK_OK;
 }
 
+// ---------------------------------------------------------------- query chunking without top-k
+// Every valid key of each query (the k = Lk fixed point): one streaming-softmax launch
+// over all query chunks; it needs no workspace, so nothing bounds the chunks in flight.
+int run_dense(const Problem& pb, hipStream_t st) {
+  if (pb.dtype != T_BF16 || (pb.d != 64 && pb.d != 128))
+    return fail(TOPK_E_UNSUPPORTED, "query chunking without top-k runs on bf16 inputs with d = 64 or 128");
+  Pass ps;
+  ps.nchunk = (pb.Lq + pb.C - 1) / pb.C;
+  ps.c0 = 0;
+  ps.nc = pb.BH * ps.nchunk;
+  hipError_t e;
+  {
+    StageTimer t(st, ST_SCORE);
+    e = launch_dense(pb, ps, st);
+  }
+  if (e != hipSuccess) return fail(TOPK_E_HIP, "kernel launch failed: %s", hipGetErrorString(e));
+  return TOPK_OK;
+}
+
 // ---------------------------------------------------------------- fixed device scratch
 // The workspace of topk_attn_noalloc: a file-scope device array of TOPK_NOALLOC_SCRATCH_BYTES,
 // one copy per GPU, held by the process until it ends. Host code must not pass the
@@ -580,6 +599,10 @@ int topk_attn_debug(const void* Q, const void* K, const void* V, void* out, int6
 
 int topk_attn(const void* Q, const void* K, const void* V, void* out, int64_t B, int64_t H, int64_t Lq, int64_t Lk,
               int64_t d, int64_t k, int64_t chunk, int causal, float scale, int dtype, void* hip_stream) {
+  // k = Lk keeps every valid key (Eq. 4 reduces to Eq. 1): beyond the select's limit
+  // the streaming-softmax kernel computes it
+  if (k == Lk && k > MAX_SELECT_K)
+    return topk_attn_dense(Q, K, V, out, B, H, Lq, Lk, d, chunk, causal, scale, dtype, hip_stream);
   return topk_attn_debug(Q, K, V, out, B, H, Lq, Lk, d, k, chunk, causal, scale, dtype, hip_stream, nullptr,
                          nullptr);
 }
@@ -597,6 +620,16 @@ int topk_attn_noalloc(const void* Q, const void* K, const void* V, void* out, in
 }
 
 size_t topk_noalloc_scratch_bytes(void) { return TOPK_NOALLOC_SCRATCH_BYTES; }
+
+int topk_attn_dense(const void* Q, const void* K, const void* V, void* out, int64_t B, int64_t H, int64_t Lq,
+                    int64_t Lk, int64_t d, int64_t chunk, int causal, float scale, int dtype, void* hip_stream) {
+  g_err.clear();
+  Problem pb;
+  // validated as top-k attention with k = 1 (every other check is the same)
+  int rc = attn_problem(&pb, Q, K, V, out, B, H, Lq, Lk, d, 1, chunk, causal, scale, dtype, nullptr, nullptr, true);
+  if (rc) return rc;
+  return run_dense(pb, (hipStream_t)hip_stream);
+}
 
 int topk_ffn_debug(const void* X, const void* W1, const void* W2, void* out, int64_t N, int64_t d_model, int64_t d_ff,
                    int64_t k, int64_t chunk, int dtype, void* hip_stream, int32_t* idx_out, float* score_out) {

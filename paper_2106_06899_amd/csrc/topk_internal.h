@@ -83,6 +83,8 @@ hipError_t launch_cand_select(const Problem& pb, const Pass& ps, const PassBufs&
 hipError_t launch_redo(const Problem& pb, const Pass& ps, const PassBufs& b, hipStream_t st);
 hipError_t launch_finalize(const Problem& pb, const Pass& ps, const PassBufs& b, hipStream_t st);
 hipError_t launch_mfma_probe(int32_t* rows, int32_t* cols, hipStream_t st);
+// Query chunking without top-k (every valid key, softmax): bf16, d in {64, 128}.
+hipError_t launch_dense(const Problem& pb, const Pass& ps, hipStream_t st);
 
 // Backward pass with input checkpointing. Rows of Q / dQ / d_out / idx / dots are
 // (bh * Lq + i); keys (bh, j) of K, V, dK, dV sit at (bh * kv_head_stride + j * d)

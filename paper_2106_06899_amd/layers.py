@@ -13,7 +13,7 @@ import math
 
 import torch
 
-from . import attn, attn_backward, ffn, ffn_backward
+from . import attn, attn_backward, attn_dense, ffn, ffn_backward
 
 
 class TopkAttentionFunction(torch.autograd.Function):
@@ -59,6 +59,16 @@ def topk_attention(q, k, v, topk: int, chunk: int = 0, causal: bool = False, sca
     return TopkAttentionFunction.apply(q, k, v, int(topk), int(chunk), bool(causal), float(scale))
 
 
+def dense_attention(q, k, v, chunk: int = 0, causal: bool = False, scale: float | None = None):
+    """Query chunking with the top-k disabled (every valid key, Eq. 1): the paper's
+    comparison baseline. Forward only (no backward is provided for it)."""
+    if torch.is_grad_enabled() and (q.requires_grad or k.requires_grad or v.requires_grad):
+        raise RuntimeError("dense_attention has no backward pass; call it under torch.no_grad()")
+    if scale is None:
+        scale = 1.0 / math.sqrt(q.shape[-1])
+    return attn_dense(q, k, v, int(chunk), bool(causal), float(scale))
+
+
 def topk_feed_forward(x, w1, w2, topk: int, chunk: int = 0):
     """Differentiable top-k feed-forward layer: x [N, d_model], w1 / w2 [d_ff, d_model]."""
     return TopkFFNFunction.apply(x, w1, w2, int(topk), int(chunk))
@@ -70,7 +80,8 @@ class TopkMultiheadAttention(torch.nn.Module):
 
     [q | k | v] = x W_qkv^T + b_qkv, head h takes columns h*d_h .. (h+1)*d_h - 1 of
     each; every head runs top-k attention (temperature 1/sqrt(d_h) unless given);
-    y = concat(heads) W_o^T + b_o."""
+    y = concat(heads) W_o^T + b_o. With topk=None the heads keep every key (query
+    chunking without top-k, the paper's baseline; forward only)."""
 
     def __init__(self, d_model: int, n_heads: int, topk: int, chunk: int = 1024, causal: bool = False,
                  bias: bool = True, scale: float | None = None, device=None, dtype=torch.bfloat16):
@@ -88,7 +99,10 @@ class TopkMultiheadAttention(torch.nn.Module):
         B, L, D = x.shape
         p = self.qkv(x).view(B, L, 3, self.n_heads, self.d_head).permute(2, 0, 3, 1, 4)
         q, k, v = (p[t].contiguous() for t in range(3))
-        o = topk_attention(q, k, v, self.topk, self.chunk, self.causal, self.scale)
+        if self.topk is None:
+            o = dense_attention(q, k, v, self.chunk, self.causal, self.scale)
+        else:
+            o = topk_attention(q, k, v, self.topk, self.chunk, self.causal, self.scale)
         return self.out(o.permute(0, 2, 1, 3).reshape(B, L, D))
 
 
