@@ -172,8 +172,13 @@ def bench_backward(args, w, x, dev_tensor):
     stages = tk.profile_end()
     ms_step = 1e3 * elapsed / args.steps
     bwd_ms = stages["backward"][0] / max(stages["backward"][1], 1)
-    algo_bytes = pairs * (4 * d * elem + 8) + (rows + 2 * keys) * d * elem
-    achieved = algo_bytes / (bwd_ms / 1e3) / 1e9
+    # HBM roofline on the bytes the call must move at least once: Q and d_out (rows),
+    # K and V (keys) read, the cache (index, score) read, d_Q, d_K, d_V written. The
+    # per-pair row gathers (V[j], K[j] per row; d_out[i], Q[i] per key) are far larger
+    # but mostly hit L2/MALL, so they are reported beside it, not against HBM.
+    io_bytes = (2 * rows + 2 * keys) * d * elem + pairs * 8 + (rows + 2 * keys) * d * elem
+    gathered = pairs * 4 * d * elem
+    achieved = io_bytes / (bwd_ms / 1e3) / 1e9
     rec = {
         "metric": "top-k attention backward (input checkpointing) queries/s",
         "value": rows / (ms_step / 1e3), "unit": "queries/s", "n_gpus": 1, "steps": args.steps,
@@ -182,7 +187,9 @@ def bench_backward(args, w, x, dev_tensor):
         "config": {"workload": f"{w.name}: {w.note}", "selected_pairs": pairs},
         "roofline": {"kernel": "backward call (list build, row and key gathers)", "bound": "hbm", "achieved": achieved,
                      "peak": PEAK_HBM_GBS, "unit": "GB/s", "frac": achieved / PEAK_HBM_GBS, "traffic": None,
-                     "algorithmic_bytes_per_launch": algo_bytes, "avg_launch_ms": bwd_ms},
+                     "algorithmic_bytes_per_launch": io_bytes, "avg_launch_ms": bwd_ms},
+        "gathered_rows": {"bytes_per_launch": gathered, "GB_per_s": gathered / (bwd_ms / 1e3) / 1e9,
+                          "served_from": "L2 / MALL mostly (each selected pair gathers four rows)"},
     }
     print(json.dumps(rec), flush=True)
 
@@ -256,6 +263,7 @@ def bench_paper_ff(args):
     gen = torch.Generator(device=dev).manual_seed(12)
     x = torch.randn(N, dm, device=dev, dtype=torch.bfloat16, generator=gen).requires_grad_()
     g = torch.randn(N, dm, device=dev, dtype=torch.bfloat16, generator=gen)
+    fits = []
     for dff in (int(t) for t in args.d_ff.split(",")):
         w1 = (0.02 * torch.randn(dff, dm, device=dev, generator=gen)).to(torch.bfloat16).requires_grad_()
         w2 = (0.02 * torch.randn(dff, dm, device=dev, generator=gen)).to(torch.bfloat16).requires_grad_()
@@ -291,8 +299,22 @@ def bench_paper_ff(args):
             "forward_workspace_gib": tk.ffn_workspace_bytes(N, dm, dff, k, C) / 2**30,
             "peak_gib_forward": peak_fwd / 2**30, "peak_gib_train": peak_train / 2**30,
             "library_stage_ms_per_step": {k_: round(v[0] / n, 4) for k_, v in st.items() if v[1]}}), flush=True)
+        fits.append((dff, peak_train / 2**30))
         del w1, w2
         x.grad = None
+    if len(fits) >= 2:
+        # least-squares line through (d_ff, peak GiB of a training step); the largest
+        # d_ff whose fitted peak stays within 30 GiB (the paper's Fig. 3b extrapolation)
+        xs = np.array([f[0] for f in fits], dtype=np.float64)
+        ys = np.array([f[1] for f in fits], dtype=np.float64)
+        slope, icpt = np.polyfit(xs, ys, 1)
+        print(json.dumps({
+            "metric": "largest d_ff whose forward + backward peak memory fits 30 GiB (linear fit)",
+            "value": float((30.0 - icpt) / slope) if slope > 0 else None, "unit": "hidden units",
+            "n_gpus": 1, "higher_is_better": True, "dtype": "bf16", "data": "synthetic",
+            "config": {"workload": "feed-forward layer N 2^18, d_model 768, k 512, chunk 2^14",
+                       "fit_points": [[int(a), round(b, 4)] for a, b in fits]},
+            "gib_per_hidden_unit": slope, "intercept_gib": icpt}), flush=True)
 
 
 def bench_chunk_sweep(args):
@@ -503,6 +525,35 @@ def main():
     score_tflops_call = flops / (ms_step / 1e3) / 1e12
     traffic = traffic_for_current_kernel(w.name, path)
 
+    # score + select: the fused path's candidate select finishes what the scan's filter
+    # started, so the pair is reported as one figure beside the scan alone
+    sel_ms = stages["select"][0] / args.steps
+    score_step_ms = scan_ms / args.steps
+    score_select = {"ms_per_step": score_step_ms + sel_ms,
+                    "tflops": flops / ((score_step_ms + sel_ms) / 1e3) / 1e12}
+    score_select["frac"] = score_select["tflops"] / PEAK_BF16_TFLOPS
+    core = None
+    if path == 1 and w.kind == "attn" and w.d == 64 and 32 < w.k <= 64 and not w.causal:
+        # the scan's score-core ablation at the same launch shape (no filter): its ceiling
+        for abl in (False, True):
+            tk.scan_ablation(q, k, w.k, w.chunk, score_only=abl)  # warm-up
+        torch.cuda.synchronize()
+        res = {}
+        for abl in (False, True):
+            tk.profile_begin()
+            for _ in range(5):
+                tk.scan_ablation(q, k, w.k, w.chunk, score_only=abl)
+            torch.cuda.synchronize()
+            st_ = tk.profile_end()["score"]
+            res[abl] = st_[0] / max(st_[1], 1)
+        core = {"kernel": "k_fused_scan score-only ablation (MFMA, K tiles, block maxima; no filter)",
+                "avg_launch_ms": res[True], "tflops": flops_per_launch / (res[True] / 1e3) / 1e12,
+                "full_scan_same_run_ms": res[False]}
+        core["frac"] = core["tflops"] / PEAK_BF16_TFLOPS
+    mt, mhz = tk.probe_mfma()
+    mfma = {"sustained_tflops": mt, "frac_of_datasheet": mt / PEAK_BF16_TFLOPS, "shader_clock_mhz": mhz,
+            "note": "register-only v_mfma_f32_32x32x16_bf16 stream, two waves per SIMD on every CU"}
+
     cpu = None
     if not args.no_cpu:
         print("[bench] timing the CPU oracle", file=sys.stderr, flush=True)
@@ -529,8 +580,16 @@ def main():
         "score_tflops_whole_call": score_tflops_call,
         "score_frac_of_bf16_peak_whole_call": score_tflops_call / PEAK_BF16_TFLOPS,
         "stage_ms_per_step": {s: stages[s][0] / args.steps for s in stages},
+        "score_select": score_select,
+        "score_core_ceiling": core,
+        "mfma_probe": mfma,
         "roofline": {
-            "kernel": f"k_fused_scan (d={w.d})" if path == 1 else "k_tile_scores",
+            "kernel": {1: f"k_fused_scan (d={w.d})",
+                       2: "score stage: k_tile_scores_mfma" if w.dtype == wl.BF16 and w.d % 32 == 0 else
+                          "score stage: k_tile_scores (fp32)",
+                       3: "score stage: k_tile_scores_mfma (rows below 1024 R) + k_fused_scan",
+                       4: "score stage: k_tile_scores_mfma sample + k_filter_threshold + filtered "
+                          "k_tile_scores_mfma"}.get(path, str(path)),
             "bound": "mfma",
             "achieved": achieved,
             "peak": PEAK_BF16_TFLOPS,

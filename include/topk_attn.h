@@ -316,6 +316,27 @@ int64_t topk_last_fallback_rows(void);
  */
 int topk_selftest_mfma_layout(int32_t* rows_out, int32_t* cols_out, void* hip_stream);
 
+/*
+ * Measurement hook: run only the fused path's score kernel (its sampled threshold
+ * phase and scan) of a topk_attn call on bf16 Q, K [B, H, L, 64] with 32 < k <= 64,
+ * as many passes as the call would run; with score_only = 1 the scan's score-core
+ * ablation runs instead (the same K tile pipeline, MFMAs and block maxima, no
+ * filter and no candidate output). Nothing useful is written; the kernels' time is
+ * read with topk_profile_begin / topk_profile_end (stage "score"). Allocates its
+ * workspace. TOPK_E_UNSUPPORTED for other shapes or paths.
+ */
+int topk_scan_ablation(const void* Q, const void* K, int64_t B, int64_t H, int64_t Lq, int64_t Lk,
+                       int64_t d, int64_t k, int64_t chunk, int score_only, void* hip_stream);
+
+/*
+ * Measurement hook: the sustained rate of v_mfma_f32_32x32x16_bf16 on the current
+ * device (a register-only stream of independent MFMAs, two waves per SIMD on every
+ * CU, timed with HIP events), in TFLOP/s, and the shader clock those MFMAs ran at
+ * (shader clock counter over the constant 100 MHz counter), in MHz. Waits for the
+ * stream. Returns TOPK_OK, TOPK_E_NULL, TOPK_E_NOMEM or TOPK_E_HIP.
+ */
+int topk_probe_mfma(double* tflops, double* clock_mhz, void* hip_stream);
+
 #ifdef __cplusplus
 }
 #endif

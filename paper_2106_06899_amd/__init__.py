@@ -18,7 +18,7 @@ import ctypes
 import math
 import os
 
-__all__ = ["attn", "attn_dense", "ffn", "attn_workspace_bytes", "ffn_workspace_bytes", "attn_path", "ffn_path",
+__all__ = ["attn", "attn_dense", "scan_ablation", "probe_mfma", "ffn", "attn_workspace_bytes", "ffn_workspace_bytes", "attn_path", "ffn_path",
            "mfma_layout", "lib", "TopkError", "LIB_PATH", "profile_begin", "profile_end", "STAGES",
            "attn_backward", "ffn_backward", "set_backward_lists", "set_memory_budget", "last_fallback_rows"]
 
@@ -76,6 +76,8 @@ def lib() -> ctypes.CDLL:
         "topk_attn_path": ([i64] * 7 + [i32, i32], i32),
         "topk_ffn_path": ([i64] * 5 + [i32], i32),
         "topk_selftest_mfma_layout": ([vp, vp, vp], i32),
+        "topk_scan_ablation": ([vp, vp] + [i64] * 7 + [i32, vp], i32),
+        "topk_probe_mfma": ([ctypes.POINTER(ctypes.c_double), ctypes.POINTER(ctypes.c_double), vp], i32),
         "topk_profile_begin": ([], i32),
         "topk_profile_end": ([ctypes.POINTER(ctypes.c_double), ctypes.POINTER(ctypes.c_int64), i32], i32),
     }
@@ -188,6 +190,24 @@ def attn(q, k, v, topk: int, chunk: int = 0, causal: bool = False, scale: float 
         return out, idx, sc
     _with_workspace(nbytes, device, lambda: L.topk_attn(*args))
     return out
+
+
+def scan_ablation(q, k, topk: int, chunk: int = 0, score_only: bool = False):
+    """Measurement hook: only the fused path's score kernel of an attention call
+    (``score_only``: the score-core ablation without the filter); time it with
+    profile_begin / profile_end (stage "score")."""
+    B, H, Lq, d = q.shape
+    Lk = k.shape[2]
+    _raise(lib().topk_scan_ablation(q.data_ptr(), k.data_ptr(), B, H, Lq, Lk, d, topk, chunk, int(score_only),
+                                    _stream_ptr(q.device)))
+
+
+def probe_mfma():
+    """(sustained bf16 MFMA TFLOP/s, shader clock MHz) of the current device."""
+    t, c = ctypes.c_double(), ctypes.c_double()
+    import torch
+    _raise(lib().topk_probe_mfma(ctypes.byref(t), ctypes.byref(c), _stream_ptr(torch.device("cuda", torch.cuda.current_device()))))
+    return t.value, c.value
 
 
 def attn_dense(q, k, v, chunk: int = 0, causal: bool = False, scale: float | None = None):

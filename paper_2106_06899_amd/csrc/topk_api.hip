@@ -631,6 +631,81 @@ int topk_attn_dense(const void* Q, const void* K, const void* V, void* out, int6
   return run_dense(pb, (hipStream_t)hip_stream);
 }
 
+int topk_scan_ablation(const void* Q, const void* K, int64_t B, int64_t H, int64_t Lq, int64_t Lk, int64_t d,
+                       int64_t k, int64_t chunk, int score_only, void* hip_stream) {
+  g_err.clear();
+  Problem pb;
+  int rc = attn_problem(&pb, Q, K, K, (void*)Q, B, H, Lq, Lk, d, k, chunk, 0, 1.f, TOPK_BF16, nullptr, nullptr, true);
+  if (rc) return rc;
+  Plan pl;
+  choose_path(pb, &pl);
+  if (pl.path != PATH_FUSED || pl.scan.mode != MODE_SAMPLE || pb.d != 64 || pl.scan.R != 6)
+    return fail(TOPK_E_UNSUPPORTED, "the scan ablation runs on the sampled fused path with d = 64, 32 < k <= 64");
+  pl.scan.score_only = score_only ? 1 : 0;
+  plan_sizes(pb, &pl, g_budget.load(std::memory_order_relaxed));
+  const size_t need = plan_total(pl, pb);
+  hipStream_t st = (hipStream_t)hip_stream;
+  char* ws = nullptr;
+  if (hipMallocAsync((void**)&ws, need, st) != hipSuccess)
+    return fail(TOPK_E_NOMEM, "could not allocate %zu bytes of workspace", need);
+  hipError_t e = hipSuccess;
+  for (int64_t c0 = 0; c0 < pl.total_chunks && e == hipSuccess; c0 += pl.per_pass) {
+    Pass ps;
+    ps.c0 = c0;
+    ps.nc = pl.total_chunks - c0 < pl.per_pass ? pl.total_chunks - c0 : pl.per_pass;
+    ps.nchunk = pl.nchunk;
+    PassBufs b = carve(pb, pl, ws);
+    e = launch_init(b, st);
+    if (e == hipSuccess) {
+      StageTimer t(st, ST_SCORE);
+      e = launch_fused_scan(pb, ps, b, pl.scan, st);
+    }
+  }
+  hipFreeAsync(ws, st);
+  if (e != hipSuccess) return fail(TOPK_E_HIP, "kernel launch failed: %s", hipGetErrorString(e));
+  return TOPK_OK;
+}
+
+int topk_probe_mfma(double* tflops, double* clock_mhz, void* hip_stream) {
+  g_err.clear();
+  if (!tflops || !clock_mhz) return fail(TOPK_E_NULL, "tflops and clock_mhz are required");
+  hipStream_t st = (hipStream_t)hip_stream;
+  int dev = 0, cus = 0;
+  if (hipGetDevice(&dev) != hipSuccess || hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) !=
+                                              hipSuccess)
+    return fail(TOPK_E_HIP, "no current HIP device");
+  const int blocks = cus * 8;  // two waves per SIMD
+  float* sink = nullptr;
+  uint64_t* clk = nullptr;
+  if (hipMallocAsync((void**)&sink, (size_t)blocks * 256 * 4, st) != hipSuccess ||
+      hipMallocAsync((void**)&clk, (size_t)blocks * 16, st) != hipSuccess)
+    return fail(TOPK_E_NOMEM, "could not allocate the probe buffers");
+  hipEvent_t a, b;
+  hipEventCreate(&a);
+  hipEventCreate(&b);
+  hipError_t e = launch_mfma_rate(sink, clk, blocks, st);  // warm-up
+  hipEventRecord(a, st);
+  if (e == hipSuccess) e = launch_mfma_rate(sink, clk, blocks, st);
+  hipEventRecord(b, st);
+  std::vector<uint64_t> h((size_t)blocks * 2);
+  if (e == hipSuccess) e = hipMemcpyAsync(h.data(), clk, h.size() * 8, hipMemcpyDeviceToHost, st);
+  if (e == hipSuccess) e = hipStreamSynchronize(st);
+  float ms = 0.f;
+  if (e == hipSuccess) e = hipEventElapsedTime(&ms, a, b);
+  hipEventDestroy(a);
+  hipEventDestroy(b);
+  hipFreeAsync(sink, st);
+  hipFreeAsync(clk, st);
+  hipStreamSynchronize(st);
+  if (e != hipSuccess) return fail(TOPK_E_HIP, "MFMA probe failed: %s", hipGetErrorString(e));
+  const double flops = (double)blocks * 4 * mfma_rate_iters() * 8 * 32768.0;
+  *tflops = flops / (ms * 1e-3) / 1e12;
+  double sum = 0;
+  for (int i = 0; i < blocks; ++i) sum += (double)h[2 * i] / (double)(h[2 * i + 1] ? h[2 * i + 1] : 1) * 100.0;
+  *clock_mhz = sum / blocks;
+  return TOPK_OK;
+}
+
 int topk_ffn_debug(const void* X, const void* W1, const void* W2, void* out, int64_t N, int64_t d_model, int64_t d_ff,
                    int64_t k, int64_t chunk, int dtype, void* hip_stream, int32_t* idx_out, float* score_out) {
   g_err.clear();

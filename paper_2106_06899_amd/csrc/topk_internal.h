@@ -72,6 +72,7 @@ struct ScanCfg {
   int stride;         // SAMPLE: one key tile in `stride` is sampled
   int R;              // SAMPLE: order statistic kept per lane (3, 6 or 12)
   int groups;         // 32-query groups per wave (2, or 4 when d = 64)
+  int score_only;     // the scan's score-core ablation (no filter, no candidates)
 };
 
 hipError_t launch_init(const PassBufs& b, hipStream_t st);
@@ -83,6 +84,8 @@ hipError_t launch_cand_select(const Problem& pb, const Pass& ps, const PassBufs&
 hipError_t launch_redo(const Problem& pb, const Pass& ps, const PassBufs& b, hipStream_t st);
 hipError_t launch_finalize(const Problem& pb, const Pass& ps, const PassBufs& b, hipStream_t st);
 hipError_t launch_mfma_probe(int32_t* rows, int32_t* cols, hipStream_t st);
+hipError_t launch_mfma_rate(float* sink, uint64_t* clocks, int blocks, hipStream_t st);
+int mfma_rate_iters();
 // Query chunking without top-k (every valid key, softmax): bf16, d in {64, 128}.
 hipError_t launch_dense(const Problem& pb, const Pass& ps, hipStream_t st);
 

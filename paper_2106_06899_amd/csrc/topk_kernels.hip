@@ -688,7 +688,11 @@ template <int G>
 constexpr int scan_queries_per_wg() { return 4 * 32 * G; }
 
 
-template <int D, int R, int G, bool CAUSAL>
+// SCORE_ONLY: the ablation that keeps the sample phase, the K tile pipeline, the MFMAs
+// and each block's maximum, and drops the filter (no staging, no drain, no candidate
+// output; the maxima go to cnt so that the work is kept). It measures what the score
+// core alone costs at the same launch shape.
+template <int D, int R, int G, bool CAUSAL, bool SCORE_ONLY = false>
 __global__ __launch_bounds__(256, D == 64 ? (CAUSAL ? ScanShape<G>::OCC_CAUSAL : ScanShape<G>::OCC) : 2) void k_fused_scan(
     ScanArgs a) {
   static_assert(ScanShape<G>::CAP >= 128, "a ring holds one block's 64 lanes, both halves");
@@ -982,6 +986,7 @@ __global__ __launch_bounds__(256, D == 64 ? (CAUSAL ? ScanShape<G>::OCC_CAUSAL :
   };
   // Main scan: tile by tile. A tile's wait and barrier, and the loads of the next
   // tile into the other buffer, come first; then its 32-key blocks.
+  float core_sink = -INFINITY;
   issue(0, ks0);
   alternate(ntiles, [&](int64_t t, const unsigned char* cur, unsigned char* nxt) {
     __builtin_amdgcn_s_waitcnt(TOPK_WAIT_VM(0));
@@ -1003,9 +1008,16 @@ __global__ __launch_bounds__(256, D == 64 ? (CAUSAL ? ScanShape<G>::OCC_CAUSAL :
       }
       mask_future(x, t, rb);
 #pragma unroll
-      for (int g = 0; g < G; ++g) filter(g, x[g], t, rb);
+      for (int g = 0; g < G; ++g) {
+        if (SCORE_ONLY) core_sink = fmax_(core_sink, block_max(x[g]) - tau[g]);
+        else filter(g, x[g], t, rb);
+      }
     }
   });
+  if (SCORE_ONLY) {
+    if (ok[0]) a.cnt[(wave_row0 + n) * 2 + half] = (int32_t)__float_as_uint(core_sink);
+    return;
+  }
   drain();
 #pragma unroll
   for (int g = 0; g < G; ++g)
@@ -1872,6 +1884,49 @@ __global__ void k_mfma_probe(int32_t* rows, int32_t* cols) {
   }
 }
 
+// ------------------------------------------------------------------ MFMA rate probe
+// A register-only stream of independent v_mfma_f32_32x32x16_bf16 (eight accumulators
+// per wave, no memory traffic in the loop): the sustained MFMA rate of the chip. Wave 0
+// of each workgroup also reads the shader clock counter and the constant 100 MHz
+// counter around the loop, so the host can derive the clock the MFMAs ran at.
+constexpr int PROBE_ITERS = 4096;
+__global__ __launch_bounds__(256) void k_mfma_rate(float* sink, uint64_t* clocks) {
+  const int lane = threadIdx.x & 63;
+  bf16x8 av, bv;
+#pragma unroll
+  for (int e = 0; e < 8; ++e) {
+    av[e] = (__bf16)(1.0f + 0.001f * (lane + e));
+    bv[e] = (__bf16)(1.0f - 0.001f * (lane + e));
+  }
+  f32x16 acc[8];
+#pragma unroll
+  for (int j = 0; j < 8; ++j) acc[j] = (f32x16){};
+  uint64_t t0 = 0, r0 = 0;
+  if (threadIdx.x == 0) {
+    t0 = __builtin_amdgcn_s_memtime();
+    r0 = __builtin_amdgcn_s_memrealtime();
+  }
+  for (int it = 0; it < PROBE_ITERS; ++it) {
+#pragma unroll
+    for (int j = 0; j < 8; ++j) acc[j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(av, bv, acc[j], 0, 0, 0);
+  }
+  float s = 0.f;
+#pragma unroll
+  for (int j = 0; j < 8; ++j) s += acc[j][lane & 15];
+  sink[blockIdx.x * 256 + threadIdx.x] = s;
+  if (threadIdx.x == 0) {
+    const uint64_t t1 = __builtin_amdgcn_s_memtime(), r1 = __builtin_amdgcn_s_memrealtime();
+    clocks[2 * blockIdx.x] = t1 - t0;
+    clocks[2 * blockIdx.x + 1] = r1 - r0;
+  }
+}
+
+hipError_t launch_mfma_rate(float* sink, uint64_t* clocks, int blocks, hipStream_t st) {
+  k_mfma_rate<<<blocks, 256, 0, st>>>(sink, clocks);
+  return hipGetLastError();
+}
+int mfma_rate_iters() { return PROBE_ITERS; }
+
 // ------------------------------------------------------------------ launchers
 static int64_t pass_rows(const Problem& pb, const Pass& ps) { return ps.nc * pb.C; }
 
@@ -1937,6 +1992,11 @@ hipError_t launch_fused_scan(const Problem& pb, const Pass& ps, const PassBufs& 
     else k_fused_scan<D_, 12, G_, C_><<<grid, 256, 0, st>>>(a);               \
   } while (0)
   if (G != 2) return hipErrorInvalidValue;
+  if (cfg.score_only) {  // the ablation exists for the d = 64, k <= 64 sampled non-causal shape only
+    if (pb.d != 64 || causal || cfg.mode != MODE_SAMPLE || cfg.R != 6) return hipErrorInvalidValue;
+    k_fused_scan<64, 6, 2, false, true><<<grid, 256, 0, st>>>(a);
+    return hipGetLastError();
+  }
   if (pb.d == 64 && !causal) TOPK_SCAN(64, 2, false);
   else if (pb.d == 64) TOPK_SCAN(64, 2, true);
   else if (!causal) TOPK_SCAN(128, 2, false);

@@ -205,4 +205,26 @@ def pin_bwd_sampled_equals_full(bo):
     _close(got[2], fullf[2][keys], 1e-12, "sampled dW2")
 
 
+def pin_bwd_magnitudes_bound_the_gradients(bo):
+    """The sums of absolute terms bound the gradients elementwise (triangle inequality),
+    equal them where every term has one sign (d_V with non-negative d_out: softmax
+    weights are non-negative), and the sampled form returns the same sums."""
+    rng = _rng(108)
+    L, d, k = 30, 4, 5
+    Q, K, V = (rng.standard_normal((1, 1, L, d)) for _ in range(3))
+    G = np.abs(rng.standard_normal((1, 1, L, d)))
+    r = fwd.oracle_attn(Q, K, V, k, 0, True, 0.5)
+    grads, mags = bo.oracle_attn_backward(Q, K, V, r["idx"], G, 0.5, chunk=7, magnitudes=True)
+    for gr, mg, n in zip(grads, mags, ("dQ", "dK", "dV")):
+        assert np.all(np.abs(gr) <= mg + 1e-12), f"{n}: |gradient| above its magnitude"
+    _close(grads[2], mags[2], 1e-12, "dV with d_out >= 0 equals its magnitude")
+    assert np.any(mags[0] > np.abs(grads[0]) + 1e-6), "dQ terms of mixed sign must show in the magnitude"
+    rows, keys = np.array([2, 17, 29]), np.array([0, 5, 28])
+    sg, sm = bo.sampled_backward(Q[0, 0], K[0, 0], V[0, 0], r["idx"][0, 0], G[0, 0], rows, keys, "softmax", 0.5,
+                                 magnitudes=True)
+    _close(sm[0], mags[0][0, 0][rows], 1e-12, "sampled dQ magnitude")
+    _close(sm[1], mags[1][0, 0][keys], 1e-12, "sampled dK magnitude")
+    _close(sm[2], mags[2][0, 0][keys], 1e-12, "sampled dV magnitude")
+
+
 ALL_PINS = [v for kname, v in sorted(globals().items()) if kname.startswith("pin_")]

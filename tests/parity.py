@@ -13,6 +13,7 @@ from oracle import topk_oracle as o
 from paper_2106_06899_amd import workloads as wl
 
 RTOL = {wl.F32: 1e-5, wl.BF16: 2e-2}
+GRAD_KAPPA = {wl.F32: 1.0, wl.BF16: 1e-3}
 
 
 def to_dev(t: wl.Tensor, device="cuda"):
@@ -130,3 +131,26 @@ def grad_out(shape, dtype, seed) -> wl.Tensor:
         bits = wl.f32_to_bf16_bits(g)
         return wl.Tensor(wl.bf16_bits_to_f32(bits), bits, wl.BF16)
     return wl.Tensor(g, None, wl.F32)
+
+
+def check_grad_rows(name, got, ref, mag, dtype):
+    """Backward acceptance rule, per row (per key for d_K, d_V): max_t |g - r| <= rtol *
+    max(max_t |r|, kappa * max_t a), where a is the row's sum of absolute terms from the
+    oracle (the scale of rounding in a sum of terms of mixed signs), rtol = 2e-2 (bf16)
+    / 1e-5 (fp32), kappa = 1e-3 (bf16) / 1 (fp32); plus the tensor-wide rule (error
+    over the largest reference entry). Returns the largest per-row ratio. got: GPU
+    gradient (tensor or array); ref, mag: the oracle's gradient and magnitudes."""
+    g = np.asarray(got.float().cpu().numpy() if hasattr(got, "cpu") else got, dtype=np.float64)
+    g = g.reshape(-1, g.shape[-1])
+    r = ref.reshape(-1, ref.shape[-1])
+    a = mag.reshape(-1, mag.shape[-1])
+    rtol = RTOL[dtype]
+    err = np.abs(g - r).max(axis=1)
+    own = np.maximum(np.abs(r).max(axis=1), GRAD_KAPPA[dtype] * a.max(axis=1))
+    zero = own == 0
+    assert not np.any(err[zero]), f"{name}: non-zero gradient where every term is zero"
+    ratio = np.where(zero, 0.0, err / np.where(zero, 1.0, own))
+    assert np.all(ratio <= rtol), f"{name}: error {ratio.max():.3e} > {rtol} at row {int(np.argmax(ratio))}"
+    whole = err.max() / max(float(np.abs(r).max()), 1e-30)
+    assert whole <= rtol, f"{name}: tensor-wide error {whole:.3e} > {rtol}"
+    return float(ratio.max())

@@ -3,8 +3,12 @@
 The forward runs on the GPU in debug mode to produce its cache (selected keys and
 their raw scores); the backward then runs through the C ABI, and the oracle computes
 the gradients for the same selected keys in fp64 (its scores recomputed exactly).
-Outputs are compared per row (per key for d_K, d_V) in the max norm, relative to
-the largest reference entry of the tensor: 2e-2 for bf16, 1e-5 for fp32.
+Outputs are compared per row (per key for d_K, d_V) in the max norm, each row against
+its own reference: max_t |g - r| <= rtol * max(max_t |r|, kappa * max_t a), where a is
+the row's sum of absolute terms (the scale of rounding in a sum of terms of mixed
+signs), rtol = 2e-2 (bf16) / 1e-5 (fp32) and kappa = 1e-3 (bf16) / 1 (fp32). A rarely
+selected key with small gradients is thus held to its own size, not to the tensor's
+largest entry; the tensor-wide rule is checked as well.
 """
 import math
 
@@ -19,7 +23,8 @@ from tests import parity
 
 pytestmark = pytest.mark.gpu
 
-RTOL = {wl.F32: 1e-5, wl.BF16: 2e-2}
+RTOL = parity.RTOL
+check_rows = parity.check_grad_rows
 
 
 def _say(*a):
@@ -35,16 +40,6 @@ def _gpu():
 
 def _grad_out(shape, dtype, seed):
     return parity.grad_out(shape, dtype, seed)
-
-
-def _check(name, got, ref, dtype):
-    g = got.float().cpu().numpy().astype(np.float64).reshape(-1, got.shape[-1])
-    r = ref.reshape(-1, ref.shape[-1])
-    scale = max(float(np.abs(r).max()), 1e-30)
-    err = np.abs(g - r).max(axis=1) / scale
-    rtol = RTOL[dtype]
-    assert np.all(err <= rtol), f"{name}: error {err.max():.3e} > {rtol} at row {int(np.argmax(err))}"
-    return float(err.max())
 
 
 ATTN_CASES = {
@@ -68,9 +63,9 @@ def test_attn_backward_parity(name):
     g = _grad_out((w.B, w.H, w.Lq, w.d), w.dtype, 77)
     dq, dk, dv = tk.attn_backward(q, k, v, idx, dots, parity.to_dev(g), w.scale)
     torch.cuda.synchronize()
-    rq, rk, rv = bo.oracle_attn_backward(x["Q"].values, x["K"].values, x["V"].values, idx.cpu().numpy(),
-                                         g.values, w.scale, chunk=w.chunk)
-    errs = [_check(n, a, b, w.dtype) for n, a, b in (("d_Q", dq, rq), ("d_K", dk, rk), ("d_V", dv, rv))]
+    ref, mag = bo.oracle_attn_backward(x["Q"].values, x["K"].values, x["V"].values, idx.cpu().numpy(),
+                                       g.values, w.scale, chunk=w.chunk, magnitudes=True)
+    errs = [check_rows(n, a, b, m, w.dtype) for n, a, b, m in zip(("d_Q", "d_K", "d_V"), (dq, dk, dv), ref, mag)]
     _say(name, "ok", dict(zip(("dQ", "dK", "dV"), errs)))
     if w.k == 1:  # a lone survivor's softmax weight is 1 whatever its score: no score gradient
         assert torch.count_nonzero(dq) == 0 and torch.count_nonzero(dk) == 0
@@ -93,9 +88,10 @@ def test_ffn_backward_parity(name):
     g = _grad_out((w.N, w.d_model), w.dtype, 78)
     dx, dw1, dw2 = tk.ffn_backward(a, b1, b2, idx, dots, parity.to_dev(g))
     torch.cuda.synchronize()
-    rx, r1, r2 = bo.oracle_ffn_backward(x["X"].values, x["W1"].values, x["W2"].values, idx.cpu().numpy(), g.values,
-                                        chunk=w.chunk)
-    errs = [_check(n, a_, b_, w.dtype) for n, a_, b_ in (("d_X", dx, rx), ("d_W1", dw1, r1), ("d_W2", dw2, r2))]
+    ref, mag = bo.oracle_ffn_backward(x["X"].values, x["W1"].values, x["W2"].values, idx.cpu().numpy(), g.values,
+                                      chunk=w.chunk, magnitudes=True)
+    errs = [check_rows(n, a_, b_, m_, w.dtype) for n, a_, b_, m_ in zip(("d_X", "d_W1", "d_W2"), (dx, dw1, dw2), ref,
+                                                                        mag)]
     _say(name, "ok", dict(zip(("dX", "dW1", "dW2"), errs)))
 
 
@@ -189,12 +185,13 @@ def test_backward_list_edges(name):
     ix = idx.cpu().numpy()
     if kind == "attn":
         g = _grad_out((w.B, w.H, w.Lq, w.d), w.dtype, 81)
-        ref = bo.oracle_attn_backward(x["Q"].values, x["K"].values, x["V"].values, ix, g.values, w.scale,
-                                      chunk=min(w.chunk, 8))
+        ref, mag = bo.oracle_attn_backward(x["Q"].values, x["K"].values, x["V"].values, ix, g.values, w.scale,
+                                           chunk=min(w.chunk, 8), magnitudes=True)
         names = ("d_Q", "d_K", "d_V")
     else:
         g = _grad_out((w.N, w.d_model), w.dtype, 81)
-        ref = bo.oracle_ffn_backward(x["X"].values, x["W1"].values, x["W2"].values, ix, g.values, chunk=w.chunk)
+        ref, mag = bo.oracle_ffn_backward(x["X"].values, x["W1"].values, x["W2"].values, ix, g.values,
+                                          chunk=w.chunk, magnitudes=True)
         names = ("d_X", "d_W1", "d_W2")
-    errs = [_check(n, a, b, w.dtype) for n, a, b in zip(names, got, ref)]
+    errs = [check_rows(n, a, b, m, w.dtype) for n, a, b, m in zip(names, got, ref, mag)]
     _say(name, "ok", dict(zip(names, errs)))

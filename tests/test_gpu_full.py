@@ -28,6 +28,11 @@ def test_attn_full_size(name):
     rep = {}
     parity.check_attn(w, x, out, idx, rows=rows, report=rep)
     _say(name, "sampled rows ok", rep)
+    # one whole head (every row of b = 0, h = H - 1) against the oracle as well
+    head = np.stack([np.zeros(w.Lq, np.int64), np.full(w.Lq, w.H - 1), np.arange(w.Lq)], -1)
+    rep_head = {}
+    parity.check_attn(w, x, out, idx, rows=head, report=rep_head)
+    _say(name, f"whole head {w.H - 1} ok", rep_head)
     # every row, not only the sampled ones, must carry exactly k_eff distinct valid indices
     g = idx.cpu().numpy()
     k_eff = np.minimum(w.k, np.arange(w.Lq) + 1) if w.causal else np.full(w.Lq, w.k)
@@ -72,7 +77,8 @@ def test_ffn_full_size():
     x = wl.make_inputs(w)
     out, idx, sc = parity.run_ffn(w, x)
     rng = np.random.Generator(np.random.PCG64(w.seed))
-    rows = np.unique(np.concatenate([[0, 1, w.chunk - 1, w.chunk, w.N - 1], rng.integers(0, w.N, 59)]))
+    rows = np.unique(np.concatenate([[0, 1, w.chunk - 1, w.chunk, w.N - 1], rng.integers(0, w.N, 1100)]))
+    assert rows.size >= 1024
     rep = {}
     parity.check_ffn(w, x, out, idx, rows=rows, report=rep)
     _say("c5", "sampled rows ok", rep)
@@ -81,10 +87,34 @@ def test_ffn_full_size():
     assert torch.isfinite(out.float()).all()
 
 
+# ---------------------------------------------------------------- the paper's feed-forward shape
+def _paper_ff_inputs(d_ff):
+    """Inputs of the feed-forward benchmark (2^18 tokens = batch 512 x length 512,
+    d_model 768) by the c5 recipe: X ~ N(0, 1), W1, W2 ~ N(0, 0.02^2), bf16."""
+    w = wl.WORKLOADS["c5"].scaled(N=1 << 18, d_model=768, d_ff=d_ff, k=512, chunk=1 << 14)
+    return w, wl.make_inputs(w)
+
+
+@pytest.mark.parametrize("d_ff", [2048, 16384, 65536])
+def test_ffn_paper_shape(d_ff):
+    """The feed-forward benchmark of Section 3 (2^18 queries, d_model 768, k 512, token
+    chunk 2^14) at three d_ff of its sweep: sampled rows against the oracle, every row
+    with k distinct valid indices."""
+    w, x = _paper_ff_inputs(d_ff)
+    _say("paper FF", f"N {w.N} d_model {w.d_model} d_ff {d_ff} k {w.k} chunk {w.chunk}")
+    out, idx, sc = parity.run_ffn(w, x)
+    rng = np.random.Generator(np.random.PCG64(d_ff))
+    C = w.chunk
+    rows = np.unique(np.concatenate([[0, C - 1, C, w.N - C, w.N - 1], rng.integers(0, w.N, 250)]))
+    rep = {"fallback_rows": tk.last_fallback_rows()}
+    parity.check_ffn(w, x, out, idx, rows=rows, report=rep)
+    _say("paper FF", d_ff, "sampled rows ok", rep)
+    g = idx.cpu().numpy()
+    assert np.all((g >= 0).sum(-1) == w.k) and np.all(g < d_ff)
+    assert torch.isfinite(out.float()).all()
+
+
 # ---------------------------------------------------------------- backward, full size
-BWD_RTOL = {wl.F32: 1e-5, wl.BF16: 2e-2}
-
-
 def _sample_keys(idx_head, Lk, rng, n):
     """Keys 0 and Lk - 1, the three most selected keys, and n random keys."""
     counts = np.bincount(idx_head[idx_head >= 0].ravel(), minlength=Lk)
@@ -92,11 +122,9 @@ def _sample_keys(idx_head, Lk, rng, n):
     return np.unique(np.concatenate([[0, Lk - 1], hot, rng.integers(0, Lk, n)]))
 
 
-def _check_sample(name, got, ref, rtol):
-    scale = max(float(np.abs(ref).max()), 1e-30)
-    err = np.abs(got.astype(np.float64) - ref).max(axis=1) / scale
-    assert np.all(err <= rtol), f"{name}: error {err.max():.3e} > {rtol} at sample {int(np.argmax(err))}"
-    return float(err.max())
+def _check_sample(name, got, ref, mag, dtype):
+    """Each sampled row / key against its own reference (the rule of test_gpu_backward)."""
+    return parity.check_grad_rows(name, got, ref, mag, dtype)
 
 
 def _unselected_are_zero(idx, dk, dv, Lk):
@@ -126,15 +154,16 @@ def test_attn_backward_full_size(name):
     rng = np.random.Generator(np.random.PCG64(w.seed + 1))
     heads = sorted({(0, 0), (w.B - 1, w.H - 1), (int(rng.integers(w.B)), int(rng.integers(w.H)))})
     C = w.chunk or w.Lq
-    rtol = BWD_RTOL[w.dtype]
     for b, h in heads:
         rows = np.unique(np.concatenate([[0, 1, C - 1, C, min(w.k - 1, w.Lq - 1), w.Lq - 1],
                                          rng.integers(0, w.Lq, 40)]))
         keys = _sample_keys(ix[b, h], w.Lk, rng, 24)
-        rq, rk, rv = bo.sampled_backward(x["Q"].values[b, h], x["K"].values[b, h], x["V"].values[b, h], ix[b, h],
-                                         g.values[b, h], rows, keys, "softmax", w.scale)
-        errs = (_check_sample("d_Q", dq[b, h][rows], rq, rtol), _check_sample("d_K", dk[b, h][keys], rk, rtol),
-                _check_sample("d_V", dv[b, h][keys], rv, rtol))
+        (rq, rk, rv), (aq, ak, av) = bo.sampled_backward(x["Q"].values[b, h], x["K"].values[b, h],
+                                                         x["V"].values[b, h], ix[b, h], g.values[b, h], rows, keys,
+                                                         "softmax", w.scale, magnitudes=True)
+        errs = (_check_sample("d_Q", dq[b, h][rows], rq, aq, w.dtype),
+                _check_sample("d_K", dk[b, h][keys], rk, ak, w.dtype),
+                _check_sample("d_V", dv[b, h][keys], rv, av, w.dtype))
         cold = _unselected_are_zero(ix[b, h], dk[b, h], dv[b, h], w.Lk)
         _say(name, f"head ({b},{h}) rows {len(rows)} keys {len(keys)} unselected keys {cold} errors", errs)
 
@@ -156,9 +185,9 @@ def test_ffn_backward_full_size():
     rng = np.random.Generator(np.random.PCG64(w.seed + 1))
     rows = np.unique(np.concatenate([[0, 1, w.chunk - 1, w.chunk, w.N - 1], rng.integers(0, w.N, 40)]))
     keys = _sample_keys(ix, w.d_ff, rng, 16)
-    rx, r1, r2 = bo.sampled_backward(x["X"].values, x["W1"].values, x["W2"].values, ix, g.values, rows, keys, "relu")
-    rtol = BWD_RTOL[w.dtype]
-    errs = (_check_sample("d_X", dx[rows], rx, rtol), _check_sample("d_W1", dw1[keys], r1, rtol),
-            _check_sample("d_W2", dw2[keys], r2, rtol))
+    (rx, r1, r2), (ax, a1, a2) = bo.sampled_backward(x["X"].values, x["W1"].values, x["W2"].values, ix, g.values,
+                                                     rows, keys, "relu", magnitudes=True)
+    errs = (_check_sample("d_X", dx[rows], rx, ax, w.dtype), _check_sample("d_W1", dw1[keys], r1, a1, w.dtype),
+            _check_sample("d_W2", dw2[keys], r2, a2, w.dtype))
     cold = _unselected_are_zero(ix, dw1, dw2, w.d_ff)
     _say("c5", f"rows {len(rows)} keys {len(keys)} unselected keys {cold} errors", errs)

@@ -161,7 +161,8 @@ def test_feed_forward_layer_parity():
           "W2": wl.Tensor(W2.astype(np.float32), None, dt)}
     parity.check_ffn(w, xs, out, idx)
     assert torch.equal(Y.detach().reshape(-1, dm), out)
-    ref = bo.oracle_ffn_backward(Xv.reshape(-1, dm), W1, W2, idx.cpu().numpy(), Gv.reshape(-1, dm), chunk=C)
+    ref, mag = bo.oracle_ffn_backward(Xv.reshape(-1, dm), W1, W2, idx.cpu().numpy(), Gv.reshape(-1, dm), chunk=C,
+                                      magnitudes=True)
     got = (X.grad.reshape(-1, dm), layer.w1.grad, layer.w2.grad)
-    errs = {n: _rows_close(n, a.float().cpu().numpy(), b, 2e-2) for n, a, b in zip(("dX", "dW1", "dW2"), got, ref)}
+    errs = {n: parity.check_grad_rows(n, a, b, m, wl.BF16) for n, a, b, m in zip(("dX", "dW1", "dW2"), got, ref, mag)}
     _say("ffn layer ok", errs)

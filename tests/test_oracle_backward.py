@@ -54,21 +54,23 @@ def _mut_scores_off_by_one_key(orig):
 
 def _mut_dk_dv_swapped(orig):
     def f(*a, **kw):
-        dq, dk, dv = orig(*a, **kw)
-        return dq, dv, dk
+        r = orig(*a, **kw)
+        (dq, dk, dv), m = r if len(r) == 2 else (r, None)
+        return ((dq, dv, dk), m) if m is not None else (dq, dv, dk)
     return f
 
 
 def _mut_dq_sign(orig):
     def f(*a, **kw):
-        dq, dk, dv = orig(*a, **kw)
-        return -dq, dk, dv
+        r = orig(*a, **kw)
+        (dq, dk, dv), m = r if len(r) == 2 else (r, None)
+        return ((-dq, dk, dv), m) if m is not None else (-dq, dk, dv)
     return f
 
 
 def _mut_dv_unweighted(orig):
     # d_V as the plain sum of the selecting rows' output gradients (weights dropped)
-    def f(Qh, Kh, Vh, idx, G, activation, scale=1.0, chunk=None):
+    def f(Qh, Kh, Vh, idx, G, activation, scale=1.0, chunk=None, magnitudes=False):
         dq, dk, dv = orig(Qh, Kh, Vh, idx, G, activation, scale, chunk)
         dv = np.zeros_like(dv)
         rr, mm = np.nonzero(idx >= 0)
