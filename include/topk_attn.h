@@ -317,6 +317,16 @@ int64_t topk_last_fallback_rows(void);
 int topk_selftest_mfma_layout(int32_t* rows_out, int32_t* cols_out, void* hip_stream);
 
 /*
+ * Debug hook. The library also builds as libtopk_check.so (compiled with
+ * TOPK_CHECK_INDICES): there every forward call waits for its stream and returns
+ * TOPK_E_HIP for an error its kernels raised while running, and the finalize counts
+ * selected indices outside the value matrix (which it clamps in every build, so that
+ * no read leaves the matrix). This returns that count since the last call and resets
+ * it (waits for the device), or -1 in the normal build.
+ */
+int64_t topk_debug_bad_indices(void);
+
+/*
  * Measurement hook: run only the fused path's score kernel (its sampled threshold
  * phase and scan) of a topk_attn call on bf16 Q, K [B, H, L, 64] with 32 < k <= 64,
  * as many passes as the call would run; with score_only = 1 the scan's score-core

@@ -340,6 +340,13 @@ int run(Problem whole, hipStream_t st, bool report, void* fixed_ws = nullptr, si
   if (report) g_fallback_rows = e == hipSuccess ? fallback : -1;
   if (own) hipFreeAsync(ws, st);
   if (e != hipSuccess) return fail(TOPK_E_HIP, "kernel launch failed: %s", hipGetErrorString(e));
+#ifdef TOPK_CHECK_INDICES
+  // checked builds wait for the call, so that an error the kernels raise while running
+  // is returned by this call (and topk_last_error) instead of a later one
+  e = hipStreamSynchronize(st);
+  if (e == hipSuccess) e = hipGetLastError();
+  if (e != hipSuccess) return fail(TOPK_E_HIP, "the call's kernels failed: %s", hipGetErrorString(e));
+#endif
   return TOPK_OK;
 }
 
@@ -826,6 +833,8 @@ int topk_set_backward_lists(int mode) {
 }
 
 const char* topk_last_error(void) { return g_err.c_str(); }
+
+int64_t topk_debug_bad_indices(void) { return read_bad_indices(); }
 
 int64_t topk_last_fallback_rows(void) { return g_fallback_rows; }
 

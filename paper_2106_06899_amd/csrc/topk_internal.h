@@ -85,6 +85,9 @@ hipError_t launch_redo(const Problem& pb, const Pass& ps, const PassBufs& b, hip
 hipError_t launch_finalize(const Problem& pb, const Pass& ps, const PassBufs& b, hipStream_t st);
 hipError_t launch_mfma_probe(int32_t* rows, int32_t* cols, hipStream_t st);
 hipError_t launch_mfma_rate(float* sink, uint64_t* clocks, int blocks, hipStream_t st);
+// checked builds (TOPK_CHECK_INDICES): out-of-range selected indices seen by the
+// finalize since the last read (the count is reset), -1 in other builds
+int64_t read_bad_indices();
 int mfma_rate_iters();
 // Query chunking without top-k (every valid key, softmax): bf16, d in {64, 128}.
 hipError_t launch_dense(const Problem& pb, const Pass& ps, hipStream_t st);

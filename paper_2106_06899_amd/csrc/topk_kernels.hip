@@ -1731,6 +1731,13 @@ __device__ __forceinline__ void sort_by_key_index(float* w, uint32_t* jj, int n)
   __syncthreads();
 }
 
+#ifdef TOPK_CHECK_INDICES
+// Checked builds count the selected indices that lie outside the value matrix (the
+// finalize still clamps them, so that no read leaves it); read with
+// topk_debug_bad_indices.
+__device__ unsigned long long g_bad_indices = 0;
+#endif
+
 template <typename T, int NSLICES>
 __device__ __forceinline__ void finalize_row(const Problem& pb, const Pass& ps, const uint64_t* sel, int64_t p,
                                              float* w, uint32_t* jj, int slice) {
@@ -1752,6 +1759,9 @@ __device__ __forceinline__ void finalize_row(const Problem& pb, const Pass& ps, 
       j = (int32_t)key_index(key);
       w[t] = s;
       jj[t] = (uint32_t)j < jmax ? (uint32_t)j : jmax;  // keeps a bad selection from reading out of bounds
+#ifdef TOPK_CHECK_INDICES
+      if ((uint32_t)j > jmax) atomicAdd(&g_bad_indices, 1ull);
+#endif
     }
     if (slice == 0) {
       if (pb.idx_out) pb.idx_out[grow * pb.k + t] = j;
@@ -2048,6 +2058,17 @@ hipError_t launch_finalize(const Problem& pb, const Pass& ps, const PassBufs& b,
   else TOPK_FINALIZE(float);
 #undef TOPK_FINALIZE
   return hipGetLastError();
+}
+
+int64_t read_bad_indices() {
+#ifdef TOPK_CHECK_INDICES
+  unsigned long long h = 0, zero = 0;
+  if (hipMemcpyFromSymbol(&h, HIP_SYMBOL(g_bad_indices), sizeof(h)) != hipSuccess) return -2;
+  if (hipMemcpyToSymbol(HIP_SYMBOL(g_bad_indices), &zero, sizeof(zero)) != hipSuccess) return -2;
+  return (int64_t)h;
+#else
+  return -1;
+#endif
 }
 
 hipError_t launch_mfma_probe(int32_t* rows, int32_t* cols, hipStream_t st) {
