@@ -407,6 +407,9 @@ __global__ __launch_bounds__(256, 2) void k_tile_scores_mfma(Problem pb, Pass ps
           for (int v = 0; v < 16; ++v)
             m |= (kb + 8 * (v >> 2) + (v & 3) < nv && acc[a][b][v] >= ts ? 1u : 0u) << v;
         }
+        // rows past the chunk or the sequence hold the tile's first row's scores (and a
+        // threshold of +inf, which a +inf score would still meet): they append nothing
+        m = okr ? m : 0u;
         pass[a][b] = m;
         c += (uint32_t)__builtin_popcount(m);
       }
