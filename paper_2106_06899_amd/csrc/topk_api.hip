@@ -107,6 +107,24 @@ int validate_shape(int64_t BH_a, int64_t BH_b, int64_t Lq, int64_t Lk, int64_t d
 // ---------------------------------------------------------------- planning
 int order_stat_for(int64_t k) { return k <= 32 ? 3 : (k <= 64 ? 6 : 12); }
 
+// The fused scan's per-query threshold, from the 16-key block maxima of a strided
+// sample of key tiles. d = 64, k <= 64: a 1-in-8 sample, each half-wave keeps its 11
+// largest, and the threshold is the J-th largest of both lists together (J = 13 for
+// k <= 32, 20 for k <= 64: about 2.8 k candidates per row on Gaussian-like scores,
+// about one row in 20000 below k). Otherwise (d = 128, whose registers hold fewer
+// sorted maxima, or k > 64): a 1-in-16 sample and the smaller of the two half-waves'
+// R-th largest, R = order_stat_for(k) (about 4 k candidates).
+ScanCfg sample_rule(int64_t k, int64_t d, int groups) {
+  if (d == 64 && k <= 32) return {MODE_SAMPLE, 8, 11, groups, 0, 13};
+  if (d == 64 && k <= 64) return {MODE_SAMPLE, 8, 11, groups, 0, 20};
+  return {MODE_SAMPLE, 16, order_stat_for(k), groups, 0, 0};
+}
+// Valid keys a row needs for its threshold: twice the rank taken, in sampled blocks of
+// the pool it is taken from (a sampled 64-key tile gives each half-wave two blocks).
+int64_t sample_rows_needed(const ScanCfg& sc) {
+  return sc.union_rank ? (int64_t)2 * sc.union_rank * 64 * sc.stride / 4 : (int64_t)2 * sc.R * 64 * sc.stride / 2;
+}
+
 // Filtered chunk-tile path: bf16 MFMA tiles (d % 32 == 0) whose rows are long
 // enough for a sampled threshold and at most 4096 samples, k <= 512 (its
 // candidates, about 16 R per row, stay within the 1024 the select holds for
@@ -120,7 +138,7 @@ int64_t caph_for(const Problem& pb, int path) { return path == PATH_FILTER && pb
 
 void choose_path(const Problem& pb, Plan* pl) {
   pl->path = PATH_TILE;
-  pl->scan = {MODE_ALL, 16, 8, 2};
+  pl->scan = {MODE_ALL, 16, 8, 2, 0, 0};
   if (pb.tile_only) {
     if (filter_ok(pb)) pl->path = PATH_FILTER;
     return;
@@ -139,18 +157,18 @@ void choose_path(const Problem& pb, Plan* pl) {
   }
   if (pb.Lk <= 2 * FUSED_CAPH) {  // every key fits the candidate buffers
     pl->path = PATH_FUSED;
-    pl->scan = {MODE_ALL, 16, order_stat_for(pb.k), groups};
+    pl->scan = sample_rule(pb.k, pb.d, groups);  // its kernel instantiation; no sample is taken
+    pl->scan.mode = MODE_ALL;
     return;
   }
-  // Threshold mode: the R-th largest 16-key block maximum of a 1-in-16 tile sample,
-  // taken on each half-wave, gives about 4k candidates per row; each lane needs at
-  // least 2R sampled blocks of 16 keys.
-  const int R = order_stat_for(pb.k);
+  // Threshold mode, see sample_rule: needs at least 2R sampled 16-key blocks in the
+  // pool the order statistic is taken from.
+  const ScanCfg sc = sample_rule(pb.k, pb.d, groups);
   const int64_t kt = 64;  // key tile of the scan kernel
-  const int64_t sampled_tiles = ((pb.Lk + kt - 1) / kt + 15) / 16;
-  if (sampled_tiles * (kt / 32) >= 2 * R) {
+  const int64_t sampled_tiles = ((pb.Lk + kt - 1) / kt + sc.stride - 1) / sc.stride;
+  if (sampled_tiles * (sc.union_rank ? 4 : 2) >= 2 * (sc.union_rank ? sc.union_rank : sc.R)) {
     pl->path = PATH_FUSED;
-    pl->scan = {MODE_SAMPLE, 16, R, groups};
+    pl->scan = sc;
   } else if (filter_ok(pb)) {
     pl->path = PATH_FILTER;
   }
@@ -221,16 +239,17 @@ PassBufs carve(const Problem& pb, const Plan& pl, char* ws) {
   return b;
 }
 
-// Causal rows on the fused path: a row needs at least 2R valid sampled blocks per
-// half-wave for its 1-in-16 threshold sample, i.e. i + 1 >= 1024 R valid keys. The
-// first 1024 R rows of every head therefore run on the chunk-tile path, the rest
-// fused. Each row's path, and so its result, does not depend on the chunk size.
+// Causal rows on the fused path: a row needs twice the rank its threshold takes in
+// valid sampled blocks (sample_rows_needed valid keys: 3328, 5120 and 12288 for k <=
+// 32, 64 and 128 at d = 64; 3072, 6144 and 12288 at d = 128). The first such rows of every head therefore run on the
+// chunk-tile path, the rest fused. Each row's path, and so its result, does not
+// depend on the chunk size.
 int split_rows(const Problem& pb, Problem* parts) {
   parts[0] = pb;
   Plan pl;
   choose_path(pb, &pl);
   if (!pb.causal || pl.path != PATH_FUSED || pl.scan.mode != MODE_SAMPLE) return 1;
-  const int64_t T = 1024 * (int64_t)pl.scan.R;
+  const int64_t T = sample_rows_needed(pl.scan);
   if (T <= pb.q0) return 1;
   parts[0].q1 = pb.q1 < T ? pb.q1 : T;
   parts[0].tile_only = 1;
@@ -646,7 +665,7 @@ int topk_scan_ablation(const void* Q, const void* K, int64_t B, int64_t H, int64
   if (rc) return rc;
   Plan pl;
   choose_path(pb, &pl);
-  if (pl.path != PATH_FUSED || pl.scan.mode != MODE_SAMPLE || pb.d != 64 || pl.scan.R != 6)
+  if (pl.path != PATH_FUSED || pl.scan.mode != MODE_SAMPLE || pb.d != 64 || pl.scan.union_rank != 20)
     return fail(TOPK_E_UNSUPPORTED, "the scan ablation runs on the sampled fused path with d = 64, 32 < k <= 64");
   pl.scan.score_only = score_only ? 1 : 0;
   plan_sizes(pb, &pl, g_budget.load(std::memory_order_relaxed));

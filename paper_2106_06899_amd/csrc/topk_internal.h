@@ -70,9 +70,11 @@ struct PassBufs {
 struct ScanCfg {
   int mode;           // ScanMode
   int stride;         // SAMPLE: one key tile in `stride` is sampled
-  int R;              // SAMPLE: order statistic kept per lane (3, 6 or 12)
-  int groups;         // 32-query groups per wave (2, or 4 when d = 64)
+  int R;              // SAMPLE: block maxima kept per lane, sorted (11 or 12)
+  int groups;         // 32-query groups per wave (2)
   int score_only;     // the scan's score-core ablation (no filter, no candidates)
+  int union_rank;     // SAMPLE: J > 0: the threshold is the J-th largest of both half-waves'
+                      // lists together (13 or 20); 0: the smaller of their R-th
 };
 
 hipError_t launch_init(const PassBufs& b, hipStream_t st);

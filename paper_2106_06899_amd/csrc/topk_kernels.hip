@@ -695,7 +695,7 @@ constexpr int scan_queries_per_wg() { return 4 * 32 * G; }
 // and each block's maximum, and drops the filter (no staging, no drain, no candidate
 // output; the maxima go to cnt so that the work is kept). It measures what the score
 // core alone costs at the same launch shape.
-template <int D, int R, int G, bool CAUSAL, bool SCORE_ONLY = false>
+template <int D, int R, int G, bool CAUSAL, bool SCORE_ONLY = false, int J = 0>
 __global__ __launch_bounds__(256, D == 64 ? (CAUSAL ? ScanShape<G>::OCC_CAUSAL : ScanShape<G>::OCC) : 2) void k_fused_scan(
     ScanArgs a) {
   static_assert(ScanShape<G>::CAP >= 128, "a ring holds one block's 64 lanes, both halves");
@@ -880,8 +880,28 @@ __global__ __launch_bounds__(256, D == 64 ? (CAUSAL ? ScanShape<G>::OCC_CAUSAL :
     });
 #pragma unroll
     for (int g = 0; g < G; ++g) {
-      const float mine = top[g][R - 1];
-      tau[g] = fminf(mine, __shfl_xor(mine, 32, 64));
+      if (J > 0) {
+        // the J-th largest of the two half-waves' lists together (each holds its R
+        // largest block maxima, J <= 2R): the largest, over p + q = J with p, q <= R,
+        // of min(p-th of this lane's list, q-th of the partner's), the 0-th entry
+        // standing for +inf. Where more than R of the J largest of all sampled blocks
+        // fall in one half-wave this is below the exact J-th: still a lower bound.
+        static_assert(J <= 2 * R, "the J-th needs R >= J / 2 per list");
+        float other[R];
+#pragma unroll
+        for (int r = 0; r < R; ++r) other[r] = __shfl_xor(top[g][r], 32, 64);
+        float t = -INFINITY;
+#pragma unroll
+        for (int p = (J > R ? J - R : 0); p <= (J < R ? J : R); ++p) {
+          const float ap = p > 0 ? top[g][p > 0 ? p - 1 : 0] : INFINITY;
+          const float bq = J - p > 0 ? other[J - p > 0 ? J - p - 1 : 0] : INFINITY;
+          t = fmaxf(t, fminf(ap, bq));
+        }
+        tau[g] = t;
+      } else {
+        const float mine = top[g][R - 1];
+        tau[g] = fminf(mine, __shfl_xor(mine, 32, 64));
+      }
     }
   }
 #pragma unroll
@@ -952,17 +972,18 @@ __global__ __launch_bounds__(256, D == 64 ? (CAUSAL ? ScanShape<G>::OCC_CAUSAL :
       hB = fmax_(hB, acc[8 + v]);
     }
     const bool dA = hA > tau[g], dB = hB > tau[g];
-    const bool dirty = dA || dB;
-    const uint64_t bal = __ballot(dirty);
+    // the ballots straight from the comparisons (the compare masks themselves), not
+    // from a combined predicate that the compiler would turn back into a lane mask
+    const uint64_t bA = __builtin_amdgcn_ballot_w64(hA > tau[g]), bB = __builtin_amdgcn_ballot_w64(hB > tau[g]);
+    const uint64_t bal = bA | bB;
     if (bal == 0) return;
-    const bool both = dA && dB;
-    const uint64_t bal2 = __ballot(both);
+    const uint64_t bal2 = bA & bB;
     const int n1 = __popcll(bal), n2 = __popcll(bal2);
     if (rtail - rhead + n1 + n2 > STAGE_CAP) drain();
     const uint32_t mb = (uint32_t)((t * KT + rb * 32) / 32) << 8 | (uint32_t)(g << 6) | (uint32_t)lane;
-    if (dirty) {
-      const int slot = (rtail + (int)__builtin_amdgcn_mbcnt_hi((uint32_t)(bal >> 32),
-                                                              __builtin_amdgcn_mbcnt_lo((uint32_t)bal, 0u))) &
+    if (dA || dB) {
+      const int slot = (int)__builtin_amdgcn_mbcnt_hi((uint32_t)(bal >> 32),
+                                                      __builtin_amdgcn_mbcnt_lo((uint32_t)bal, (uint32_t)rtail)) &
                        (STAGE_CAP - 1);
       // the half to stage, selected in registers (a bitwise mux per score, so the
       // compiler does not turn it into an indexed read of the accumulator)
@@ -976,9 +997,9 @@ __global__ __launch_bounds__(256, D == 64 ? (CAUSAL ? ScanShape<G>::OCC_CAUSAL :
       stage_meta[wave][slot] = mb | (dA ? 0u : 128u);
     }
     if (bal2) {
-      if (both) {
-        const int slot = (rtail + n1 + (int)__builtin_amdgcn_mbcnt_hi((uint32_t)(bal2 >> 32),
-                                                                     __builtin_amdgcn_mbcnt_lo((uint32_t)bal2, 0u))) &
+      if (dA && dB) {
+        const int slot = (int)__builtin_amdgcn_mbcnt_hi((uint32_t)(bal2 >> 32),
+                                                        __builtin_amdgcn_mbcnt_lo((uint32_t)bal2, (uint32_t)(rtail + n1))) &
                          (STAGE_CAP - 1);
         stage[wave][0][slot] = make_float4(acc[8], acc[9], acc[10], acc[11]);
         stage[wave][1][slot] = make_float4(acc[12], acc[13], acc[14], acc[15]);
@@ -2000,14 +2021,21 @@ hipError_t launch_fused_scan(const Problem& pb, const Pass& ps, const PassBufs& 
   const unsigned grid = (unsigned)(ps.nc * a.wgs_per_chunk);
 #define TOPK_SCAN(D_, G_, C_)                                                 \
   do {                                                                        \
-    if (cfg.R == 3) k_fused_scan<D_, 3, G_, C_><<<grid, 256, 0, st>>>(a);     \
-    else if (cfg.R == 6) k_fused_scan<D_, 6, G_, C_><<<grid, 256, 0, st>>>(a); \
-    else k_fused_scan<D_, 12, G_, C_><<<grid, 256, 0, st>>>(a);               \
+    if (D_ == 64 && cfg.union_rank == 13) k_fused_scan<D_, 11, G_, C_, false, 13><<<grid, 256, 0, st>>>(a);      \
+    else if (D_ == 64 && cfg.union_rank == 20) k_fused_scan<D_, 11, G_, C_, false, 20><<<grid, 256, 0, st>>>(a); \
+    else if (D_ == 128 && cfg.R == 3) k_fused_scan<D_, 3, G_, C_><<<grid, 256, 0, st>>>(a);                      \
+    else if (D_ == 128 && cfg.R == 6) k_fused_scan<D_, 6, G_, C_><<<grid, 256, 0, st>>>(a);                      \
+    else k_fused_scan<D_, 12, G_, C_><<<grid, 256, 0, st>>>(a);                                                 \
   } while (0)
-  if (G != 2) return hipErrorInvalidValue;
-  if (cfg.score_only) {  // the ablation exists for the d = 64, k <= 64 sampled non-causal shape only
-    if (pb.d != 64 || causal || cfg.mode != MODE_SAMPLE || cfg.R != 6) return hipErrorInvalidValue;
-    k_fused_scan<64, 6, 2, false, true><<<grid, 256, 0, st>>>(a);
+  // the instantiated sample rules (R, J): d = 64: (11, 13), (11, 20), (12, 0); d = 128:
+  // (3, 0), (6, 0), (12, 0)
+  const bool rule_ok = pb.d == 64 ? (cfg.R == 11 && (cfg.union_rank == 13 || cfg.union_rank == 20)) ||
+                                        (cfg.R == 12 && cfg.union_rank == 0)
+                                  : cfg.union_rank == 0 && (cfg.R == 3 || cfg.R == 6 || cfg.R == 12);
+  if (G != 2 || (cfg.mode == MODE_SAMPLE && !rule_ok)) return hipErrorInvalidValue;
+  if (cfg.score_only) {  // the ablation exists for the d = 64, 32 < k <= 64 sampled non-causal shape only
+    if (pb.d != 64 || causal || cfg.mode != MODE_SAMPLE || cfg.union_rank != 20) return hipErrorInvalidValue;
+    k_fused_scan<64, 11, 2, false, true, 20><<<grid, 256, 0, st>>>(a);
     return hipGetLastError();
   }
   if (pb.d == 64 && !causal) TOPK_SCAN(64, 2, false);
