@@ -722,7 +722,10 @@ __global__ __launch_bounds__(256, D == 64 ? (CAUSAL ? ScanShape<G>::OCC_CAUSAL :
   __shared__ float tau_lds[4][32 * G];
   __shared__ uint32_t cnt_lds[4][32 * G];
 
-  const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63, half = lane >> 5, n = lane & 31;
+  // the wave index is uniform: kept in a scalar register, so LDS and load addresses
+  // that depend on it need no vector arithmetic
+  const int tid = threadIdx.x, wave = __builtin_amdgcn_readfirstlane(tid >> 6), lane = tid & 63,
+            half = lane >> 5, n = lane & 31;
   // XCD-aware order: the hardware deals workgroups round-robin over the 8 XCDs;
   // renumber so each XCD runs consecutive logical workgroups (same head) and K
   // stays in that XCD's L2.
@@ -763,7 +766,27 @@ __global__ __launch_bounds__(256, D == 64 ? (CAUSAL ? ScanShape<G>::OCC_CAUSAL :
   // fills LDS position cidx = (wave*LPW + j)*64 + lane with part
   // (cidx % CH) ^ (row & 7) of key row cidx / CH (rows past Lk load the last key;
   // their scores are masked)
+  // Load number q = wave*LPW + j covers key rows q*RPL .. q*RPL + RPL - 1; within them
+  // the lane's element offset depends on q only through q mod NPAT (the swizzle
+  // repeats every 8 rows), so the lane keeps NPAT offsets (one at d = 64).
+  constexpr int RPL = 64 / CH, NPAT = RPL % 8 == 0 ? 1 : 8 / RPL;
+  uint32_t lane_off[NPAT];
+#pragma unroll
+  for (int e = 0; e < NPAT; ++e) {
+    const int r = e * RPL + lane / CH, p = (lane % CH) ^ (r & 7);
+    lane_off[e] = (uint32_t)((lane / CH) * D + p * 8);
+  }
   auto issue = [&](int64_t t, unsigned char* dst) {
+    if ((t + 1) * KT <= a.Lk) {  // whole tile: a uniform base plus the lane's offset
+      const uint16_t* base = Kh + t * KT * D;
+#pragma unroll
+      for (int j = 0; j < LPW; ++j) {
+        const int q = wave * LPW + j;
+        __builtin_amdgcn_global_load_lds((const void*)(base + q * RPL * D + lane_off[q % NPAT]),
+                                         (__attribute__((address_space(3))) void*)&dst[q * 1024], 16, 0, 0);
+      }
+      return;
+    }
 #pragma unroll
     for (int j = 0; j < LPW; ++j) {
       const int cidx = (wave * LPW + j) * 64 + lane, r = cidx / CH, p = (cidx % CH) ^ (r & 7);
@@ -831,6 +854,28 @@ __global__ __launch_bounds__(256, D == 64 ? (CAUSAL ? ScanShape<G>::OCC_CAUSAL :
       for (int v = 0; v < 16; ++v)
         if (8 * (v >> 2) + (v & 3) > room) acc[g][v] = -INFINITY;
     }
+  };
+  // the A operand (32 keys of block rb) and one group's 4 MFMAs, for the pipelined scan
+  auto read_a = [&](const unsigned char* kb, int rb, bf16x8 (&av)[NS]) {
+    const int r = rb * 32 + n;
+#pragma unroll
+    for (int s = 0; s < NS; ++s) av[s] = *(const bf16x8*)(kb + (r * CH + ((half * NS + s) ^ (r & 7))) * 16);
+  };
+  auto group_scores = [&](const bf16x8 (&av)[NS], const bf16x8 (&bg)[NS], f32x16& acc) {
+    acc = (f32x16){};
+#pragma unroll
+    for (int s = 0; s < NS; ++s) acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(av[s], bg[s], acc, 0, 0, 0);
+  };
+  // the tail and causal masks of one group's block
+  auto mask_group = [&](f32x16& acc, int g, int64_t t, int rb) {
+    if (tail && t == ntiles - 1) mask_keys(acc, t * KT + rb * 32 + 4 * half);
+    if (!CAUSAL) return;
+    const int64_t j0 = t * KT + rb * 32;
+    if (j0 + 31 <= wave_q0) return;
+    const int room = (int)(wave_q0 - j0) + g * 32 + n - 4 * half;
+#pragma unroll
+    for (int v = 0; v < 16; ++v)
+      if (8 * (v >> 2) + (v & 3) > room) acc[v] = -INFINITY;
   };
   // maxima of finite scores (and -inf): the NaN-propagating maximum, which needs no
   // canonicalising instructions and fuses into three-input maxima
@@ -1011,33 +1056,65 @@ __global__ __launch_bounds__(256, D == 64 ? (CAUSAL ? ScanShape<G>::OCC_CAUSAL :
   // Main scan: tile by tile. A tile's wait and barrier, and the loads of the next
   // tile into the other buffer, come first; then its 32-key blocks.
   float core_sink = -INFINITY;
-  issue(0, ks0);
-  alternate(ntiles, [&](int64_t t, const unsigned char* cur, unsigned char* nxt) {
-    __builtin_amdgcn_s_waitcnt(TOPK_WAIT_VM(0));
-    __syncthreads();
-    // drain whole 64-slot rounds at the tile boundary, before the next tile's loads
-    // are issued: the drain's LDS counter updates then have no direct loads to wait
-    // for, and its candidate stores complete while this tile is computed instead of
-    // delaying a later wait
-    if (t > 0 && rtail - rhead >= 64) drain_to(rhead + ((rtail - rhead) & ~63));
-    if (t + 1 < ntiles) issue(t + 1, nxt);
+  if constexpr (SCORE_ONLY) {
+    // the ablation keeps the plain order (both groups' MFMAs, then both maxima)
+    issue(0, ks0);
+    alternate(ntiles, [&](int64_t t, const unsigned char* cur, unsigned char* nxt) {
+      __builtin_amdgcn_s_waitcnt(TOPK_WAIT_VM(0));
+      __syncthreads();
+      if (t + 1 < ntiles) issue(t + 1, nxt);
 #pragma unroll
-    for (int rb = 0; rb < NRB; ++rb) {
-      f32x16 x[G];
-      block_scores(cur, rb, x);
-      if (tail && t == ntiles - 1) {
-        const int64_t jb = t * KT + rb * 32 + 4 * half;
+      for (int rb = 0; rb < NRB; ++rb) {
+        f32x16 x[G];
+        block_scores(cur, rb, x);
+        if (tail && t == ntiles - 1) {
+          const int64_t jb = t * KT + rb * 32 + 4 * half;
 #pragma unroll
-        for (int g = 0; g < G; ++g) mask_keys(x[g], jb);
+          for (int g = 0; g < G; ++g) mask_keys(x[g], jb);
+        }
+        mask_future(x, t, rb);
+#pragma unroll
+        for (int g = 0; g < G; ++g) core_sink = fmax_(core_sink, block_max(x[g]) - tau[g]);
       }
-      mask_future(x, t, rb);
+    });
+  } else {
+    // Each block's group-0 MFMAs are issued before the previous block's group-1
+    // filter, and its group-1 MFMAs before its own group-0 filter, so a wave has a
+    // filter (VALU, LDS) to run while its own MFMAs execute. Group 1 of a tile's last
+    // block is filtered after the next tile's barrier (its scores are in registers).
+    static_assert(G == 2, "the pipelined scan alternates two query groups");
+    f32x16 x0, x1;
+    int64_t pt = -1;  // tile of the block whose group 1 still awaits its filter
+    int prb = 0;
+    auto filter1 = [&]() {
+      mask_group(x1, 1, pt, prb);
+      filter(1, x1, pt, prb);
+    };
+    issue(0, ks0);
+    alternate(ntiles, [&](int64_t t, const unsigned char* cur, unsigned char* nxt) {
+      __builtin_amdgcn_s_waitcnt(TOPK_WAIT_VM(0));
+      __syncthreads();
+      // drain whole 64-slot rounds at the tile boundary, before the next tile's loads
+      // are issued: the drain's LDS counter updates then have no direct loads to wait
+      // for, and its candidate stores complete while this tile is computed instead of
+      // delaying a later wait
+      if (t > 0 && rtail - rhead >= 64) drain_to(rhead + ((rtail - rhead) & ~63));
+      if (t + 1 < ntiles) issue(t + 1, nxt);
 #pragma unroll
-      for (int g = 0; g < G; ++g) {
-        if (SCORE_ONLY) core_sink = fmax_(core_sink, block_max(x[g]) - tau[g]);
-        else filter(g, x[g], t, rb);
+      for (int rb = 0; rb < NRB; ++rb) {
+        bf16x8 av[NS];
+        read_a(cur, rb, av);
+        group_scores(av, b[0], x0);
+        if (pt >= 0) filter1();
+        group_scores(av, b[1], x1);
+        mask_group(x0, 0, t, rb);
+        filter(0, x0, t, rb);
+        pt = t;
+        prb = rb;
       }
-    }
-  });
+    });
+    if (pt >= 0) filter1();
+  }
   if (SCORE_ONLY) {
     if (ok[0]) a.cnt[(wave_row0 + n) * 2 + half] = (int32_t)__float_as_uint(core_sink);
     return;
