@@ -57,10 +57,21 @@ def traffic_for_current_kernel(workload: str, path: int):
     return t.get("bytes_per_launch")
 
 
+def _is_scan_ablation(name: str) -> bool:
+    """The score-only ablation of the scan (fifth template argument true), which the
+    benchmark also runs: its dispatches are not the scan's."""
+    if "k_fused_scan<" not in name:
+        return False
+    args = [a.strip() for a in name.split("k_fused_scan<", 1)[1].split(">", 1)[0].split(",")]
+    return len(args) > 4 and args[4] == "true"
+
+
 def _pmc_average(path: str, kernel_substr: str) -> float:
-    """Average counter value per dispatch (KiB) of the kernels whose name holds kernel_substr."""
+    """Average counter value per dispatch (KiB) of the kernels whose name holds
+    kernel_substr (the scan's score-only ablation excluded)."""
     import csv
-    vals = [float(r["Counter_Value"]) for r in csv.DictReader(open(path)) if kernel_substr in r["Kernel_Name"]]
+    vals = [float(r["Counter_Value"]) for r in csv.DictReader(open(path))
+            if kernel_substr in r["Kernel_Name"] and not _is_scan_ablation(r["Kernel_Name"])]
     if not vals:
         raise SystemExit(f"no dispatch of {kernel_substr} in {path}")
     return sum(vals) / len(vals)
