@@ -87,6 +87,10 @@ MHA_CASES = {
     # causal heads (chunk-tile path), ragged chunks
     "bf16_causal": dict(dtype=wl.BF16, B=1, L=333, H=3, dh=64, k=32, chunk=128, causal=True),
     "fp32_causal": dict(dtype=wl.F32, B=2, L=200, H=2, dh=32, k=8, chunk=48, causal=True),
+    # BERT-base shape (d_model 768, 12 heads of 64, k 128), bidirectional (fused heads,
+    # every key a candidate) and causal (chunk-tile heads)
+    "bf16_bert_base": dict(dtype=wl.BF16, B=1, L=1024, H=12, dh=64, k=128, chunk=256, causal=False),
+    "bf16_bert_base_causal": dict(dtype=wl.BF16, B=1, L=2048, H=12, dh=64, k=128, chunk=1024, causal=True),
 }
 
 
