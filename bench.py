@@ -116,15 +116,24 @@ def cpu_baseline(w, x, budget_s: float):
     from concurrent.futures import FIRST_COMPLETED, ThreadPoolExecutor, wait
     from oracle import topk_oracle as o
     from threadpoolctl import threadpool_limits
-    Q, K, V = (x[n].values for n in ("Q", "K", "V"))
     cores = min(len(os.sched_getaffinity(0)), 16)
-    chunks = [(b, h, c0) for b in range(w.B) for h in range(w.H) for c0 in range(0, w.Lq, w.chunk)]
+    if w.kind == "attn":
+        Q, K, V = (x[n].values for n in ("Q", "K", "V"))
+        chunks = [(b, h, c0) for b in range(w.B) for h in range(w.H) for c0 in range(0, w.Lq, w.chunk)]
 
-    def one(t):
-        b, h, c0 = t
-        i = np.arange(c0, min(c0 + w.chunk, w.Lq))
-        o.topk_rows(Q[b, h, i], K[b, h], V[b, h], w.k, o.valid_lengths(i, w.Lk, w.causal), "softmax", w.scale)
-        return i.size
+        def one(t):
+            b, h, c0 = t
+            i = np.arange(c0, min(c0 + w.chunk, w.Lq))
+            o.topk_rows(Q[b, h, i], K[b, h], V[b, h], w.k, o.valid_lengths(i, w.Lk, w.causal), "softmax", w.scale)
+            return i.size
+    else:  # feed-forward: tokens against the rows of W1 (keys) and W2 (values), ReLU weights
+        X, W1, W2 = (x[n].values for n in ("X", "W1", "W2"))
+        chunks = list(range(0, w.N, w.chunk))
+
+        def one(c0):
+            i = np.arange(c0, min(c0 + w.chunk, w.N))
+            o.topk_rows(X[i], W1, W2, w.k, np.full(i.size, w.d_ff), "relu")
+            return i.size
 
     done = 0
     with threadpool_limits(1), ThreadPoolExecutor(cores) as ex:
@@ -599,8 +608,10 @@ def main():
                        2: "score stage: k_tile_scores_mfma" if w.dtype == wl.BF16 and w.d % 32 == 0 else
                           "score stage: k_tile_scores (fp32)",
                        3: "score stage: k_tile_scores_mfma (rows below 1024 R) + k_fused_scan",
-                       4: "score stage: k_tile_scores_mfma sample + k_filter_threshold + filtered "
-                          "k_tile_scores_mfma"}.get(path, str(path)),
+                       4: "score stage: k_tile_scores_mfma sample + k_filter_threshold + "
+                          + ("thresholded k_fused_scan (direct appends)"
+                             if (w.d if w.kind == "attn" else w.d_model) == 128 and w.dtype == wl.BF16
+                             else "filtered k_tile_scores_mfma")}.get(path, str(path)),
             "bound": "mfma",
             "achieved": achieved,
             "peak": PEAK_BF16_TFLOPS,

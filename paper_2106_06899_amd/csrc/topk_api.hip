@@ -228,7 +228,9 @@ PassBufs carve(const Problem& pb, const Plan& pl, char* ws) {
     off += up(rows * 8);
     b.scores = (float*)(ws + off);
     off += up((size_t)(REDO_CAP + REDO_BLOCKS) * pb.Lk * 4);
-    b.cand_single = 1;  // one list per row: the fused scan and the filtered GEMM both append to it
+    // one list per row, which the fused scan and the filtered tile GEMM append to; the
+    // filtered path's scan keeps one list per row and half-wave
+    b.cand_single = pl.path == PATH_FILTER && filter_scan_ok(pb) ? 0 : 1;
     if (pl.path == PATH_FILTER) {
       b.samp = (float*)(ws + off);
       off += up(rows * (size_t)((pb.Lk + FILTER_KSTRIDE - 1) / FILTER_KSTRIDE) * 4);

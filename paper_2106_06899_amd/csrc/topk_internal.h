@@ -12,7 +12,8 @@ enum ElemType { T_F32 = 0, T_BF16 = 1 };
 
 // Sampling modes of the fused scan: ALL keeps every valid score as a candidate;
 // SAMPLE first estimates a per-query threshold from a strided subset of key tiles.
-enum ScanMode { MODE_ALL = 0, MODE_SAMPLE = 1 };
+// THRESH takes each query's threshold from the filtered path's sample (PassBufs::thr).
+enum ScanMode { MODE_ALL = 0, MODE_SAMPLE = 1, MODE_THRESH = 2 };
 
 constexpr int REDO_CAP = 1024;          // redo rows recomputed by the wide fallback kernels
 constexpr int REDO_SPLIT = 512;         // keys per work item of the wide fallback
@@ -53,6 +54,11 @@ struct Pass {
 constexpr int FILTER_KSTRIDE = 16;
 constexpr int64_t FILTER_MAX_LK = 65536;  // at most 4096 samples per row
 
+// The filtered path scores its candidates with the scan kernel (direct mode, one
+// candidate list per row and half-wave) for bf16 keys of d = 128; with the MFMA tile
+// GEMM (one list per row) otherwise.
+inline bool filter_scan_ok(const Problem& pb) { return pb.dtype == T_BF16 && pb.d == 128; }
+
 // Workspace pointers of one pass.
 struct PassBufs {
   uint64_t* sel;      // [rows, k] selected keys, (score desc, index asc); 0 pads
@@ -62,7 +68,8 @@ struct PassBufs {
   uint64_t* cand;     // fused and filtered paths: [rows, 2, caph]
   int32_t* cnt;       // fused and filtered paths: [rows, 2]
   int64_t caph;
-  int cand_single;    // filtered path: one list of up to 2 caph per row, its length in cnt[2p]
+  int cand_single;    // one list of up to 2 caph per row, its length in cnt[2p] (fused scan,
+                      // filtered tile GEMM); 0: two lists of caph, lengths cnt[2p], cnt[2p + 1]
   float* samp;        // filtered path: [rows, ceil(Lk / FILTER_KSTRIDE)] sampled scores
   float* thr;         // filtered path: [rows] thresholds
 };
@@ -158,5 +165,6 @@ struct BwdBufs {
 
 hipError_t launch_backward(const BwdProblem& bp, const BwdBufs& b, hipStream_t st);
 hipError_t launch_filter(const Problem& pb, const Pass& ps, const PassBufs& b, int stage, hipStream_t st);
+hipError_t launch_filter_scan(const Problem& pb, const Pass& ps, const PassBufs& b, hipStream_t st);
 
 }  // namespace topk

@@ -71,11 +71,24 @@ struct RowRef {
   bool ok;
 };
 __device__ __forceinline__ RowRef row_of(const Problem& pb, const Pass& ps, int64_t p) {
-  int64_t chunk_local = p / pb.C, r = p - chunk_local * pb.C;
-  int64_t id = ps.c0 + chunk_local;
+  int64_t chunk_local, r, id, c;
   RowRef rr;
-  rr.bh = id / ps.nchunk;
-  rr.i = pb.q0 + (id - rr.bh * ps.nchunk) * pb.C + r;
+  if (((uint64_t)p | (uint64_t)pb.C | (uint64_t)(ps.c0 + ps.nc) | (uint64_t)ps.nchunk) >> 31 == 0) {
+    // the common case: 32-bit divisions (a few instructions instead of a 64-bit routine)
+    const uint32_t cl32 = (uint32_t)p / (uint32_t)pb.C, id32 = (uint32_t)ps.c0 + cl32;
+    chunk_local = cl32;
+    r = (uint32_t)p - cl32 * (uint32_t)pb.C;
+    id = id32;
+    rr.bh = id32 / (uint32_t)ps.nchunk;
+    c = id32 - (uint32_t)rr.bh * (uint32_t)ps.nchunk;
+  } else {
+    chunk_local = p / pb.C;
+    r = p - chunk_local * pb.C;
+    id = ps.c0 + chunk_local;
+    rr.bh = id / ps.nchunk;
+    c = id - rr.bh * ps.nchunk;
+  }
+  rr.i = pb.q0 + c * pb.C + r;
   rr.ok = chunk_local < ps.nc && rr.i < pb.q1;
   return rr;
 }
@@ -378,12 +391,15 @@ __global__ __launch_bounds__(256, 2) void k_tile_scores_mfma(Problem pb, Pass ps
   if (MODE == 2) {
     // candidates: count this lane's passing scores per row, reserve room per row in
     // LDS, then once per row and workgroup in the row's global list
-    uint32_t* rc = (uint32_t*)&sm[0][0];
+    static_assert(4 * 8192 + 4 * TQ <= 2 * (QBYTES + KBYTES), "stash and row counts fit the operand buffers");
+    uint32_t* rc = (uint32_t*)&sm[0][0] + 4 * 2048;  // after the four waves' stashes
+    float* stash = (float*)&sm[0][0] + wave * 2048;  // this wave's 32 scores per lane
     __syncthreads();  // every wave is done with the operand buffers
     if (tid < TQ) rc[tid] = 0;
     __syncthreads();
     uint32_t off[2];
-    uint32_t pass[2][4];  // bit v: score v of block (a, b) is a candidate
+    // pass[a][h], bit j = 16 * (b - 2h) + v: score v of block (a, b) is a candidate
+    uint32_t pass[2][2];
     // keys of this wave's sub-tile all valid for every row of the tile (no causal
     // diagonal, no tail): the per-key test can go
     const int64_t kend = key0 + wk + 128;
@@ -396,21 +412,26 @@ __global__ __launch_bounds__(256, 2) void k_tile_scores_mfma(Problem pb, Pass ps
       const float ts = okr ? bufs.thr[cl * pb.C + lr] : INFINITY;
       uint32_t c = 0;
 #pragma unroll
-      for (int b = 0; b < 4; ++b) {
+      for (int h = 0; h < 2; ++h) {
         uint32_t m = 0;
         if (all_valid) {
+          // highest bit first, m = 2m + pass: an add with the comparison as carry-in
 #pragma unroll
-          for (int v = 0; v < 16; ++v) m |= (acc[a][b][v] >= ts ? 1u : 0u) << v;
+          for (int j = 31; j >= 0; --j) m = m + m + (uint32_t)(acc[a][2 * h + (j >> 4)][j & 15] >= ts);
         } else {
-          const int64_t kb = key0 + wk + b * 32 + 4 * half;
 #pragma unroll
-          for (int v = 0; v < 16; ++v)
-            m |= (kb + 8 * (v >> 2) + (v & 3) < nv && acc[a][b][v] >= ts ? 1u : 0u) << v;
+          for (int bb = 0; bb < 2; ++bb) {
+            const int b = 2 * h + bb;
+            const int64_t kb = key0 + wk + b * 32 + 4 * half;
+#pragma unroll
+            for (int v = 0; v < 16; ++v)
+              m |= (kb + 8 * (v >> 2) + (v & 3) < nv && acc[a][b][v] >= ts ? 1u : 0u) << (16 * bb + v);
+          }
         }
         // rows past the chunk or the sequence hold the tile's first row's scores (and a
         // threshold of +inf, which a +inf score would still meet): they append nothing
         m = okr ? m : 0u;
-        pass[a][b] = m;
+        pass[a][h] = m;
         c += (uint32_t)__builtin_popcount(m);
       }
       off[a] = c ? atomicAdd(&rc[wq + a * 32 + n], c) : 0u;
@@ -430,27 +451,22 @@ __global__ __launch_bounds__(256, 2) void k_tile_scores_mfma(Problem pb, Pass ps
       uint32_t pos = rc[wq + a * 32 + n] + off[a];
       uint64_t* dst = bufs.cand + 2 * (cl * pb.C + lr) * bufs.caph;
 #pragma unroll
-      for (int b = 0; b < 4; ++b) {
-        const uint32_t kb = (uint32_t)(key0 + wk + b * 32 + 4 * half);
-        // scores of this block as a list of set bits: the wave loops as often as its
-        // busiest lane; the score is picked from the 16 registers by a binary tree of
-        // bitwise muxes, one level per bit of its index
-        for (uint32_t m = pass[a][b]; m; m &= m - 1) {
-          const uint32_t v = (uint32_t)__builtin_ctz(m);
-          const f32x16& x16 = acc[a][b];
-          uint32_t t8[8], t4[4], t2[2];
-          const uint32_t s0 = 0u - (v & 1u), s1 = 0u - ((v >> 1) & 1u), s2 = 0u - ((v >> 2) & 1u),
-                         s3 = 0u - ((v >> 3) & 1u);
+      for (int h = 0; h < 2; ++h) {
+        // The 32 scores of blocks (a, 2h) and (a, 2h + 1) go to the wave's LDS stash,
+        // score j of the lane at float j * 64 + lane (full-width writes, two scores per
+        // instruction); the lane then walks its set bits and reads each passing score
+        // back by its index, from its own bank. A wave reads only what its own lanes
+        // wrote, and its LDS accesses complete in order: no barrier. The next stash
+        // overwrites this one only after every read of this one was issued.
 #pragma unroll
-          for (int u = 0; u < 8; ++u)
-            t8[u] = (__float_as_uint(x16[2 * u + 1]) & s0) | (__float_as_uint(x16[2 * u]) & ~s0);
-#pragma unroll
-          for (int u = 0; u < 4; ++u) t4[u] = (t8[2 * u + 1] & s1) | (t8[2 * u] & ~s1);
-#pragma unroll
-          for (int u = 0; u < 2; ++u) t2[u] = (t4[2 * u + 1] & s2) | (t4[2 * u] & ~s2);
-          const float x = __uint_as_float((t2[1] & s3) | (t2[0] & ~s3));
-          if (pos < cap)
-            dst[pos] = ((uint64_t)__float_as_uint(x) << 32) | (uint64_t)(0xFFFFFFFFu - (kb + 8 * (v >> 2) + (v & 3)));
+        for (int j = 0; j < 32; ++j) stash[j * 64 + lane] = acc[a][2 * h + (j >> 4)][j & 15];
+        // bit j is key 8 * (j / 4) + j % 4 = j + (j & ~3) past the lane's first key of
+        // block 2h
+        const uint32_t nk0 = 0xFFFFFFFFu - (uint32_t)(key0 + wk + 64 * h + 4 * half);
+        for (uint32_t m = pass[a][h]; m; m &= m - 1) {
+          const uint32_t j = (uint32_t)__builtin_ctz(m);
+          const float x = stash[j * 64 + lane];
+          if (pos < cap) dst[pos] = ((uint64_t)__float_as_uint(x) << 32) | (uint64_t)(nk0 - (j + (j & ~3u)));
           ++pos;
         }
       }
@@ -666,10 +682,12 @@ struct ScanArgs {
   uint64_t* cand;
   int32_t* cnt;
   int64_t caph;
+  const float* thr;  // MODE_THRESH: per pass-local row, the threshold its candidates beat
   int mode, stride, causal;
 };
 
 constexpr int SCAN_KT = 64;  // keys per K tile
+typedef uint64_t u64x2 __attribute__((ext_vector_type(2)));
 
 // Launch shape of the scan: G = 32-query groups per wave, NB = K tile buffers in
 // LDS, CAP = staged 8-score half blocks per wave (whole 64-slot rounds drain at
@@ -695,7 +713,11 @@ constexpr int scan_queries_per_wg() { return 4 * 32 * G; }
 // and each block's maximum, and drops the filter (no staging, no drain, no candidate
 // output; the maxima go to cnt so that the work is kept). It measures what the score
 // core alone costs at the same launch shape.
-template <int D, int R, int G, bool CAUSAL, bool SCORE_ONLY = false, int J = 0>
+// DIRECT: the variant for dense candidates (the filtered path, MODE_THRESH): each
+// row's threshold comes from a.thr, and every lane appends its own passing scores of
+// each block straight to its own list (one per query and half-wave, the length in
+// cnt[2 * row + half]) instead of staging dirty blocks; see `extract`.
+template <int D, int R, int G, bool CAUSAL, bool SCORE_ONLY = false, int J = 0, bool DIRECT = false>
 __global__ __launch_bounds__(256, D == 64 ? (CAUSAL ? ScanShape<G>::OCC_CAUSAL : ScanShape<G>::OCC) : 2) void k_fused_scan(
     ScanArgs a) {
   static_assert(ScanShape<G>::CAP >= 128, "a ring holds one block's 64 lanes, both halves");
@@ -889,7 +911,7 @@ __global__ __launch_bounds__(256, D == 64 ? (CAUSAL ? ScanShape<G>::OCC_CAUSAL :
 
   float tau[G];
 #pragma unroll
-  for (int g = 0; g < G; ++g) tau[g] = -INFINITY;
+  for (int g = 0; g < G; ++g) tau[g] = a.mode == MODE_THRESH && ok[g] ? a.thr[wave_row0 + g * 32 + n] : -INFINITY;
   // Causal rows sample the same 1-in-stride tiles; the masked (future) keys of a
   // sampled tile give -inf block maxima, so a row's threshold depends on the row
   // alone. The host sends only rows with enough valid sampled blocks this way.
@@ -1053,6 +1075,43 @@ __global__ __launch_bounds__(256, D == 64 ? (CAUSAL ? ScanShape<G>::OCC_CAUSAL :
     }
     rtail += n1 + n2;
   };
+  // DIRECT: the lane's passing scores of one 16-score lane block, as bits (highest
+  // first, m = 2m + pass: an add with the comparison as carry-in); the 16 scores go to
+  // the wave's stash in LDS (score v of the lane at float v * 64 + lane, full-width
+  // writes), and the lane walks its bits, reading each passing score back by its index
+  // from its own bank and appending it to its list. A wave reads only what its own
+  // lanes wrote and its LDS accesses complete in order, so the stash needs no barrier,
+  // and the next block's stash is written only after every read of this one.
+  uint32_t dpos[G] = {};
+  uint64_t dheld[G] = {};
+  float* const dstash = (float*)&stage[wave][0][0];
+  static_assert(sizeof(stage[0]) >= 16 * 64 * sizeof(float), "a wave's stash holds 16 scores per lane");
+  auto extract = [&](int g, const f32x16& acc, int64_t t, int rb) {
+    uint32_t m = 0;
+#pragma unroll
+    for (int v = 15; v >= 0; --v) m = m + m + (uint32_t)(acc[v] > tau[g]);
+    if (__builtin_amdgcn_ballot_w64(m != 0) == 0) return;
+#pragma unroll
+    for (int v = 0; v < 16; ++v) dstash[v * 64 + lane] = acc[v];
+    // score v is key 8 * (v / 4) + v % 4 = v + (v & ~3) past the lane's first key
+    const uint32_t nk0 = 0xFFFFFFFFu - (uint32_t)(t * KT + rb * 32 + 4 * half);
+    uint64_t* dst = a.cand + ((wave_row0 + g * 32 + n) * 2 + half) * a.caph;
+    uint32_t pos = dpos[g];
+    for (; m; m &= m - 1) {
+      const uint32_t v = (uint32_t)__builtin_ctz(m);
+      const float x = dstash[v * 64 + lane];
+      const uint64_t w = ((uint64_t)__float_as_uint(x) << 32) | (uint64_t)(nk0 - (v + (v & ~3u)));
+      // words go out in pairs (one 16-byte store per two candidates); an even position
+      // waits in a register for its partner
+      if (pos & 1) {
+        if (pos < (uint32_t)a.caph) *(u64x2*)&dst[pos - 1] = (u64x2){dheld[g], w};
+      } else {
+        dheld[g] = w;
+      }
+      ++pos;
+    }
+    dpos[g] = pos;
+  };
   // Main scan: tile by tile. A tile's wait and barrier, and the loads of the next
   // tile into the other buffer, come first; then its 32-key blocks.
   float core_sink = -INFINITY;
@@ -1088,7 +1147,8 @@ __global__ __launch_bounds__(256, D == 64 ? (CAUSAL ? ScanShape<G>::OCC_CAUSAL :
     int prb = 0;
     auto filter1 = [&]() {
       mask_group(x1, 1, pt, prb);
-      filter(1, x1, pt, prb);
+      if constexpr (DIRECT) extract(1, x1, pt, prb);
+      else filter(1, x1, pt, prb);
     };
     issue(0, ks0);
     alternate(ntiles, [&](int64_t t, const unsigned char* cur, unsigned char* nxt) {
@@ -1098,7 +1158,7 @@ __global__ __launch_bounds__(256, D == 64 ? (CAUSAL ? ScanShape<G>::OCC_CAUSAL :
       // are issued: the drain's LDS counter updates then have no direct loads to wait
       // for, and its candidate stores complete while this tile is computed instead of
       // delaying a later wait
-      if (t > 0 && rtail - rhead >= 64) drain_to(rhead + ((rtail - rhead) & ~63));
+      if (!DIRECT && t > 0 && rtail - rhead >= 64) drain_to(rhead + ((rtail - rhead) & ~63));
       if (t + 1 < ntiles) issue(t + 1, nxt);
 #pragma unroll
       for (int rb = 0; rb < NRB; ++rb) {
@@ -1108,7 +1168,8 @@ __global__ __launch_bounds__(256, D == 64 ? (CAUSAL ? ScanShape<G>::OCC_CAUSAL :
         if (pt >= 0) filter1();
         group_scores(av, b[1], x1);
         mask_group(x0, 0, t, rb);
-        filter(0, x0, t, rb);
+        if constexpr (DIRECT) extract(0, x0, t, rb);
+        else filter(0, x0, t, rb);
         pt = t;
         prb = rb;
       }
@@ -1117,6 +1178,15 @@ __global__ __launch_bounds__(256, D == 64 ? (CAUSAL ? ScanShape<G>::OCC_CAUSAL :
   }
   if (SCORE_ONLY) {
     if (ok[0]) a.cnt[(wave_row0 + n) * 2 + half] = (int32_t)__float_as_uint(core_sink);
+    return;
+  }
+  if constexpr (DIRECT) {
+#pragma unroll
+    for (int g = 0; g < G; ++g) {
+      const uint32_t pos = dpos[g];
+      if ((pos & 1) && pos - 1 < (uint32_t)a.caph) a.cand[((wave_row0 + g * 32 + n) * 2 + half) * a.caph + pos - 1] = dheld[g];
+      if (ok[g]) a.cnt[(wave_row0 + g * 32 + n) * 2 + half] = (int32_t)pos;
+    }
     return;
   }
   drain();
@@ -1424,14 +1494,21 @@ __global__ __launch_bounds__(64) void k_cand_select(Problem pb, Pass ps, PassBuf
 // ------------------------------------------------------------------ filtered chunk-tile path
 // Per row, the threshold is the R-th largest of its valid sampled scores (every
 // FILTER_KSTRIDE-th key), R a few standard deviations above the sample's expected
-// share mu of the top k_eff, resolved to THRESH_PASSES radix digits (it may lie a
-// little below that sample, never above). About R * FILTER_KSTRIDE scores of the row
+// share mu of the top k_eff, resolved to a few bits below those all the row's samples
+// share (it may lie a little below that sample, never above). About R * FILTER_KSTRIDE scores of the row
 // are then at or above it; a row with fewer than R valid samples keeps every valid key. The
 // candidate select proves each row's set complete (at least k_eff entries, no
 // overflow) or sends the row to the exact fallback.
-__global__ __launch_bounds__(64) void k_filter_threshold(Problem pb, Pass ps, PassBufs bufs) {
-  __shared__ uint32_t hist[256];
-  const int64_t p = blockIdx.x;
+// One wave per row, four rows per workgroup. The R-th largest sample is built bit by
+// bit, high to low, on the samples' order-preserving 32-bit keys: a bit is kept when at
+// least R samples are at or above the prefix with it set (one ballot per register of
+// samples, no LDS). Starting below the bits every sample shares, THRESH_BITS bits are
+// resolved; the threshold is then the smallest sample at or above the prefix, which is
+// at most the R-th largest.
+constexpr int THRESH_BITS = 16;
+__global__ __launch_bounds__(256) void k_filter_threshold(Problem pb, Pass ps, PassBufs bufs) {
+  const int64_t p = (int64_t)blockIdx.x * 4 + __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);  // uniform
+  if (p >= ps.nc * pb.C) return;
   const RowRef rr = row_of(pb, ps, p);
   if (!rr.ok) return;
   const int lane = threadIdx.x & 63;
@@ -1445,19 +1522,44 @@ __global__ __launch_bounds__(64) void k_filter_threshold(Problem pb, Pass ps, Pa
     const float* row = bufs.samp + p * ((pb.Lk + FILTER_KSTRIDE - 1) / FILTER_KSTRIDE);
     auto rth = [&](auto tag) {  // the R-th largest of the row's ns samples, or a little less
       constexpr int E = decltype(tag)::value;
-      uint64_t key[E];
+      uint32_t u[E];  // order-preserving keys; 0 (below every score's key) past the samples
+      uint32_t kmin = 0xFFFFFFFFu, kmax = 0u;
+#pragma unroll
+      for (int e = 0; e < E; ++e) {  // every load in flight at once (slots past ns read sample 0)
+        const int64_t s = lane + 64 * e;
+        u[e] = ord_u32(row[s < ns ? s : 0]);
+      }
 #pragma unroll
       for (int e = 0; e < E; ++e) {
-        const int64_t s = lane + 64 * e;
-        key[e] = s < ns ? make_key(row[s], (uint32_t)s) : 0ull;
+        if (lane + 64 * e < ns) {
+          kmin = min(kmin, u[e]);
+          kmax = max(kmax, u[e]);
+        } else {
+          u[e] = 0u;
+        }
       }
-      int shift;
-      uint64_t prefix;
-      wave_radix_select<E>(key, (int)ns, (uint32_t)R, hist, &shift, &prefix, THRESH_PASSES);
-      uint32_t m = 0xFFFFFFFFu;
+#pragma unroll
+      for (int off = 32; off > 0; off >>= 1) {
+        kmin = min(kmin, (uint32_t)__shfl_xor(kmin, off, 64));
+        kmax = max(kmax, (uint32_t)__shfl_xor(kmax, off, 64));
+      }
+      kmin = (uint32_t)__builtin_amdgcn_readfirstlane(kmin);
+      kmax = (uint32_t)__builtin_amdgcn_readfirstlane(kmax);
+      // bits [0, top) differ among the samples; the ones above are every sample's
+      const int top = kmin == kmax ? 0 : 32 - __builtin_clz(kmin ^ kmax);
+      uint32_t prefix = top >= 32 ? 0u : (kmax >> top) << top;
+      const int stop = top > THRESH_BITS ? top - THRESH_BITS : 0;
+      for (int b = top - 1; b >= stop; --b) {
+        const uint32_t cand = prefix | (1u << b);
+        uint32_t cnt = 0;
+#pragma unroll
+        for (int e = 0; e < E; ++e) cnt += (uint32_t)__popcll(__ballot(u[e] >= cand));
+        if (cnt >= (uint32_t)R) prefix = cand;
+      }
+      uint32_t m = 0xFFFFFFFFu;  // the smallest sample at or above the prefix
 #pragma unroll
       for (int e = 0; e < E; ++e)
-        if (lane + 64 * e < ns && (key[e] >> shift) >= (prefix >> shift)) m = min(m, (uint32_t)(key[e] >> 32));
+        if (lane + 64 * e < ns && u[e] >= prefix) m = min(m, u[e]);
       for (int off = 32; off > 0; off >>= 1) m = min(m, (uint32_t)__shfl_xor(m, off, 64));
       return ord_to_f32(m);
     };
@@ -1518,9 +1620,10 @@ hipError_t launch_filter(const Problem& pb, const Pass& ps, const PassBufs& b, i
     const int64_t g = ((slots + TSM_TK - 1) / TSM_TK) * ((pb.C + TSM_TQ - 1) / TSM_TQ) * ps.nc;
     if (g > 0x7FFFFFFF || pb.dtype != T_BF16 || pb.d % 32 != 0 || pb.Lk > FILTER_MAX_LK) return hipErrorInvalidValue;
     if (stage == 1) k_tile_scores_mfma<1><<<(unsigned)g, 256, 0, st>>>(pb, ps, b);
+    else if (filter_scan_ok(pb)) return launch_filter_scan(pb, ps, b, st);
     else k_tile_scores_mfma<2><<<(unsigned)g, 256, 0, st>>>(pb, ps, b);
   } else if ((pb.Lk + FILTER_KSTRIDE - 1) / FILTER_KSTRIDE <= 64 * CAND_REGS) {
-    k_filter_threshold<<<(unsigned)rows, 64, 0, st>>>(pb, ps, b);
+    k_filter_threshold<<<(unsigned)((rows + 3) / 4), 256, 0, st>>>(pb, ps, b);
   } else {
     k_filter_threshold_wg<<<(unsigned)rows, 256, 0, st>>>(pb, ps, b);
   }
@@ -2073,8 +2176,8 @@ hipError_t launch_tile_select(const Problem& pb, const Pass& ps, const PassBufs&
   return hipGetLastError();
 }
 
-hipError_t launch_fused_scan(const Problem& pb, const Pass& ps, const PassBufs& b, const ScanCfg& cfg,
-                             hipStream_t st) {
+// the scan's arguments for one pass (G = 2 query groups per wave)
+ScanArgs scan_args(const Problem& pb, const Pass& ps, const PassBufs& b, int mode, int stride) {
   ScanArgs a;
   a.Q = (const uint16_t*)pb.Q;
   a.K = (const uint16_t*)pb.K;
@@ -2089,12 +2192,31 @@ hipError_t launch_fused_scan(const Problem& pb, const Pass& ps, const PassBufs& 
   a.cand = b.cand;
   a.cnt = b.cnt;
   a.caph = b.caph;
-  a.mode = cfg.mode;
-  a.stride = cfg.stride;
+  a.thr = b.thr;
+  a.mode = mode;
+  a.stride = stride;
   a.causal = pb.causal ? 1 : 0;
+  a.wgs_per_chunk = (pb.C + scan_queries_per_wg<2>() - 1) / scan_queries_per_wg<2>();
+  return a;
+}
+
+// The filtered path's candidates (stage 3) by the scan in its direct mode: thresholds
+// from b.thr, one list per row and half-wave (b.cand_single == 0).
+hipError_t launch_filter_scan(const Problem& pb, const Pass& ps, const PassBufs& b, hipStream_t st) {
+  if (!filter_scan_ok(pb) || b.cand_single || !b.thr) return hipErrorInvalidValue;
+  const ScanArgs a = scan_args(pb, ps, b, MODE_THRESH, 1);
+  const int64_t grid = ps.nc * a.wgs_per_chunk;
+  if (grid > 0x7FFFFFFF) return hipErrorInvalidValue;
+  if (pb.causal) k_fused_scan<128, 3, 2, true, false, 0, true><<<(unsigned)grid, 256, 0, st>>>(a);
+  else k_fused_scan<128, 3, 2, false, false, 0, true><<<(unsigned)grid, 256, 0, st>>>(a);
+  return hipGetLastError();
+}
+
+hipError_t launch_fused_scan(const Problem& pb, const Pass& ps, const PassBufs& b, const ScanCfg& cfg,
+                             hipStream_t st) {
+  ScanArgs a = scan_args(pb, ps, b, cfg.mode, cfg.stride);
   const int G = cfg.groups;
   const bool causal = pb.causal != 0;
-  a.wgs_per_chunk = (pb.C + 128 * G - 1) / (128 * G);
   const unsigned grid = (unsigned)(ps.nc * a.wgs_per_chunk);
 #define TOPK_SCAN(D_, G_, C_)                                                 \
   do {                                                                        \
