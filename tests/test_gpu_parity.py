@@ -344,6 +344,23 @@ def test_filter_fallback_for_every_row():
     parity.check_attn(w, x, out, idx)
 
 
+@pytest.mark.parametrize("d", [128, 96])
+def test_filter_overflow_for_every_row(d):
+    """Filtered path, the other way round: every 16th key (the sampled ones) scores low
+    and the rest high, so each row's threshold lies below almost every key and its
+    candidate lists overflow (more than 512 per half-wave list at d = 128, where the
+    scan kernel appends them; more than 1024 per row list at d = 96, where the tile
+    GEMM does): every row is recomputed by the fallback kernels."""
+    w = wl.WORKLOADS["c4"].scaled(B=1, H=1, Lq=1100, Lk=4000, d=d, causal=False, chunk=512)
+    assert tk.attn_path(w.B, w.H, w.Lq, w.Lk, w.d, w.k, w.chunk, w.causal, tk.TOPK_BF16) == 4
+    alpha = np.where(np.arange(w.Lk) % 16 == 0, 3.0, 10.0)
+    _say("filter overflow", w)
+    x = _planted(w, alpha, 11)
+    out, idx, _ = parity.run_attn(w, x)
+    assert tk.last_fallback_rows() == w.Lq
+    parity.check_attn(w, x, out, idx)
+
+
 def test_tile_long_row_fallback():
     """Rows over 8192 keys: 30 of the 1024 sampled keys score high, the rest of the
     sample lowest; the threshold (24th sampled key) keeps 24 < k keys, and the row is
