@@ -604,13 +604,31 @@ __device__ void wg_row_select(const float* row, int64_t nv, uint32_t k_eff, int6
       cand[s] = e < nv ? make_key(row[e], (uint32_t)e) : 0ull;
     }
     __syncthreads();
-    team_sort_desc<256>(cand, TS_SAMPLE);
     // expected sampled keys among the row's top k_eff: mu = k_eff * TS_SAMPLE / nv;
     // R = mu + 6 sqrt(mu) + 8 keeps P(sample rank R below the k-th key) negligible
     const float mu = (float)k_eff * (float)TS_SAMPLE / (float)nv;
     int R = (int)ceilf(mu + 6.0f * sqrtf(mu) + 8.0f);
     R = R < TS_SAMPLE ? R : TS_SAMPLE;
-    ts = key_score(cand[R - 1]);
+    if (tid < 64) {
+      // one wave: the R-th largest sampled score, built bit by bit on the scores'
+      // order-preserving keys (a bit stays when at least R samples are at or above the
+      // prefix with it set; a missing sample's key is 0, below every score)
+      constexpr int E = TS_SAMPLE / 64;
+      uint32_t u[E];
+#pragma unroll
+      for (int e = 0; e < E; ++e) u[e] = (uint32_t)(cand[lane + 64 * e] >> 32);
+      uint32_t prefix = 0;
+      for (int b = 31; b >= 0; --b) {
+        const uint32_t c = prefix | (1u << b);
+        uint32_t cnt = 0;
+#pragma unroll
+        for (int e = 0; e < E; ++e) cnt += (uint32_t)__popcll(__ballot(u[e] >= c));
+        if (cnt >= (uint32_t)R) prefix = c;
+      }
+      if (lane == 0) misc[0] = prefix;
+    }
+    __syncthreads();
+    ts = ord_to_f32(misc[0]);
     __syncthreads();
   }
   if (tid == 0) *ccount = 0;
