@@ -768,9 +768,12 @@ __global__ __launch_bounds__(256, D == 64 ? (CAUSAL ? ScanShape<G>::OCC_CAUSAL :
             half = lane >> 5, n = lane & 31;
   // XCD-aware order: the hardware deals workgroups round-robin over the 8 XCDs;
   // renumber so each XCD runs consecutive logical workgroups (same head) and K
-  // stays in that XCD's L2.
+  // stays in that XCD's L2. Under the causal mask a workgroup's key tiles grow with
+  // its queries' position, so the logical order is reversed: the longest workgroups
+  // start first and the last to start are the shortest.
   const int64_t NG = gridDim.x, bid = blockIdx.x;
-  const int64_t wg = (NG % 8 == 0) ? (bid % 8) * (NG / 8) + bid / 8 : bid;
+  int64_t wg = (NG % 8 == 0) ? (bid % 8) * (NG / 8) + bid / 8 : bid;
+  if (CAUSAL) wg = NG - 1 - wg;
   const int64_t cl = wg / a.wgs_per_chunk, blk = wg - cl * a.wgs_per_chunk;
   const int64_t id = a.c0 + cl, bh = id / a.nchunk, c = id - bh * a.nchunk;
   const uint16_t* Kh = a.K + bh * a.kv_head_stride;
