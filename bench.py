@@ -159,9 +159,10 @@ def cpu_baseline(w, x, budget_s: float):
 def bench_backward(args, w, x, dev_tensor):
     """Time the backward pass of one workload: the forward runs once in debug mode to
     produce its cache (selected keys, their raw scores); each timed step is one
-    backward call. Roofline: the gathered rows (4 rows of d elements per selected
-    (query, key) pair: V and K per query, d_out and Q per key) plus the cache read
-    and the three gradients written, against the HBM peak."""
+    backward call. Roofline: the bytes the call must move at least once (Q, d_out, K,
+    V and the cache read, the three gradients written) against the HBM peak; beside it
+    the gathered rows (4 rows of d elements per selected (query, key) pair: V and K per
+    query, d_out and Q per key), which L2 and MALL mostly serve."""
     import torch
     import paper_2106_06899_amd as tk
     from paper_2106_06899_amd import workloads as wl
