@@ -1570,11 +1570,19 @@ __global__ __launch_bounds__(256) void k_filter_threshold(Problem pb, Pass ps, P
       const int top = kmin == kmax ? 0 : 32 - __builtin_clz(kmin ^ kmax);
       uint32_t prefix = top >= 32 ? 0u : (kmax >> top) << top;
       const int stop = top > THRESH_BITS ? top - THRESH_BITS : 0;
+      // the search runs over each lane's two largest samples (all of them for E = 2):
+      // the R-th largest of that subset is at most the R-th largest sample (k <= 512
+      // and one sample in 16 keep R near 60 at most, within the subset's 128)
+      uint32_t t1 = 0u, t2 = 0u;
+#pragma unroll
+      for (int e = 0; e < E; ++e) {
+        const uint32_t hi = max(t1, u[e]), lo = min(t1, u[e]);
+        t1 = hi;
+        t2 = max(t2, lo);
+      }
       for (int b = top - 1; b >= stop; --b) {
         const uint32_t cand = prefix | (1u << b);
-        uint32_t cnt = 0;
-#pragma unroll
-        for (int e = 0; e < E; ++e) cnt += (uint32_t)__popcll(__ballot(u[e] >= cand));
+        const uint32_t cnt = (uint32_t)__popcll(__ballot(t1 >= cand)) + (uint32_t)__popcll(__ballot(t2 >= cand));
         if (cnt >= (uint32_t)R) prefix = cand;
       }
       uint32_t m = 0xFFFFFFFFu;  // the smallest sample at or above the prefix
