@@ -1520,6 +1520,18 @@ __global__ __launch_bounds__(64) void k_cand_select(Problem pb, Pass ps, PassBuf
 // are then at or above it; a row with fewer than R valid samples keeps every valid key. The
 // candidate select proves each row's set complete (at least k_eff entries, no
 // overflow) or sends the row to the exact fallback.
+// The rank R of a row's threshold among its ns valid samples (nv valid keys): mu =
+// k_eff * ns / nv is the sample's expected share of the row's top k_eff, and R = mu +
+// z sqrt(mu) + z puts the k-th score below the threshold about z standard deviations
+// away. A row that misses is recomputed exactly, at a cost of nv * d products: where
+// that is small (at most 2^21) z = 3 (about one row in 10^4 recomputed, fewer
+// candidates for all the others), else z = 4.
+__device__ __forceinline__ int filter_rank(uint32_t k_eff, int64_t ns, int64_t nv, int64_t d) {
+  const float mu = (float)k_eff * (float)ns / (float)nv;
+  const float z = nv * d <= (int64_t(1) << 21) ? 3.0f : 4.0f;
+  return (int)ceilf(mu + z * sqrtf(mu) + z);
+}
+
 // One wave per row, four rows per workgroup. The R-th largest sample is built bit by
 // bit, high to low, on the samples' order-preserving 32-bit keys: a bit is kept when at
 // least R samples are at or above the prefix with it set (one ballot per register of
@@ -1536,8 +1548,7 @@ __global__ __launch_bounds__(256) void k_filter_threshold(Problem pb, Pass ps, P
   const int64_t nv = valid_keys(pb, rr.i);
   const int64_t ns = (nv + FILTER_KSTRIDE - 1) / FILTER_KSTRIDE;  // valid samples (<= 64 * CAND_REGS)
   const uint32_t k_eff = (uint32_t)(pb.k < nv ? pb.k : nv);
-  const float mu = (float)k_eff * (float)ns / (float)nv;
-  const int R = (int)ceilf(mu + 4.0f * sqrtf(mu) + 4.0f);
+  const int R = filter_rank(k_eff, ns, nv, pb.d);
   float ts = -INFINITY;
   if (R < ns) {
     const float* row = bufs.samp + p * ((pb.Lk + FILTER_KSTRIDE - 1) / FILTER_KSTRIDE);
@@ -1611,8 +1622,7 @@ __global__ __launch_bounds__(256) void k_filter_threshold_wg(Problem pb, Pass ps
   const int64_t nv = valid_keys(pb, rr.i);
   const int64_t ns = (nv + FILTER_KSTRIDE - 1) / FILTER_KSTRIDE;
   const uint32_t k_eff = (uint32_t)(pb.k < nv ? pb.k : nv);
-  const float mu = (float)k_eff * (float)ns / (float)nv;
-  const int R = (int)ceilf(mu + 4.0f * sqrtf(mu) + 4.0f);
+  const int R = filter_rank(k_eff, ns, nv, pb.d);
   float ts = -INFINITY;
   if (R < ns) {
     const float* row = bufs.samp + p * ((pb.Lk + FILTER_KSTRIDE - 1) / FILTER_KSTRIDE);
