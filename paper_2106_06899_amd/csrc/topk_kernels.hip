@@ -1488,8 +1488,13 @@ __device__ __forceinline__ void cand_select_row(const Problem& pb, const Pass& p
   const uint64_t* b0 = bufs.cand + (2 * p) * bufs.caph;
   uint64_t* out = bufs.sel + p * pb.k;
   if (!BIG) {
+    // registers sized to the list in steps of 64 keys
     if (n <= 128) cand_select_regs<2>(b0, b0 + bufs.caph, (int)c0, n, k_eff, pb.k, sbuf, hist, out);
+    else if (n <= 192) cand_select_regs<3>(b0, b0 + bufs.caph, (int)c0, n, k_eff, pb.k, sbuf, hist, out);
     else if (n <= 256) cand_select_regs<4>(b0, b0 + bufs.caph, (int)c0, n, k_eff, pb.k, sbuf, hist, out);
+    else if (n <= 320) cand_select_regs<5>(b0, b0 + bufs.caph, (int)c0, n, k_eff, pb.k, sbuf, hist, out);
+    else if (n <= 384) cand_select_regs<6>(b0, b0 + bufs.caph, (int)c0, n, k_eff, pb.k, sbuf, hist, out);
+    else if (n <= 448) cand_select_regs<7>(b0, b0 + bufs.caph, (int)c0, n, k_eff, pb.k, sbuf, hist, out);
     else if (n <= 512) cand_select_regs<8>(b0, b0 + bufs.caph, (int)c0, n, k_eff, pb.k, sbuf, hist, out);
     else {
       // rare long lists: the exact select over the words where they are (global
