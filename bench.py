@@ -33,12 +33,17 @@ SCAN_END = "// -----------------------------------------------------------------
 
 def scan_source_digest() -> str:
     """Digest of the scan kernel's own source (its section of topk_kernels.hip: the
-    argument block, launch shape and kernel): counter readings stay valid while it
-    is unchanged."""
+    argument block, launch shape and kernel), with line comments and blank lines left
+    out: counter readings stay valid while its code is unchanged."""
     with open(os.path.join(CSRC, "topk_kernels.hip")) as f:
         text = f.read()
     a, b = text.index(SCAN_BEGIN), text.index(SCAN_END)
-    return hashlib.sha256(text[a:b].encode()).hexdigest()[:16]
+    code = []
+    for line in text[a:b].splitlines():
+        line = line.split("//", 1)[0].rstrip()
+        if line:
+            code.append(line)
+    return hashlib.sha256("\n".join(code).encode()).hexdigest()[:16]
 
 
 def traffic_for_current_kernel(workload: str, path: int):

@@ -1096,8 +1096,8 @@ __global__ __launch_bounds__(256, D == 64 ? (CAUSAL ? ScanShape<G>::OCC_CAUSAL :
     }
     rtail += n1 + n2;
   };
-  // DIRECT: the lane's passing scores of one 16-score lane block, as bits (highest
-  // first, m = 2m + pass: an add with the comparison as carry-in); the 16 scores go to
+  // DIRECT: the lane's passing scores of one 16-score lane block, as bits (built
+  // highest first, m = 2m + pass); the 16 scores go to
   // the wave's stash in LDS (score v of the lane at float v * 64 + lane, full-width
   // writes), and the lane walks its bits, reading each passing score back by its index
   // from its own bank and appending it to its list. A wave reads only what its own
