@@ -77,6 +77,9 @@ ATTN_CASES = {
     "filter_causal_d128_k128": ("c4", dict(B=1, H=2, Lq=3000, Lk=3000, chunk=512)),
     "filter_d96_k200": ("c2", dict(B=1, H=1, Lq=300, Lk=12000, d=96, k=200, chunk=128)),
     "filter_d32_k7_ragged": ("c2", dict(B=2, H=1, Lq=333, Lk=2601, d=32, k=7, chunk=100)),
+    # the filtered path's scan at d = 128 with k > 256 (two 1024-word lists per row, the
+    # larger select) under the causal mask: early rows keep every key (k_eff < k)
+    "filter_causal_d128_k300": ("c4", dict(B=1, H=1, Lq=5000, Lk=5000, k=300, chunk=1000)),
 }
 
 
