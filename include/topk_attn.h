@@ -215,9 +215,10 @@ const char* topk_last_error(void);
  * (causal masks on the fused path: the first 1024 R rows of every head, whose few
  * valid keys give the fused threshold sample too few blocks, run on the chunk-tile
  * path; R = 3, 6, 12 for k <= 32, 64, 128), 4 = filtered chunk-tile path (bf16,
- * d % 32 == 0, k <= 256, 2048 < Lk <= 16384: every 16th key is scored first, each
- * row's threshold comes from those samples, and the tile GEMM keeps only the scores
- * at or above it; the rest as the fused path), or a negative status for invalid
+ * d % 32 == 0, k <= 512, 2048 < Lk <= 65536: every 16th key is scored first, each
+ * row's threshold comes from those samples, and only the scores reaching it are kept
+ * as candidates, by the fused path's score kernel at d = 128 and by the chunk-tile
+ * GEMM otherwise; the rest as the fused path), or a negative status for invalid
  * arguments. For tests and reports.
  */
 int topk_attn_path(int64_t B, int64_t H, int64_t Lq, int64_t Lk, int64_t d,
@@ -229,7 +230,7 @@ int topk_ffn_path(int64_t N, int64_t d_model, int64_t d_ff, int64_t k,
  * Stage timing, for benchmarks. After topk_profile_begin(), every call made on
  * the calling thread records a pair of HIP events on its own stream around each
  * launch group: stage 0 = score tiles (fused scan, or chunk-tile scores),
- * 1 = row select, 2 = fallback recomputation (fused path only), 3 = activation
+ * 1 = row select, 2 = fallback recomputation (fused and filtered paths), 3 = activation
  * and gather, 4 = a backward call. topk_profile_end() waits for those events, writes the summed
  * milliseconds and the number of timed launches of the first n_stages stages
  * into stage_ms / stage_launches (host arrays, either may be NULL) and stops

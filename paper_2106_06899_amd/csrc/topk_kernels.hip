@@ -1537,12 +1537,12 @@ __device__ __forceinline__ int filter_rank(uint32_t k_eff, int64_t ns, int64_t n
   return (int)ceilf(mu + z * sqrtf(mu) + z);
 }
 
-// One wave per row, four rows per workgroup. The R-th largest sample is built bit by
-// bit, high to low, on the samples' order-preserving 32-bit keys: a bit is kept when at
-// least R samples are at or above the prefix with it set (one ballot per register of
-// samples, no LDS). Starting below the bits every sample shares, THRESH_BITS bits are
-// resolved; the threshold is then the smallest sample at or above the prefix, which is
-// at most the R-th largest.
+// One wave per row, four rows per workgroup. Each lane keeps the two largest of its
+// samples; the R-th largest of those 128 is built bit by bit, high to low, on their
+// order-preserving 32-bit keys: a bit is kept when at least R of them are at or above
+// the prefix with it set (two ballots per bit, no LDS). Starting below the bits every
+// sample shares, THRESH_BITS bits are resolved; the threshold is then the smallest
+// sample at or above the prefix, which is at most the R-th largest sample.
 constexpr int THRESH_BITS = 16;
 __global__ __launch_bounds__(256) void k_filter_threshold(Problem pb, Pass ps, PassBufs bufs) {
   const int64_t p = (int64_t)blockIdx.x * 4 + __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);  // uniform
