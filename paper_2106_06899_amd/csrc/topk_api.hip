@@ -188,7 +188,8 @@ void plan_sizes(const Problem& pb, Plan* pl, size_t budget) {
   pl->nchunk = (pb.q1 - pb.q0 + pb.C - 1) / pb.C;
   pl->total_chunks = pb.BH * pl->nchunk;
   pl->per_chunk = row_bytes(pb, *pl) * (size_t)pb.C + 6 * ALIGN;
-  pl->fixed = 2 * ALIGN + (pl->path != PATH_TILE ? up((size_t)(REDO_CAP + REDO_BLOCKS) * pb.Lk * 4) : 0);
+  pl->fixed = 2 * ALIGN + (pl->path != PATH_TILE ? up((size_t)(REDO_CAP + REDO_BLOCKS) * pb.Lk * 4) : 0) +
+              (pl->path == PATH_FILTER ? FILTER_SAMP_PAD : 0);
   int64_t n = 1;
   if (budget > pl->fixed + pl->per_chunk) n = (int64_t)((budget - pl->fixed) / pl->per_chunk);
   if (n > pl->total_chunks) n = pl->total_chunks;
@@ -233,7 +234,7 @@ PassBufs carve(const Problem& pb, const Plan& pl, char* ws) {
     b.cand_single = pl.path == PATH_FILTER && filter_scan_ok(pb) ? 0 : 1;
     if (pl.path == PATH_FILTER) {
       b.samp = (float*)(ws + off);
-      off += up(rows * (size_t)((pb.Lk + FILTER_KSTRIDE - 1) / FILTER_KSTRIDE) * 4);
+      off += up(rows * (size_t)((pb.Lk + FILTER_KSTRIDE - 1) / FILTER_KSTRIDE) * 4 + FILTER_SAMP_PAD);
       b.thr = (float*)(ws + off);
       off += up(rows * 4);
     }

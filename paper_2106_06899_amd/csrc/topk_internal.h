@@ -53,6 +53,9 @@ struct Pass {
 // scores at or above it.
 constexpr int FILTER_KSTRIDE = 16;
 constexpr int64_t FILTER_MAX_LK = 65536;  // at most 4096 samples per row
+// Bytes of padding after the sample buffer: the per-row threshold kernel loads up to
+// 1024 samples from a row's start whatever the row's length, and discards the rest.
+constexpr size_t FILTER_SAMP_PAD = 4096;
 
 // The filtered path scores its candidates with the scan kernel (direct mode, one
 // candidate list per row and half-wave) for bf16 keys of d = 128; with the MFMA tile

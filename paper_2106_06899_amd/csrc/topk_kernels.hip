@@ -1249,6 +1249,21 @@ __device__ __forceinline__ uint32_t xor_lane_u32(uint32_t x, int m) {
 __device__ __forceinline__ uint64_t xor_lane_u64(uint64_t x, int m) {
   return ((uint64_t)xor_lane_u32((uint32_t)(x >> 32), m) << 32) | xor_lane_u32((uint32_t)x, m);
 }
+// The minimum or maximum of x over a wave whose lanes are all active, as a
+// wave-uniform value: two DPP quad permutations and the half-row and row mirrors
+// leave every row of 16 lanes holding its row's extreme, and the four rows' values
+// are read into scalar registers (no LDS traffic, unlike a shuffle).
+template <bool MAX>
+__device__ __forceinline__ uint32_t wave_extreme_u32_full(uint32_t x) {
+  auto op = [](uint32_t u, uint32_t v) { return MAX ? max(u, v) : min(u, v); };
+  x = op(x, (uint32_t)__builtin_amdgcn_mov_dpp((int)x, 0xB1, 0xF, 0xF, false));   // quad [1,0,3,2]
+  x = op(x, (uint32_t)__builtin_amdgcn_mov_dpp((int)x, 0x4E, 0xF, 0xF, false));   // quad [2,3,0,1]
+  x = op(x, (uint32_t)__builtin_amdgcn_mov_dpp((int)x, 0x141, 0xF, 0xF, false));  // row_half_mirror
+  x = op(x, (uint32_t)__builtin_amdgcn_mov_dpp((int)x, 0x140, 0xF, 0xF, false));  // row_mirror
+  const uint32_t r0 = (uint32_t)__builtin_amdgcn_readlane((int)x, 0), r1 = (uint32_t)__builtin_amdgcn_readlane((int)x, 16);
+  const uint32_t r2 = (uint32_t)__builtin_amdgcn_readlane((int)x, 32), r3 = (uint32_t)__builtin_amdgcn_readlane((int)x, 48);
+  return op(op(r0, r1), op(r2, r3));
+}
 // Inclusive prefix sum over the 64 lanes of a wave whose lanes are all active, by
 // DPP: row shifts 1, 2, 4, 8 scan each row of 16 lanes, then the broadcasts of lane
 // 15 (into rows 1 and 3) and lane 31 (into rows 2 and 3) carry the row totals.
@@ -1538,12 +1553,18 @@ __device__ __forceinline__ int filter_rank(uint32_t k_eff, int64_t ns, int64_t n
 }
 
 // One wave per row, four rows per workgroup. Each lane keeps the two largest of its
-// samples; the R-th largest of those 128 is built bit by bit, high to low, on their
+// samples (a running maximum and median of three, on the scores themselves); the
+// R-th largest of those 128 is built bit by bit, high to low, on their
 // order-preserving 32-bit keys: a bit is kept when at least R of them are at or above
-// the prefix with it set (two ballots per bit, no LDS). Starting below the bits every
-// sample shares, THRESH_BITS bits are resolved; the threshold is then the smallest
-// sample at or above the prefix, which is at most the R-th largest sample.
+// the prefix with it set (two ballots per bit, no LDS). Starting below the bits that
+// the largest and the smallest of the 128 share, THRESH_BITS bits are resolved; the
+// threshold is then the smallest of the 128 at or above the prefix, which is at most
+// their R-th largest and so at most the R-th largest sample. The kernel is bound by
+// its vector instructions: per sample it spends a range test, a select, a maximum and
+// a median, and the row's sample loads run past its end (into the next rows, or the
+// padding that ends the sample buffer) instead of being clamped.
 constexpr int THRESH_BITS = 16;
+static_assert(64 * CAND_REGS * sizeof(float) <= FILTER_SAMP_PAD, "a row's loads stay within the padded buffer");
 __global__ __launch_bounds__(256) void k_filter_threshold(Problem pb, Pass ps, PassBufs bufs) {
   const int64_t p = (int64_t)blockIdx.x * 4 + __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);  // uniform
   if (p >= ps.nc * pb.C) return;
@@ -1557,56 +1578,37 @@ __global__ __launch_bounds__(256) void k_filter_threshold(Problem pb, Pass ps, P
   float ts = -INFINITY;
   if (R < ns) {
     const float* row = bufs.samp + p * ((pb.Lk + FILTER_KSTRIDE - 1) / FILTER_KSTRIDE);
+    const int nsi = (int)ns;
     auto rth = [&](auto tag) {  // the R-th largest of the row's ns samples, or a little less
       constexpr int E = decltype(tag)::value;
-      uint32_t u[E];  // order-preserving keys; 0 (below every score's key) past the samples
-      uint32_t kmin = 0xFFFFFFFFu, kmax = 0u;
+      float x[E];
 #pragma unroll
-      for (int e = 0; e < E; ++e) {  // every load in flight at once (slots past ns read sample 0)
-        const int64_t s = lane + 64 * e;
-        u[e] = ord_u32(row[s < ns ? s : 0]);
-      }
+      for (int e = 0; e < E; ++e) x[e] = row[lane + 64 * e];  // every load in flight at once
+      // this lane's two largest samples, t1 >= t2 (-inf where it has fewer)
+      float t1 = -INFINITY, t2 = -INFINITY;
 #pragma unroll
       for (int e = 0; e < E; ++e) {
-        if (lane + 64 * e < ns) {
-          kmin = min(kmin, u[e]);
-          kmax = max(kmax, u[e]);
-        } else {
-          u[e] = 0u;
-        }
+        const float v = lane + 64 * e < nsi ? x[e] : -INFINITY;
+        t2 = __builtin_amdgcn_fmed3f(t1, t2, v);
+        t1 = __builtin_elementwise_maximum(t1, v);
       }
-#pragma unroll
-      for (int off = 32; off > 0; off >>= 1) {
-        kmin = min(kmin, (uint32_t)__shfl_xor(kmin, off, 64));
-        kmax = max(kmax, (uint32_t)__shfl_xor(kmax, off, 64));
-      }
-      kmin = (uint32_t)__builtin_amdgcn_readfirstlane(kmin);
-      kmax = (uint32_t)__builtin_amdgcn_readfirstlane(kmax);
-      // bits [0, top) differ among the samples; the ones above are every sample's
+      const uint32_t u1 = ord_u32(t1), u2 = ord_u32(t2);
+      // the smallest of the 128 that is a sample (t2 is one wherever ns > 128)
+      const uint32_t lo = t2 != -INFINITY ? u2 : t1 != -INFINITY ? u1 : 0xFFFFFFFFu;
+      const uint32_t kmin = wave_extreme_u32_full<false>(lo), kmax = wave_extreme_u32_full<true>(u1);
+      // bits [0, top) differ among them; the ones above are shared by all, so also by
+      // their R-th largest
       const int top = kmin == kmax ? 0 : 32 - __builtin_clz(kmin ^ kmax);
       uint32_t prefix = top >= 32 ? 0u : (kmax >> top) << top;
       const int stop = top > THRESH_BITS ? top - THRESH_BITS : 0;
-      // the search runs over each lane's two largest samples (all of them for E = 2):
-      // the R-th largest of that subset is at most the R-th largest sample (k <= 512
-      // and one sample in 16 keep R near 60 at most, within the subset's 128)
-      uint32_t t1 = 0u, t2 = 0u;
-#pragma unroll
-      for (int e = 0; e < E; ++e) {
-        const uint32_t hi = max(t1, u[e]), lo = min(t1, u[e]);
-        t1 = hi;
-        t2 = max(t2, lo);
-      }
+      // (k <= 512 and one sample in 16 keep R near 60 at most, within the 128)
       for (int b = top - 1; b >= stop; --b) {
         const uint32_t cand = prefix | (1u << b);
-        const uint32_t cnt = (uint32_t)__popcll(__ballot(t1 >= cand)) + (uint32_t)__popcll(__ballot(t2 >= cand));
+        const uint32_t cnt = (uint32_t)__popcll(__ballot(u1 >= cand)) + (uint32_t)__popcll(__ballot(u2 >= cand));
         if (cnt >= (uint32_t)R) prefix = cand;
       }
-      uint32_t m = 0xFFFFFFFFu;  // the smallest sample at or above the prefix
-#pragma unroll
-      for (int e = 0; e < E; ++e)
-        if (lane + 64 * e < ns && u[e] >= prefix) m = min(m, u[e]);
-      for (int off = 32; off > 0; off >>= 1) m = min(m, (uint32_t)__shfl_xor(m, off, 64));
-      return ord_to_f32(m);
+      const uint32_t m = min(u1 >= prefix ? u1 : 0xFFFFFFFFu, u2 >= prefix ? u2 : 0xFFFFFFFFu);
+      return ord_to_f32(wave_extreme_u32_full<false>(m));
     };
     if (ns <= 128) ts = rth(std::integral_constant<int, 2>{});
     else if (ns <= 256) ts = rth(std::integral_constant<int, 4>{});
@@ -1742,8 +1744,7 @@ __global__ __launch_bounds__(64) void k_tile_select_wave(Problem pb, Pass ps, co
 #pragma unroll
       for (int e = 0; e < 2; ++e)
         if ((k2[e] >> shift) >= (prefix >> shift)) m = min(m, (uint32_t)(k2[e] >> 32));
-      for (int off = 32; off > 0; off >>= 1) m = min(m, (uint32_t)__shfl_xor(m, off, 64));
-      ts = ord_to_f32(m);
+      ts = ord_to_f32(wave_extreme_u32_full<false>(m));
     } else {
       uint64_t key[CAND_REGS];
 #pragma unroll
@@ -1753,8 +1754,7 @@ __global__ __launch_bounds__(64) void k_tile_select_wave(Problem pb, Pass ps, co
 #pragma unroll
       for (int e = 0; e < CAND_REGS; ++e)
         if ((key[e] >> shift) >= (prefix >> shift)) m = min(m, (uint32_t)(key[e] >> 32));
-      for (int off = 32; off > 0; off >>= 1) m = min(m, (uint32_t)__shfl_xor(m, off, 64));
-      ts = ord_to_f32(m);
+      ts = ord_to_f32(wave_extreme_u32_full<false>(m));
     }
   }
   // gather (wave-level compaction; c is wave-uniform)
