@@ -942,13 +942,13 @@ __global__ __launch_bounds__(256, D == 64 ? (CAUSAL ? ScanShape<G>::OCC_CAUSAL :
     for (int g = 0; g < G; ++g)
 #pragma unroll
       for (int r = 0; r < R; ++r) top[g][r] = -INFINITY;
+    // sorted insert, descending: entry r becomes the median of the old entries r - 1
+    // and r and the new value (entry 0 the larger of it and the value), so the R
+    // updates do not wait on each other (a chain of maxima and minima would)
     auto insert = [&](float (&tp)[R], float m) {
 #pragma unroll
-      for (int r = 0; r < R; ++r) {  // sorted insert, descending
-        const float hi = fmaxf(tp[r], m);
-        m = fminf(tp[r], m);
-        tp[r] = hi;
-      }
+      for (int r = R - 1; r > 0; --r) tp[r] = __builtin_amdgcn_fmed3f(tp[r - 1], tp[r], m);
+      tp[0] = __builtin_elementwise_maximum(tp[0], m);
     };
     const int64_t ns = (ntiles + a.stride - 1) / a.stride;
     pipeline(ns, a.stride, [&](int64_t t, const unsigned char* kb) {
