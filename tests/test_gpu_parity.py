@@ -80,6 +80,10 @@ ATTN_CASES = {
     # the filtered path's scan at d = 128 with k > 256 (two 1024-word lists per row, the
     # larger select) under the causal mask: early rows keep every key (k_eff < k)
     "filter_causal_d128_k300": ("c4", dict(B=1, H=1, Lq=5000, Lk=5000, k=300, chunk=1000)),
+    # a handful of rows of 563 samples each: the threshold kernel's loads (1024 samples
+    # from each row's start) run past the last row into the padding after the samples
+    "filter_d96_few_rows": ("c2", dict(B=1, H=1, Lq=3, Lk=9000, d=96, k=200, chunk=3)),
+    "filter_d128_few_rows": ("c4", dict(B=1, H=1, Lq=2, Lk=9000, k=200, causal=False, chunk=2)),
 }
 
 
